@@ -1,0 +1,222 @@
+"""CPU oracle for the skew-symmetric LTL^T factorization and its Pfaffian.
+
+TEST INFRASTRUCTURE ONLY: only ``tests/``, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import this package.  The GPU library
+never links, imports or calls it, and it shares no code with the GPU library.
+
+What it computes (textbook definitions, written out plainly):
+
+* ``ltlt`` -- Parlett & Reid's unblocked reduction of a skew-symmetric X to
+  tridiagonal form with partial pivoting, P X P^T = L T L^T, in scalar C
+  (``ltlt_oracle_body.h``): one column step at a time, pivot = first index of
+  the largest magnitude, exchange, multipliers, skew rank-2 update of the
+  trailing strict lower triangle.
+* ``pfaffian`` -- Pf(X) = det(P) * prod_j T(2j, 2j+1), returned as
+  (log|Pf|, sign), from Pf(B X B^T) = det(B) Pf(X).
+* ``skew_update`` -- the definition of one trailing-matrix block update of
+  the blocked method: new(i, c) = S(perm[i], perm[c]) + (Lx @ B^T)(i, c) on
+  the strict lower triangle, with the mirrored upper entry, via one numpy
+  matrix product.
+* ``unpack`` -- reads L, the tridiagonal T and P back out of the packed
+  output, for the residual P X P^T - L T L^T.
+
+Every floating-point routine runs in the precision of its input (fp64, or fp32
+for fp32 parity); the Pfaffian accumulates in fp64.
+
+Pins (tests that tie these functions to facts outside themselves) live in
+``tests/test_oracle_pins.py``; no function here is unpinned.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "ltlt_oracle.c")
+_HDR = os.path.join(_HERE, "ltlt_oracle_body.h")
+_LIB = os.path.join(_HERE, "libltlt_oracle.so")
+_lock = threading.Lock()
+_lib = None
+
+GCC_FLAGS = ["-O2", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared", "-std=c99"]
+
+
+def build(force: bool = False) -> str:
+    """Compile the C oracle with gcc (no FMA contraction, no reassociation)."""
+    stale = (not os.path.exists(_LIB)
+             or os.path.getmtime(_LIB) < max(os.path.getmtime(_SRC), os.path.getmtime(_HDR)))
+    if force or stale:
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", *GCC_FLAGS, _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(_LIB):
+                build()
+            lib = ctypes.CDLL(_LIB)
+            i64, p = ctypes.c_int64, ctypes.c_void_p
+            for name in ("oracle_ltlt_f64", "oracle_ltlt_f32"):
+                getattr(lib, name).argtypes = [i64, p, i64, p, i64]
+                getattr(lib, name).restype = None
+            lib.oracle_swap_f64.argtypes = [i64, p, i64, i64, i64]
+            lib.oracle_swap_f64.restype = None
+            for name in ("oracle_pfaffian_f64", "oracle_pfaffian_f32"):
+                getattr(lib, name).argtypes = [i64, p, i64, p, p, p]
+                getattr(lib, name).restype = None
+            for name in ("oracle_ltlt_batched_f64", "oracle_ltlt_batched_f32"):
+                getattr(lib, name).argtypes = [i64, i64, p, i64, i64, p, i64, p, p]
+                getattr(lib, name).restype = None
+            _lib = lib
+    return _lib
+
+
+def _sfx(dtype) -> str:
+    dt = np.dtype(dtype)
+    if dt == np.float64:
+        return "f64"
+    if dt == np.float32:
+        return "f32"
+    raise TypeError("oracle supports float64 and float32 only")
+
+
+def ltlt_colmajor(buf: np.ndarray, n: int, nsteps: int = -1):
+    """Factor in place.  ``buf`` is a C-ordered (n, lda) array holding the
+    column-major matrix (``buf[c, i]`` = element (i, c)); only its strict
+    lower triangle (in column-major terms) is read or written.
+    Returns the int32 pivot vector (0-based, LAPACK laswp order)."""
+    lib = _load()
+    if not (buf.flags.c_contiguous and buf.ndim == 2 and buf.shape[0] >= n):
+        raise ValueError("buf must be a C-contiguous (n, lda) array")
+    lda = buf.shape[1]
+    ipiv = np.zeros(max(n, 1), dtype=np.int32)
+    fn = getattr(lib, "oracle_ltlt_" + _sfx(buf.dtype))
+    fn(n, buf.ctypes.data, lda, ipiv.ctypes.data, int(nsteps))
+    return ipiv[:n]
+
+
+def ltlt(X: np.ndarray, nsteps: int = -1):
+    """Factor the skew matrix ``X`` (n x n, C order, X[i, j] = row i col j).
+
+    Returns ``(packed, ipiv)`` where ``packed`` is an n x n array (row/col
+    indexing) whose strict lower triangle holds alpha_k at (k+1, k) and
+    L(r, k+1) at (r, k) for r >= k+2; its other entries are zero.
+    """
+    n = X.shape[0]
+    buf = np.ascontiguousarray(X.T)          # column-major image of X
+    ipiv = ltlt_colmajor(buf, n, nsteps)
+    packed = np.tril(buf.T, -1)
+    return np.ascontiguousarray(packed), ipiv
+
+
+def pfaffian_packed(packed: np.ndarray, ipiv: np.ndarray):
+    """(log|Pf(X)|, sign) from the packed factors (row/col indexed n x n)."""
+    lib = _load()
+    n = packed.shape[0]
+    buf = np.ascontiguousarray(packed.T)     # column-major image
+    logabs = ctypes.c_double(0.0)
+    sign = ctypes.c_int32(0)
+    ip = np.ascontiguousarray(ipiv, dtype=np.int32)
+    fn = getattr(lib, "oracle_pfaffian_" + _sfx(packed.dtype))
+    fn(n, buf.ctypes.data, n, ip.ctypes.data, ctypes.byref(logabs), ctypes.byref(sign))
+    return float(logabs.value), int(sign.value)
+
+
+def pfaffian(X: np.ndarray):
+    """(log|Pf(X)|, sign) of a skew matrix via the factorization."""
+    packed, ipiv = ltlt(X)
+    return pfaffian_packed(packed, ipiv)
+
+
+def ltlt_batched(Xs: np.ndarray):
+    """Factor a stack of skew matrices ``Xs`` (batch, n, n).
+
+    Returns ``(packed, ipiv, logabs, sign)`` with packed (batch, n, n)."""
+    lib = _load()
+    batch, n, _ = Xs.shape
+    buf = np.ascontiguousarray(np.transpose(Xs, (0, 2, 1)))
+    ipiv = np.zeros((batch, max(n, 1)), dtype=np.int32)
+    logabs = np.zeros(batch, dtype=np.float64)
+    sign = np.zeros(batch, dtype=np.int32)
+    fn = getattr(lib, "oracle_ltlt_batched_" + _sfx(Xs.dtype))
+    fn(n, batch, buf.ctypes.data, n, n * n, ipiv.ctypes.data, ipiv.shape[1],
+       logabs.ctypes.data, sign.ctypes.data)
+    packed = np.tril(np.transpose(buf, (0, 2, 1)), -1)
+    return np.ascontiguousarray(packed), ipiv[:, :n], logabs, sign
+
+
+def swap_indices(X: np.ndarray, r: int, p: int) -> np.ndarray:
+    """Q X Q^T for the transposition (r p), through the oracle's lower-storage
+    exchange; returns the full skew matrix rebuilt from the strict lower part."""
+    lib = _load()
+    n = X.shape[0]
+    buf = np.ascontiguousarray(X.T).astype(np.float64)
+    lib.oracle_swap_f64(n, buf.ctypes.data, n, r, p)
+    low = np.tril(buf.T, -1)
+    return low - low.T
+
+
+def unpack(packed: np.ndarray, ipiv: np.ndarray):
+    """Return (L, T, perm) with P X P^T = L T L^T, P[i, perm[i]] = 1.
+
+    L is unit lower triangular with L[:, 0] = e_0 and L[r, k+1] = packed[r, k]
+    (r >= k+2); T is skew tridiagonal with T[k+1, k] = packed[k+1, k];
+    perm applies the exchanges (i, ipiv[i]) for i = 0 .. n-1 in order to the
+    identity ordering, so (P X P^T)[i, j] = X[perm[i], perm[j]].
+    """
+    n = packed.shape[0]
+    dt = np.float64
+    L = np.eye(n, dtype=dt)
+    T = np.zeros((n, n), dtype=dt)
+    for k in range(n - 1):
+        T[k + 1, k] = packed[k + 1, k]
+        T[k, k + 1] = -packed[k + 1, k]
+    for k in range(max(n - 2, 0)):
+        L[k + 2:, k + 1] = packed[k + 2:, k]
+    perm = np.arange(n)
+    for i in range(n):
+        j = int(ipiv[i])
+        perm[i], perm[j] = perm[j], perm[i]
+    return L, T, perm
+
+
+def residual(X: np.ndarray, packed: np.ndarray, ipiv: np.ndarray) -> float:
+    """||P X P^T - L T L^T||_F / (n * eps * ||X||_F), eps of X's dtype."""
+    n = X.shape[0]
+    if n == 0:
+        return 0.0
+    L, T, perm = unpack(packed.astype(np.float64), ipiv)
+    Xd = X.astype(np.float64)
+    PXP = Xd[np.ix_(perm, perm)]
+    R = PXP - L @ T @ L.T
+    eps = np.finfo(X.dtype).eps
+    nx = np.linalg.norm(Xd)
+    if nx == 0:
+        return float(np.linalg.norm(R))
+    return float(np.linalg.norm(R) / (n * eps * nx))
+
+
+def skew_update(S: np.ndarray, Lx: np.ndarray, B: np.ndarray, perm: np.ndarray) -> np.ndarray:
+    """One trailing-block update of the blocked method, by definition.
+
+    ``S`` is the m x m skew matrix before the block (full storage), ``perm``
+    maps each current index to the index it held before the block's exchanges,
+    ``Lx`` and ``B`` are m x K.  Returns the full skew matrix whose strict
+    lower entries are S[perm[i], perm[c]] + (Lx @ B.T)[i, c] (i > c) and whose
+    upper entries are their negations, diagonal 0.
+    """
+    m = S.shape[0]
+    P = S[np.ix_(perm, perm)]
+    new = P + Lx @ B.T
+    low = np.tril(new, -1)
+    out = low - low.T
+    assert out.shape == (m, m)
+    return out

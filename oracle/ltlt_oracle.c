@@ -1,0 +1,76 @@
+/* CPU oracle for the skew-symmetric LTL^T factorization and the Pfaffian.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is plain, slow, scalar C that follows
+ * the textbook definitions (Parlett & Reid's partially pivoted reduction of a
+ * skew-symmetric matrix to tridiagonal form, and the Pfaffian identity
+ * Pf(B X B^T) = det(B) Pf(X)).  It shares no code, header or constant with
+ * the GPU library; only the tests, the smoke check and the benchmark's CPU
+ * baseline may load it.
+ *
+ * Build: gcc -O2 -ffp-contract=off -fno-fast-math -shared -fPIC
+ * (no contraction into FMA, no reassociation: every operation rounds once,
+ * in the order written).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+
+#define CAT_(a, b) a##b
+#define CAT(a, b) CAT_(a, b)
+#define AT(i, j) A[(int64_t)(i) + (int64_t)(j) * lda]
+
+#define REAL double
+#define SFX _f64
+#define FABS fabs
+#include "ltlt_oracle_body.h"
+#undef REAL
+#undef SFX
+#undef FABS
+
+#define REAL float
+#define SFX _f32
+#define FABS fabsf
+#include "ltlt_oracle_body.h"
+#undef REAL
+#undef SFX
+#undef FABS
+
+/* Exported entry points (ctypes). */
+void oracle_ltlt_f64(int64_t n, double* A, int64_t lda, int32_t* ipiv, int64_t nsteps)
+{ ltlt_f64(n, A, lda, ipiv, nsteps); }
+
+void oracle_ltlt_f32(int64_t n, float* A, int64_t lda, int32_t* ipiv, int64_t nsteps)
+{ ltlt_f32(n, A, lda, ipiv, nsteps); }
+
+void oracle_swap_f64(int64_t n, double* A, int64_t lda, int64_t r, int64_t p)
+{ swap_indices_f64(n, A, lda, r, p); }
+
+void oracle_pfaffian_f64(int64_t n, const double* A, int64_t lda, const int32_t* ipiv,
+                         double* logabs, int32_t* sign)
+{ pfaffian_f64(n, A, lda, ipiv, logabs, sign); }
+
+void oracle_pfaffian_f32(int64_t n, const float* A, int64_t lda, const int32_t* ipiv,
+                         double* logabs, int32_t* sign)
+{ pfaffian_f32(n, A, lda, ipiv, logabs, sign); }
+
+/* Batched: `batch` matrices, matrix b at A + b*strideA, pivots at
+ * ipiv + b*strideIpiv, one after the other. */
+void oracle_ltlt_batched_f64(int64_t n, int64_t batch, double* A, int64_t lda, int64_t strideA,
+                             int32_t* ipiv, int64_t strideIpiv, double* logabs, int32_t* sign)
+{
+    int64_t b;
+    for (b = 0; b < batch; ++b) {
+        ltlt_f64(n, A + b * strideA, lda, ipiv + b * strideIpiv, -1);
+        pfaffian_f64(n, A + b * strideA, lda, ipiv + b * strideIpiv, logabs + b, sign + b);
+    }
+}
+
+void oracle_ltlt_batched_f32(int64_t n, int64_t batch, float* A, int64_t lda, int64_t strideA,
+                             int32_t* ipiv, int64_t strideIpiv, double* logabs, int32_t* sign)
+{
+    int64_t b;
+    for (b = 0; b < batch; ++b) {
+        ltlt_f32(n, A + b * strideA, lda, ipiv + b * strideIpiv, -1);
+        pfaffian_f32(n, A + b * strideA, lda, ipiv + b * strideIpiv, logabs + b, sign + b);
+    }
+}

@@ -1,0 +1,116 @@
+/* Body of the CPU oracle, instantiated once per floating-point type by
+ * ltlt_oracle.c (REAL = double or float, SFX = _f64 or _f32, FABS = fabs or
+ * fabsf).  Test infrastructure only: nothing in the library links this.
+ *
+ * Storage: column-major with leading dimension lda; element (i, j) is
+ * A[i + j*lda].  Only the strict lower triangle is read or written; the
+ * skew-symmetric matrix is X(i,j) = A(i,j) for i > j, X(j,i) = -A(i,j),
+ * X(i,i) = 0.
+ */
+
+/* Swap indices r < p of the skew matrix held in the strict lower triangle,
+ * i.e. replace X by Q X Q^T where Q exchanges rows/columns r and p.
+ * Every stored entry (a, b), a > b, of the new matrix is X(s(a), s(b)) with s
+ * the transposition (r p); read off case by case:
+ *   b <  r          : rows r and p exchange                (a in {r, p})
+ *   b == r, r<a<p   : X(a, p) = -X(p, a)  (upper entry of X read from lower)
+ *   b == r, a == p  : X(r, p) = -X(p, r)
+ *   b == r, a >  p  : X(a, p)
+ *   r<b<p,  a == p  : X(r, b) = -X(b, r)
+ *   b == p, a >  p  : X(a, r)
+ * and nothing else changes. */
+static void CAT(swap_indices, SFX)(int64_t n, REAL* A, int64_t lda, int64_t r, int64_t p)
+{
+    int64_t b, a;
+    REAL t;
+    for (b = 0; b < r; ++b) {               /* rows r and p, columns left of r */
+        t = AT(r, b); AT(r, b) = AT(p, b); AT(p, b) = t;
+    }
+    for (a = r + 1; a < p; ++a) {           /* column r against row p */
+        t = AT(a, r);
+        AT(a, r) = -AT(p, a);
+        AT(p, a) = -t;
+    }
+    AT(p, r) = -AT(p, r);
+    for (a = p + 1; a < n; ++a) {           /* columns r and p below row p */
+        t = AT(a, r); AT(a, r) = AT(a, p); AT(a, p) = t;
+    }
+}
+
+/* Unblocked Parlett-Reid reduction with partial pivoting,
+ * P X P^T = L T L^T, run for `nsteps` column steps (all n-2 steps when
+ * nsteps < 0 or nsteps > n-2).
+ *
+ * Step k (k = 0 .. n-3) eliminates column k below row k+1:
+ *   1. p = first index r >= k+1 maximising |X(r, k)|            (pivot)
+ *   2. ipiv[k+1] = p; exchange indices k+1 and p                 (Q_k)
+ *   3. alpha_k = X(k+1, k); l_r = X(r, k) / alpha_k for r >= k+2
+ *      (l = 0 when alpha_k = 0: the column is already eliminated)
+ *   4. X <- M X M^T with M = I - l e_{k+1}^T, which on the trailing
+ *      strict lower triangle (i > j >= k+2) is the skew rank-2 update
+ *      X(i, j) += l_i v_j - v_i l_j,  v = X(k+2:, k+1)
+ *      (column k+1 itself is unchanged because X(k+1, k+1) = 0).
+ * On exit A(k+1, k) = alpha_k = T(k+1, k) and A(r, k) = l_r = L(r, k+1) for
+ * r >= k+2, with rows of earlier columns carried through later exchanges. */
+static void CAT(ltlt, SFX)(int64_t n, REAL* A, int64_t lda, int32_t* ipiv, int64_t nsteps)
+{
+    int64_t i, j, k, r, p, last;
+    REAL best, alpha;
+    REAL* v;
+
+    for (i = 0; i < n; ++i) ipiv[i] = (int32_t)i;
+    last = n - 2;                                 /* number of column steps */
+    if (nsteps >= 0 && nsteps < last) last = nsteps;
+    if (last <= 0) return;
+    v = (REAL*)malloc((size_t)n * sizeof(REAL));
+    if (!v) return;
+
+    for (k = 0; k < last; ++k) {
+        /* 1. pivot: strict '>' keeps the first of equal magnitudes */
+        p = k + 1;
+        best = FABS(AT(k + 1, k));
+        for (r = k + 2; r < n; ++r) {
+            if (FABS(AT(r, k)) > best) { best = FABS(AT(r, k)); p = r; }
+        }
+        /* 2. exchange */
+        ipiv[k + 1] = (int32_t)p;
+        if (p != k + 1) CAT(swap_indices, SFX)(n, A, lda, k + 1, p);
+        /* 3. multipliers */
+        alpha = AT(k + 1, k);
+        for (r = k + 2; r < n; ++r) AT(r, k) = (alpha != (REAL)0) ? AT(r, k) / alpha : (REAL)0;
+        /* 4. skew rank-2 update of the trailing strict lower triangle */
+        for (r = k + 2; r < n; ++r) v[r] = AT(r, k + 1);
+        for (j = k + 2; j < n; ++j) {
+            REAL lj = AT(j, k), vj = v[j];
+            for (i = j + 1; i < n; ++i) {
+                AT(i, j) = AT(i, j) + (AT(i, k) * vj - v[i] * lj);
+            }
+        }
+    }
+    free(v);
+}
+
+/* Pfaffian from the factors.  Pf(B X B^T) = det(B) Pf(X) gives
+ * Pf(X) = det(P) det(L) Pf(T) with det(L) = 1, det(P) = (-1)^(#exchanges),
+ * and for the skew tridiagonal T with T(2j+1, 2j) = alpha_{2j}:
+ * Pf(T) = prod_j T(2j, 2j+1) = prod_j (-alpha_{2j}).
+ * Returned as sign in {-1, 0, +1} and log|Pf| (fp64, summed in index order);
+ * odd n or a zero alpha_{2j} gives sign 0 and logabs = -inf. */
+static void CAT(pfaffian, SFX)(int64_t n, const REAL* A, int64_t lda, const int32_t* ipiv,
+                               double* logabs, int32_t* sign)
+{
+    int64_t j, i;
+    int s = 1;
+    double acc = 0.0;
+    if (n % 2 != 0) { *logabs = -INFINITY; *sign = 0; return; }
+    for (j = 0; 2 * j < n; ++j) {
+        double a = (double)A[(2 * j + 1) + (2 * j) * lda];
+        if (a == 0.0) { *logabs = -INFINITY; *sign = 0; return; }
+        acc += log(fabs(a));
+        if (-a < 0.0) s = -s;                    /* factor T(2j,2j+1) = -alpha */
+    }
+    for (i = 0; i < n; ++i)
+        if (ipiv[i] != i) s = -s;                /* each exchange flips det(P) */
+    *logabs = acc;
+    *sign = s;
+}
