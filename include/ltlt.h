@@ -1,0 +1,184 @@
+/*
+ * ltlt.h -- C ABI of the MI355X (gfx950) skew-symmetric LTL^T / Pfaffian library.
+ *
+ * The operation.  For a dense real skew-symmetric X (X^T = -X), the pivoted
+ * triangular tridiagonalization (Parlett & Reid's reduction with partial
+ * pivoting) computes
+ *
+ *        P X P^T = L T L^T
+ *
+ * with L unit lower triangular and L(:,0) = e_0, T skew-symmetric tridiagonal
+ * and P a permutation built from one row/column exchange per column step.
+ * Step k (k = 0 .. n-3) takes as pivot the first index r >= k+1 of largest
+ * |X(r,k)| in the partially reduced matrix, exchanges indices k+1 and r,
+ * sets alpha_k = X(k+1,k) = T(k+1,k) and eliminates column k below row k+1
+ * with multipliers L(r,k+1) = X(r,k)/alpha_k (0 when alpha_k = 0).  The
+ * Pfaffian follows from Pf(B X B^T) = det(B) Pf(X):
+ *        Pf(X) = det(P) * prod_j T(2j, 2j+1) = det(P) * prod_j (-alpha_{2j}).
+ * The paper behind this library gives no interface for the method; these
+ * entry points follow the problem statement, and matrix storage follows the
+ * Fortran column-major convention the paper adopts (section 2, "Data
+ * storage"): element (i, j) of A is A[i + j*lda].
+ *
+ * Common rules for every entry point
+ *   - All pointers are DEVICE pointers (memory of the current HIP device)
+ *     unless stated otherwise.  Calls are stream-ordered and asynchronous:
+ *     they enqueue work on `stream` (0 = legacy default stream) and return.
+ *   - The caller owns every buffer it passes; nothing is retained after the
+ *     call returns.  The library owns a per-device workspace that it grows on
+ *     demand (hipMalloc) and keeps until ltlt_release_workspace().
+ *   - Calls that overlap in time on one device (e.g. on two streams) share
+ *     that workspace and race; serialize them.
+ *   - Return value: 0 on success; -i when argument i (1-based) is invalid
+ *     (nothing is enqueued); LTLT_ERR_HIP_BASE - e for a HIP runtime error e;
+ *     LTLT_ERR_UNSUPPORTED when the size cannot be run (e.g. the panel would
+ *     need more co-resident workgroups than the device holds).
+ *   - Non-finite input gives unspecified factors but every call terminates.
+ */
+#ifndef LTLT_H
+#define LTLT_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Element types (argument `dtype`). */
+#define LTLT_F64 0
+#define LTLT_F32 1
+
+#define LTLT_OK 0
+#define LTLT_ERR_HIP_BASE (-1000)      /* returned as LTLT_ERR_HIP_BASE - (int)hipError_t */
+#define LTLT_ERR_UNSUPPORTED (-2000)
+#define LTLT_ERR_DEVICE_TIMEOUT (-3000) /* a device-side wait exceeded its bound (see ltlt_device_status) */
+
+/* Largest n accepted by ltlt_factor_batched. */
+#define LTLT_BATCHED_MAX_N 64
+
+/*
+ * ltlt_factor -- P X P^T = L T L^T of one n x n skew-symmetric matrix, in place.
+ *   n      (1) order, 0 <= n < 2^21 - 1 (larger orders return
+ *              LTLT_ERR_UNSUPPORTED; an fp64 matrix of that order is 32 TiB).
+ *   A      (2) device, column-major, leading dimension lda.  On entry the
+ *              STRICT LOWER triangle defines X (X(i,j) = A(i,j) for i > j,
+ *              X(j,i) = -A(i,j)); the diagonal is taken as 0 and is never
+ *              read or written.  On exit A(k+1,k) = alpha_k = T(k+1,k) for
+ *              k = 0..n-2 and A(r,k) = L(r,k+1) for r >= k+2, with rows in the
+ *              final pivot order.  The strict upper triangle is never read or
+ *              written.
+ *   lda    (3) lda >= max(1, n).
+ *   dtype  (4) LTLT_F64 or LTLT_F32 (element type of A; arithmetic in it).
+ *   ipiv   (5) device int32[n]: 0-based exchanges in LAPACK laswp order:
+ *              ipiv[0] = 0, ipiv[k+1] = the index exchanged with k+1 at step
+ *              k (>= k+1), ipiv[n-1] = n-1.  P applies (i, ipiv[i]) for
+ *              i = 0..n-1 in increasing order.
+ *   stream (6) HIP stream.
+ * Uses the default panel width (128).
+ */
+int ltlt_factor(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, hipStream_t stream);
+
+/*
+ * ltlt_factor_nb -- as ltlt_factor with an explicit panel width.
+ *   nb (6) number of column steps per block, 1 <= nb <= 256; the trailing
+ *          update of each block is one rank-(nb+1) lower-triangular product.
+ *   stream is argument 7.
+ */
+int ltlt_factor_nb(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, int64_t nb,
+                   hipStream_t stream);
+
+/*
+ * ltlt_pfaffian -- sign and log|Pf(X)| from the output of ltlt_factor.
+ *   n, A, lda, dtype, ipiv (1-5) exactly as returned by ltlt_factor (read only).
+ *   logabs (6) device double[1]: log|Pf(X)| (natural log), summed in fp64.
+ *   sign   (7) device int32[1]: -1, 0 or +1.
+ *   stream (8).
+ * n = 0 gives sign 1, logabs 0.  Odd n, or any alpha_{2j} = 0, gives sign 0
+ * and logabs = -inf (Pf(X) = 0).
+ */
+int ltlt_pfaffian(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* ipiv,
+                  double* logabs, int32_t* sign, hipStream_t stream);
+
+/*
+ * ltlt_factor_batched -- independent factorizations and Pfaffians of `batch`
+ * matrices of order n <= LTLT_BATCHED_MAX_N, one workgroup per matrix.
+ *   n          (1) order, 0 <= n <= LTLT_BATCHED_MAX_N.
+ *   batch      (2) number of matrices, >= 0.
+ *   A          (3) device; matrix b is column-major at A + b*strideA
+ *                  (elements), leading dimension lda; strict lower triangle
+ *                  in, factors out exactly as ltlt_factor (upper triangle and
+ *                  diagonal neither read nor written).
+ *   lda        (4) lda >= max(1, n).
+ *   strideA    (5) >= lda*n (matrices must not overlap).
+ *   dtype      (6) LTLT_F64 or LTLT_F32.
+ *   ipiv       (7) device int32; pivots of matrix b at ipiv + b*strideIpiv.
+ *   strideIpiv (8) >= n.
+ *   logabs     (9) device double[batch]: log|Pf| per matrix.
+ *   sign      (10) device int32[batch]: sign of Pf per matrix.
+ *   stream    (11).
+ */
+int ltlt_factor_batched(int64_t n, int64_t batch, void* A, int64_t lda, int64_t strideA,
+                        int dtype, int32_t* ipiv, int64_t strideIpiv, double* logabs,
+                        int32_t* sign, hipStream_t stream);
+
+/*
+ * ltlt_skew_update -- the trailing update of one block on its own:
+ *   for m x m indices i > c:
+ *     C(i,c) <- S(perm[i], perm[c]) + sum_{u<K} Lx(i,u) * Bt(c,u),
+ *   where S(a,b) = C(a,b) for a > b and -C(b,a) for a < b (the skew matrix
+ *   held in the strict lower triangle).
+ *   C      (2) device, column-major, ldc; only the strict lower triangle of
+ *              the m x m block is written; the diagonal and the upper
+ *              triangle are never written.
+ *   perm   (4) device int32[m] or NULL (identity).  Entries must form a
+ *              permutation and, for every pair i > c with perm[i] != i or
+ *              perm[c] != c, the element C(perm[i], perm[c]) must lie outside
+ *              the m x m block being written -- i.e. callers pass a C that is a
+ *              sub-block of a larger matrix and offsets in perm that point
+ *              into the surrounding rows/columns (read through the same
+ *              strict-lower-triangle rule); with perm == NULL this is a plain
+ *              skew-symmetric rank-K update.  perm entries are relative to C
+ *              (may be negative, reaching rows/columns before C).
+ *   Lx, Bt (6, 8) device, column-major m x K with leading dims ldl, ldb.
+ *   In the factorization, K = nb + 1, Lx = [L(:, j+1..j+nb), carry column]
+ *   and Bt = Lx Tx^T with Tx skew tridiagonal (Tx[u,u+1] = alpha_{j+u+1},
+ *   Tx[nb-1,nb] = 1), so Lx Bt^T = Lx Tx Lx^T.
+ * Arguments: (1) m, (2) C, (3) ldc, (4) perm, (5) K, (6) Lx, (7) ldl,
+ * (8) Bt, (9) ldb, (10) dtype, (11) stream.
+ */
+int ltlt_skew_update(int64_t m, void* C, int64_t ldc, const int32_t* perm, int64_t K,
+                     const void* Lx, int64_t ldl, const void* Bt, int64_t ldb, int dtype,
+                     hipStream_t stream);
+
+/*
+ * ltlt_device_status -- synchronizes `stream` and reports whether a
+ * device-side bounded wait of an earlier ltlt_factor on this device gave up
+ * (LTLT_ERR_DEVICE_TIMEOUT; the factors are then invalid) and clears the flag.
+ * Returns 0 when no wait gave up.
+ */
+int ltlt_device_status(hipStream_t stream);
+
+/*
+ * Per-kernel timing of ltlt_factor, measured with HIP events recorded on the
+ * stream each kernel runs on.
+ *   ltlt_profile_enable(1) starts recording (and clears earlier records),
+ *   ltlt_profile_enable(0) stops.
+ *   ltlt_profile_read synchronizes the recorded events and writes, for each
+ *   kernel kind k < nkinds (0 = panel, 1 = trailing update, 2 = commit,
+ *   3 = other), the launch count, the summed milliseconds and the summed
+ *   nominal flops (trailing update: m2^2 * nb per launch; others 0) into the
+ *   HOST arrays launches[k], ms[k], flops[k].  Returns the number of kinds
+ *   written.
+ */
+int ltlt_profile_enable(int on);
+int ltlt_profile_read(int nkinds, int64_t* launches, double* ms, double* flops);
+
+/* Frees the cached workspace of every device (host call; synchronizes). */
+int ltlt_release_workspace(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LTLT_H */

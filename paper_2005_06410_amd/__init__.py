@@ -1,0 +1,258 @@
+"""MI355X (gfx950) skew-symmetric LTL^T factorization and Pfaffian.
+
+Thin Python binding over the C ABI of ``libltlt.so`` (``include/ltlt.h``):
+it only checks layouts and marshals pointers, sizes and the current HIP
+stream; every step of the computation runs in the library's gfx950 kernels.
+PyTorch supplies device memory and streams.
+
+Matrices are column-major (the Fortran convention): pass a 2-D tensor ``A``
+with ``A.stride(0) == 1`` and ``A.stride(1) == lda >= n`` (for example
+``torch.empty_strided((n, n), (1, lda), ...)`` or ``X.t().contiguous().t()``),
+so that ``A[i, j]`` is element (i, j).  A row-major tensor is rejected: read as
+column-major it would be X^T = -X (same L and P, T negated, Pf times
+(-1)^(n/2)).
+
+If the library is not built, or no GPU is visible, every call raises; there
+is no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+__all__ = [
+    "LIB_PATH",
+    "load",
+    "factor",
+    "pfaffian",
+    "factor_batched",
+    "skew_update",
+    "device_status",
+    "profile_enable",
+    "profile_read",
+    "release_workspace",
+    "LtltError",
+    "F64",
+    "F32",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libltlt.so")
+F64, F32 = 0, 1
+BATCHED_MAX_N = 64
+_lock = threading.Lock()
+_lib = None
+
+_SYMBOLS = {
+    "ltlt_factor": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
+                     ctypes.c_void_p], ctypes.c_int),
+    "ltlt_factor_nb": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
+                        ctypes.c_int64, ctypes.c_void_p], ctypes.c_int),
+    "ltlt_pfaffian": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
+                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
+    "ltlt_factor_batched": ([ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                             ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                             ctypes.c_void_p], ctypes.c_int),
+    "ltlt_skew_update": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
+                          ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                          ctypes.c_void_p], ctypes.c_int),
+    "ltlt_device_status": ([ctypes.c_void_p], ctypes.c_int),
+    "ltlt_profile_enable": ([ctypes.c_int], ctypes.c_int),
+    "ltlt_profile_read": ([ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
+    "ltlt_release_workspace": ([], ctypes.c_int),
+}
+
+
+class LtltError(RuntimeError):
+    """A nonzero return code of the C ABI."""
+
+    def __init__(self, fn: str, code: int):
+        self.code = code
+        if code <= -3000 and code > -4000:
+            what = "a device-side bounded wait gave up"
+        elif code == -2000:
+            what = "size not supported on this device"
+        elif code <= -1000:
+            what = f"HIP runtime error {-1000 - code}"
+        else:
+            what = f"argument {-code} is invalid"
+        super().__init__(f"{fn} returned {code}: {what}")
+
+
+def load():
+    """Load ``libltlt.so`` (raises if it has not been built)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError(
+                    f"{LIB_PATH} is missing: build it with `python -m paper_2005_06410_amd.build` "
+                    "(the GPU path has no fallback)")
+            lib = ctypes.CDLL(LIB_PATH)
+            for name, (args, res) in _SYMBOLS.items():
+                fn = getattr(lib, name)
+                fn.argtypes = args
+                fn.restype = res
+            _lib = lib
+    return _lib
+
+
+def _check(fn: str, code: int):
+    if code != 0:
+        raise LtltError(fn, code)
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.float64:
+        return F64
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError("only float64 and float32 are supported")
+
+
+def _stream_ptr(device) -> int:
+    torch = _torch()
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _require_gpu(t):
+    if not t.is_cuda:
+        raise ValueError("tensor must live on a GPU (the library has no CPU path)")
+
+
+def _colmajor_lda(A) -> int:
+    if A.dim() != 2 or A.shape[0] != A.shape[1]:
+        raise ValueError("A must be a square 2-D tensor")
+    n = A.shape[0]
+    if n <= 1:
+        return max(1, A.stride(1) if A.dim() == 2 else 1)
+    if A.stride(0) != 1 or A.stride(1) < n:
+        raise ValueError("A must be column-major: stride(0) == 1 and stride(1) = lda >= n "
+                         "(a row-major skew matrix would be read as its negation)")
+    return A.stride(1)
+
+
+def factor(A, ipiv=None, nb: int | None = None):
+    """In-place P X P^T = L T L^T of the column-major skew matrix ``A``.
+
+    Returns the int32 pivot tensor (0-based, LAPACK laswp order).  On return
+    A's strict lower triangle holds alpha_k at (k+1, k) and L(r, k+1) at (r, k);
+    its strict upper triangle is scratch (unspecified)."""
+    torch = _torch()
+    _require_gpu(A)
+    lda = _colmajor_lda(A)
+    n = A.shape[0]
+    if ipiv is None:
+        ipiv = torch.empty(max(n, 1), dtype=torch.int32, device=A.device)
+    if ipiv.dtype != torch.int32 or not ipiv.is_contiguous() or ipiv.numel() < n:
+        raise ValueError("ipiv must be a contiguous int32 tensor with at least n entries")
+    lib = load()
+    s = _stream_ptr(A.device)
+    if nb is None:
+        code = lib.ltlt_factor(n, A.data_ptr(), lda, _dtype_code(A), ipiv.data_ptr(), s)
+    else:
+        code = lib.ltlt_factor_nb(n, A.data_ptr(), lda, _dtype_code(A), ipiv.data_ptr(), int(nb), s)
+    _check("ltlt_factor", code)
+    return ipiv[:n] if ipiv.numel() != n else ipiv
+
+
+def pfaffian(A, ipiv):
+    """(logabs, sign) device tensors of Pf(X) from ``factor``'s output."""
+    torch = _torch()
+    _require_gpu(A)
+    lda = _colmajor_lda(A)
+    n = A.shape[0]
+    logabs = torch.empty(1, dtype=torch.float64, device=A.device)
+    sign = torch.empty(1, dtype=torch.int32, device=A.device)
+    lib = load()
+    code = lib.ltlt_pfaffian(n, A.data_ptr(), lda, _dtype_code(A), ipiv.data_ptr(), logabs.data_ptr(),
+                             sign.data_ptr(), _stream_ptr(A.device))
+    _check("ltlt_pfaffian", code)
+    return logabs, sign
+
+
+def factor_batched(A, ipiv=None):
+    """Factor and take the Pfaffian of every matrix of a (batch, n, n) tensor
+    whose matrices are column-major (``A.stride(1) == 1``, ``A.stride(2) == lda``).
+
+    Returns (ipiv (batch, n) int32, logabs (batch,) f64, sign (batch,) int32)."""
+    torch = _torch()
+    _require_gpu(A)
+    if A.dim() != 3 or A.shape[1] != A.shape[2]:
+        raise ValueError("A must be (batch, n, n)")
+    batch, n = A.shape[0], A.shape[1]
+    if n > 1 and (A.stride(1) != 1 or A.stride(2) < n):
+        raise ValueError("each matrix must be column-major: stride(1) == 1, stride(2) = lda >= n")
+    lda = A.stride(2) if n > 1 else max(1, n)
+    strideA = A.stride(0) if batch > 1 else lda * max(n, 1)
+    if ipiv is None:
+        ipiv = torch.empty((batch, max(n, 1)), dtype=torch.int32, device=A.device)
+    logabs = torch.empty(batch, dtype=torch.float64, device=A.device)
+    sign = torch.empty(batch, dtype=torch.int32, device=A.device)
+    lib = load()
+    code = lib.ltlt_factor_batched(n, batch, A.data_ptr(), lda, strideA, _dtype_code(A), ipiv.data_ptr(),
+                                   ipiv.stride(0), logabs.data_ptr(), sign.data_ptr(), _stream_ptr(A.device))
+    _check("ltlt_factor_batched", code)
+    return ipiv[:, :n], logabs, sign
+
+
+def skew_update(C, Lx, Bt, perm=None, offset: int = 0):
+    """The trailing-block update on its own (see ``ltlt_skew_update``).
+
+    ``C`` is a column-major tensor view; the m x m block starting ``offset``
+    rows and columns into it is updated; ``perm`` (int32, length m) holds
+    source indices relative to that block start."""
+    torch = _torch()
+    _require_gpu(C)
+    if C.dim() != 2 or C.stride(0) != 1:
+        raise ValueError("C must be column-major")
+    m, K = Lx.shape
+    ldc = C.stride(1)
+    for t in (Lx, Bt):
+        if t.dim() != 2 or (t.shape[0] > 1 and t.stride(0) != 1):
+            raise ValueError("Lx and Bt must be column-major")
+    elem = C.element_size()
+    ptr = C.data_ptr() + (offset + offset * ldc) * elem
+    pp = 0 if perm is None else perm.data_ptr()
+
+    def ld(t):  # leading dimension; a single column may carry any stride
+        return max(t.stride(1), 1) if t.shape[1] > 1 else max(t.shape[0], 1)
+
+    lib = load()
+    code = lib.ltlt_skew_update(m, ptr, ldc, pp, K, Lx.data_ptr(), ld(Lx), Bt.data_ptr(), ld(Bt),
+                                _dtype_code(C), _stream_ptr(C.device))
+    _check("ltlt_skew_update", code)
+
+
+def device_status(device=None):
+    """Synchronize and raise if a device-side bounded wait gave up."""
+    torch = _torch()
+    lib = load()
+    _check("ltlt_device_status", lib.ltlt_device_status(_stream_ptr(device or torch.cuda.current_device())))
+
+
+def profile_enable(on: bool = True):
+    load().ltlt_profile_enable(1 if on else 0)
+
+
+def profile_read():
+    """{kind: (launches, ms, flops)} for kinds panel, update, commit, other."""
+    lib = load()
+    launches = (ctypes.c_int64 * 4)()
+    ms = (ctypes.c_double * 4)()
+    flops = (ctypes.c_double * 4)()
+    k = lib.ltlt_profile_read(4, launches, ms, flops)
+    if k < 0:
+        raise LtltError("ltlt_profile_read", k)
+    names = ["panel", "update", "commit", "other"]
+    return {names[i]: (int(launches[i]), float(ms[i]), float(flops[i])) for i in range(k)}
+
+
+def release_workspace():
+    _check("ltlt_release_workspace", load().ltlt_release_workspace())

@@ -1,0 +1,370 @@
+// Host side of the C ABI declared in include/ltlt.h: argument checks, the
+// per-device workspace, the block loop of the factorization and optional
+// per-kernel event timing.  Every compute step runs in the gfx950 kernels of
+// this library; nothing here touches matrix data on the host.
+
+#include <algorithm>
+#include <map>
+#include <mutex>
+#include <vector>
+
+#include "ltlt.h"
+#include "ltlt_internal.h"
+
+using namespace ltlt;
+
+namespace {
+
+constexpr int kDefaultNb = 128;
+constexpr int64_t kMaxOrder = (1 << 21) - 1;   // exchange records pack indices in 21 bits
+constexpr size_t kLdsBudget = 160 * 1024 - 2048;   // dynamic LDS a panel workgroup may use
+
+int hip_err(hipError_t e) { return LTLT_ERR_HIP_BASE - (int)e; }
+
+// ---- per-device workspace -------------------------------------------------
+struct Workspace {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+  int* status = nullptr;     // device flag for bounded waits (kept separately)
+};
+std::mutex g_ws_mu;
+std::map<int, Workspace> g_ws;
+
+hipError_t workspace(size_t bytes, void** out, int** status) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  Workspace& w = g_ws[dev];
+  if (!w.status) {
+    e = hipMalloc(&w.status, 256);
+    if (e != hipSuccess) { w.status = nullptr; return e; }
+    e = hipMemset(w.status, 0, 256);
+    if (e != hipSuccess) return e;
+  }
+  if (w.bytes < bytes) {
+    if (w.ptr) {
+      e = hipDeviceSynchronize();       // earlier work may still use it
+      if (e != hipSuccess) return e;
+      e = hipFree(w.ptr);
+      if (e != hipSuccess) return e;
+      w.ptr = nullptr;
+      w.bytes = 0;
+    }
+    size_t want = std::max(bytes, (size_t)1 << 20);
+    e = hipMalloc(&w.ptr, want);
+    if (e != hipSuccess) { w.ptr = nullptr; return e; }
+    w.bytes = want;
+  }
+  *out = w.ptr;
+  *status = w.status;
+  return hipSuccess;
+}
+
+// bump allocator inside the workspace (256-byte aligned pieces)
+struct Carve {
+  size_t off = 0;
+  template <typename U> size_t take(size_t count) {
+    size_t at = off;
+    off += (count * sizeof(U) + 255) & ~(size_t)255;
+    return at;
+  }
+};
+
+// ---- profiling ---------------------------------------------------------------
+struct ProfRec {
+  int kind;
+  hipEvent_t a, b;
+  double flops;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<ProfRec> g_prof;
+
+struct ProfScope {
+  ProfRec rec{};
+  bool on = false;
+  hipStream_t s;
+  ProfScope(int kind, double flops, hipStream_t st) : s(st) {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    if (!g_prof_on) return;
+    rec.kind = kind;
+    rec.flops = flops;
+    if (hipEventCreate(&rec.a) != hipSuccess) return;
+    if (hipEventCreate(&rec.b) != hipSuccess) { (void)hipEventDestroy(rec.a); return; }
+    on = (hipEventRecord(rec.a, s) == hipSuccess);
+  }
+  ~ProfScope() {
+    if (!on) return;
+    (void)hipEventRecord(rec.b, s);
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    g_prof.push_back(rec);
+  }
+};
+
+void prof_clear_locked() {
+  for (auto& r : g_prof) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
+  g_prof.clear();
+}
+
+// ---- factorization -----------------------------------------------------------
+template <typename T>
+int choose_rows(int bw) {
+  const int R = panel_rows(bw);
+  return panel_lds_bytes<T>(bw, R) <= kLdsBudget ? R : 0;
+}
+
+template <typename T>
+int factor_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, hipStream_t s) {
+  if (n64 == 0) return 0;
+  if (n64 >= kMaxOrder) return LTLT_ERR_UNSUPPORTED;
+  const int n = (int)n64;
+  const int nsteps = std::max(n - 2, 0);
+  const int nblk = nsteps > 0 ? (nsteps + nb - 1) / nb : 0;
+  const int bw0 = std::min(nb, std::max(nsteps, 1));
+
+  // panel geometry of the largest block (block 0) bounds every other block
+  const int R = choose_rows<T>(bw0);
+  int Pmax = 1;
+  if (nblk > 0) {
+    if (R == 0) return LTLT_ERR_UNSUPPORTED;
+    const size_t lds = panel_lds_bytes<T>(bw0, R);
+    Pmax = (n - 1 + R - 1) / R;
+    const int cap = panel_max_blocks<T>(R, lds);
+    if (cap <= 0 || Pmax > cap) return LTLT_ERR_UNSUPPORTED;
+  }
+
+  const int64_t ldw = ((int64_t)n + 63) / 64 * 64;
+  const int c_end = nblk >= 2 ? (nblk - 1) * nb : 0;
+  Carve cv;
+  const size_t o_PO = cv.take<T>((size_t)ldw * (nb + 1));
+  const size_t o_Bm = cv.take<T>((size_t)ldw * (nb + 1));
+  const size_t o_G = cv.take<T>((size_t)ldw * nb);
+  const size_t o_al = cv.take<T>((size_t)nb);
+  const size_t o_T = cv.take<int>((size_t)std::max(nblk, 1) * n);
+  const size_t o_GC = cv.take<int>((size_t)std::max(nblk, 1) * n);
+  const size_t o_rec = cv.take<uint64_t>((size_t)4 * (Pmax + 1));
+  const size_t o_st = cv.take<T>(perm_stage_elems<T>(n, c_end));
+
+  void* ws = nullptr;
+  int* status = nullptr;
+  hipError_t e = workspace(cv.off, &ws, &status);
+  if (e != hipSuccess) return hip_err(e);
+  char* base = static_cast<char*>(ws);
+  T* PO = reinterpret_cast<T*>(base + o_PO);
+  T* Bm = reinterpret_cast<T*>(base + o_Bm);
+  T* Gm = reinterpret_cast<T*>(base + o_G);
+  T* al = reinterpret_cast<T*>(base + o_al);
+  int* Tblk = reinterpret_cast<int*>(base + o_T);
+  int* Gc = reinterpret_cast<int*>(base + o_GC);
+  uint64_t* rec = reinterpret_cast<uint64_t*>(base + o_rec);
+  T* stage = reinterpret_cast<T*>(base + o_st);
+
+  {
+    ProfScope ps(3, 0.0, s);
+    e = launch_init(ipiv, n, status, s);
+    if (e == hipSuccess && nblk > 0) e = launch_rec_init(rec, Pmax + 1, s);
+  }
+  if (e != hipSuccess) return hip_err(e);
+
+  for (int J = 0; J < nblk; ++J) {
+    const int j = J * nb;
+    const int bw = std::min(nb, nsteps - j);
+    const int m = n - j - 1;
+    PanelArgs pa{};
+    pa.A = A; pa.lda = lda; pa.n = n; pa.j = j; pa.bw = bw;
+    pa.R = choose_rows<T>(bw);
+    pa.P = (m + pa.R - 1) / pa.R;
+    pa.kslot = Pmax;
+    pa.G = Gm; pa.PO = PO; pa.Bm = Bm; pa.ldw = ldw; pa.alpha = al;
+    pa.perm = Tblk + (int64_t)J * n;
+    pa.ipiv = ipiv;
+    pa.rec = rec;
+    pa.status = status;
+    {
+      ProfScope ps(0, 0.0, s);
+      e = launch_panel<T>(pa, panel_lds_bytes<T>(bw, pa.R), s);
+    }
+    if (e != hipSuccess) return hip_err(e);
+
+    const int i0 = j + bw + 1;
+    const int m2 = n - i0;
+    if (m2 >= 2) {
+      UpdateArgs ua{};
+      ua.C = A + (int64_t)i0 + (int64_t)i0 * lda;
+      ua.ldc = lda;
+      ua.m = m2;
+      ua.perm = Tblk + (int64_t)J * n + i0;
+      ua.perm_base = i0;
+      ua.K = bw + 1;
+      ua.Lx = PO + bw;
+      ua.ldl = ldw;
+      ua.Bt = Bm;
+      ua.ldb = ldw;
+      ProfScope ps(1, (double)m2 * (double)m2 * (double)bw, s);
+      e = launch_update<T>(ua, s);
+      if (e != hipSuccess) return hip_err(e);
+    }
+    {
+      ProfScope ps(2, 0.0, s);
+      e = launch_commit<T>(A, lda, n, j, bw, PO, ldw, al, s);
+    }
+    if (e != hipSuccess) return hip_err(e);
+  }
+
+  if (nblk >= 2) {
+    ProfScope ps(3, 0.0, s);
+    e = launch_perm_chain(Tblk, nb, nblk, n, Gc, s);
+    if (e == hipSuccess) e = launch_perm_apply<T>(A, lda, n, Gc, nb, c_end, stage, s);
+    if (e != hipSuccess) return hip_err(e);
+  }
+  return 0;
+}
+
+bool bad_dtype(int d) { return d != LTLT_F64 && d != LTLT_F32; }
+
+}  // namespace
+
+extern "C" {
+
+int ltlt_factor_nb(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, int64_t nb, hipStream_t stream) {
+  if (n < 0 || n > (int64_t)INT32_MAX / 2) return -1;
+  if (A == nullptr && n > 0) return -2;
+  if (lda < std::max<int64_t>(1, n)) return -3;
+  if (bad_dtype(dtype)) return -4;
+  if (ipiv == nullptr && n > 0) return -5;
+  if (nb < 1 || nb > kMaxNb) return -6;
+  if (n == 0) return 0;
+  if (dtype == LTLT_F64) return factor_impl<double>(n, static_cast<double*>(A), lda, ipiv, (int)nb, stream);
+  return factor_impl<float>(n, static_cast<float*>(A), lda, ipiv, (int)nb, stream);
+}
+
+int ltlt_factor(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, hipStream_t stream) {
+  return ltlt_factor_nb(n, A, lda, dtype, ipiv, kDefaultNb, stream);
+}
+
+int ltlt_pfaffian(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* ipiv, double* logabs,
+                  int32_t* sign, hipStream_t stream) {
+  if (n < 0 || n > (int64_t)INT32_MAX / 2) return -1;
+  if (A == nullptr && n > 0) return -2;
+  if (lda < std::max<int64_t>(1, n)) return -3;
+  if (bad_dtype(dtype)) return -4;
+  if (ipiv == nullptr && n > 0) return -5;
+  if (logabs == nullptr) return -6;
+  if (sign == nullptr) return -7;
+  hipError_t e;
+  if (dtype == LTLT_F64)
+    e = launch_pfaffian<double>((int)n, static_cast<const double*>(A), lda, ipiv, logabs, sign, stream);
+  else
+    e = launch_pfaffian<float>((int)n, static_cast<const float*>(A), lda, ipiv, logabs, sign, stream);
+  return e == hipSuccess ? 0 : hip_err(e);
+}
+
+int ltlt_factor_batched(int64_t n, int64_t batch, void* A, int64_t lda, int64_t strideA, int dtype,
+                        int32_t* ipiv, int64_t strideIpiv, double* logabs, int32_t* sign, hipStream_t stream) {
+  if (n < 0 || n > LTLT_BATCHED_MAX_N) return -1;
+  if (batch < 0 || batch > (int64_t)INT32_MAX) return -2;
+  if (A == nullptr && n > 0 && batch > 0) return -3;
+  if (lda < std::max<int64_t>(1, n)) return -4;
+  if (batch > 1 && strideA < lda * n) return -5;
+  if (bad_dtype(dtype)) return -6;
+  if (ipiv == nullptr && n > 0 && batch > 0) return -7;
+  if (batch > 1 && strideIpiv < n) return -8;
+  if (logabs == nullptr && batch > 0) return -9;
+  if (sign == nullptr && batch > 0) return -10;
+  if (batch == 0) return 0;
+  hipError_t e;
+  if (dtype == LTLT_F64)
+    e = launch_batched<double>((int)n, (int)batch, static_cast<double*>(A), lda, strideA, ipiv, strideIpiv, logabs,
+                               sign, stream);
+  else
+    e = launch_batched<float>((int)n, (int)batch, static_cast<float*>(A), lda, strideA, ipiv, strideIpiv, logabs,
+                              sign, stream);
+  return e == hipSuccess ? 0 : hip_err(e);
+}
+
+int ltlt_skew_update(int64_t m, void* C, int64_t ldc, const int32_t* perm, int64_t K, const void* Lx, int64_t ldl,
+                     const void* Bt, int64_t ldb, int dtype, hipStream_t stream) {
+  if (m < 0 || m > (int64_t)INT32_MAX / 2) return -1;
+  if (C == nullptr && m > 0) return -2;
+  if (ldc < std::max<int64_t>(1, m)) return -3;
+  if (K < 0 || K > (int64_t)INT32_MAX / 2) return -5;
+  if (Lx == nullptr && m > 0 && K > 0) return -6;
+  if (ldl < std::max<int64_t>(1, m)) return -7;
+  if (Bt == nullptr && m > 0 && K > 0) return -8;
+  if (ldb < std::max<int64_t>(1, m)) return -9;
+  if (bad_dtype(dtype)) return -10;
+  if (m < 2) return 0;
+  UpdateArgs ua{};
+  ua.C = C; ua.ldc = ldc; ua.m = (int)m; ua.perm = perm; ua.perm_base = 0;
+  ua.K = (int)K; ua.Lx = Lx; ua.ldl = ldl; ua.Bt = Bt; ua.ldb = ldb;
+  hipError_t e = dtype == LTLT_F64 ? launch_update<double>(ua, stream) : launch_update<float>(ua, stream);
+  return e == hipSuccess ? 0 : hip_err(e);
+}
+
+int ltlt_device_status(hipStream_t stream) {
+  hipError_t e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return hip_err(e);
+  int dev = 0;
+  e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_err(e);
+  int* st = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    auto it = g_ws.find(dev);
+    if (it == g_ws.end() || !it->second.status) return 0;
+    st = it->second.status;
+  }
+  int h = 0;
+  e = hipMemcpy(&h, st, sizeof(int), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_err(e);
+  if (h != 0) {
+    e = hipMemset(st, 0, sizeof(int));
+    if (e != hipSuccess) return hip_err(e);
+    return LTLT_ERR_DEVICE_TIMEOUT;
+  }
+  return 0;
+}
+
+int ltlt_profile_enable(int on) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (on) prof_clear_locked();
+  g_prof_on = on != 0;
+  return 0;
+}
+
+int ltlt_profile_read(int nkinds, int64_t* launches, double* ms, double* flops) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  const int kinds = std::min(nkinds, 4);
+  for (int k = 0; k < kinds; ++k) { launches[k] = 0; ms[k] = 0.0; flops[k] = 0.0; }
+  for (auto& r : g_prof) {
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e != hipSuccess) return hip_err(e);
+    float t = 0.f;
+    e = hipEventElapsedTime(&t, r.a, r.b);
+    if (e != hipSuccess) return hip_err(e);
+    if (r.kind < kinds) {
+      launches[r.kind] += 1;
+      ms[r.kind] += t;
+      flops[r.kind] += r.flops;
+    }
+  }
+  return kinds;
+}
+
+int ltlt_release_workspace(void) {
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  int dev0 = 0;
+  (void)hipGetDevice(&dev0);
+  for (auto& kv : g_ws) {
+    if (hipSetDevice(kv.first) != hipSuccess) continue;
+    (void)hipDeviceSynchronize();
+    if (kv.second.ptr) (void)hipFree(kv.second.ptr);
+    if (kv.second.status) (void)hipFree(kv.second.status);
+  }
+  g_ws.clear();
+  (void)hipSetDevice(dev0);
+  return 0;
+}
+
+}  // extern "C"

@@ -1,0 +1,68 @@
+// Internal declarations shared by the host driver and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ltlt {
+
+constexpr int kThreads = 256;        // workgroup size of the panel and update kernels
+constexpr int kMaxNb = 256;          // widest panel
+
+// Arguments of one panel launch (block of steps k = j .. j+bw-1).
+struct PanelArgs {
+  const void* A;      // matrix, column-major, strict lower triangle as of block start
+  int64_t lda;
+  int n;
+  int j;              // first column step of the block
+  int bw;             // steps in the block
+  int R;              // rows per workgroup
+  int P;              // workgroups
+  int kslot;          // record index of the position-(k+1) record (>= every P of the factorization)
+  void* G;            // multipliers by block-start index: G[(idx - j - 1) + u*ldw]
+  void* PO;           // panel out, rows j+1.., columns 0..bw (bw = carry), ld = ldw
+  void* Bm;           // Bt = Lx Tx^T for rows >= j+bw+1, columns 0..bw, ld = ldw
+  int64_t ldw;
+  void* alpha;        // alpha_{j+t}, t < bw
+  int* perm;          // perm[i] for positions i >= j+1: index held at block start
+  int* ipiv;
+  uint64_t* rec;      // exchange records [2][kslot+1][2]
+  int* status;        // nonzero: a bounded wait gave up
+};
+
+// Arguments of one trailing update.
+struct UpdateArgs {
+  void* C;            // first element of the m x m trailing block
+  int64_t ldc;
+  int m;
+  const int* perm;    // source index per row/column (minus perm_base), or nullptr
+  int perm_base;
+  int K;
+  const void* Lx;
+  int64_t ldl;
+  const void* Bt;
+  int64_t ldb;
+  int tiles;          // number of 128-row tile rows
+};
+
+template <typename T> hipError_t launch_panel(const PanelArgs& a, size_t lds, hipStream_t s);
+template <typename T> size_t panel_lds_bytes(int bw, int R);
+template <typename T> hipError_t launch_update(const UpdateArgs& a, hipStream_t s);
+
+template <typename T> hipError_t launch_commit(T* A, int64_t lda, int n, int j, int bw, const T* PO,
+                                               int64_t ldw, const T* alpha, hipStream_t s);
+template <typename T> hipError_t launch_perm_apply(T* A, int64_t lda, int n, const int* G, int nb, int c_end,
+                                                   T* stage, hipStream_t s);
+template <typename T> size_t perm_stage_elems(int n, int c_end);
+template <typename T> hipError_t launch_pfaffian(int n, const T* A, int64_t lda, const int* ipiv, double* logabs,
+                                                 int* sign, hipStream_t s);
+template <typename T> hipError_t launch_batched(int n, int batch, T* A, int64_t lda, int64_t strideA, int* ipiv,
+                                                int64_t strideIpiv, double* logabs, int* sign, hipStream_t s);
+
+hipError_t launch_init(int* ipiv, int n, int* status, hipStream_t s);
+hipError_t launch_rec_init(uint64_t* rec, int nrec_per_slot, hipStream_t s);
+hipError_t launch_perm_chain(const int* Tblk, int nb, int nblk, int n, int* G, hipStream_t s);
+template <typename T> int panel_max_blocks(int R, size_t lds);
+int panel_rows(int bw);
+
+}  // namespace ltlt

@@ -1,0 +1,198 @@
+// Trailing update of one block: for the m x m trailing block C (skew, held in
+// its strict lower triangle) and each pair i > c,
+//     C(i,c) <- S(perm[i], perm[c]) + sum_u Lx(i,u) Bt(c,u),
+// S(a,b) = C(a,b) for a > b and -C(b,a) for a < b.
+// With Bt = Lx Tx^T this is C + Lx Tx Lx^T: the block's 2*nb rank-1 terms
+// collapsed into one product of inner dimension nb+1 (the skew rank-2k update
+// A22 - (L21 W^T - W L21^T) of the method, with W formed from L21 and the
+// alphas, so only the lower triangle is computed, once).
+//
+// gfx950 mapping:
+//  * one 256-thread workgroup per 128x128 tile of the LOWER triangle only
+//    (tile row >= tile column); the triangular tile index is decoded once per
+//    workgroup;
+//  * each of the 4 waves owns a 64x64 sub-tile = 4x4 MFMA blocks of 16x16
+//    (v_mfma_f64_16x16x4_f64, or v_mfma_f32_16x16x4_f32 for fp32),
+//    accumulating in registers;
+//  * Lx and Bt are streamed through LDS in K-chunks of 16 columns, double
+//    buffered, with 16-byte coalesced global loads (128 contiguous rows per
+//    column chunk);
+//  * the epilogue reads the old value through perm (the exchanges of the
+//    panel, applied as a gather: every displaced source lies outside the
+//    block being written, so tiles never race), adds, and writes the lower
+//    entry only; diagonal tiles mask i <= c.  Per block the kernel moves
+//    8 m^2 bytes (read + write of the lower triangle) against m^2 (nb+1)
+//    flops, about (nb+1)/8 flop/byte in fp64.
+// The operand staging follows the paper's packing idea (section 2, packing
+// of A_c/B_c amortized over the inner loops), re-shaped for LDS and MFMA.
+
+#include "ltlt_device.h"
+#include "ltlt_internal.h"
+
+namespace ltlt {
+
+constexpr int kMT = 128;     // tile edge
+constexpr int kKC = 16;      // K chunk
+
+typedef double v4d __attribute__((ext_vector_type(4)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+template <typename T> struct Mfma;
+template <> struct Mfma<double> {
+  typedef v4d acc_t;
+  static __device__ __forceinline__ acc_t run(double a, double b, acc_t c) {
+    return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+  }
+  // output element v of lane l sits at row (l/16) + 4v, column l%16
+  static __device__ __forceinline__ int row(int l, int v) { return (l >> 4) + 4 * v; }
+};
+template <> struct Mfma<float> {
+  typedef v4f acc_t;
+  static __device__ __forceinline__ acc_t run(float a, float b, acc_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+  // output element v of lane l sits at row 4(l/16) + v, column l%16
+  static __device__ __forceinline__ int row(int l, int v) { return 4 * (l >> 4) + v; }
+};
+
+template <typename T>
+__device__ __forceinline__ void load_chunk(const T* __restrict__ X, int64_t ldx, int m, int K, int r0, int k0,
+                                           T (&reg)[8], int tid) {
+  // thread -> column (tid / 16), rows (tid % 16) * 8 .. +8 of a 128 x 16 chunk
+  const int col = tid >> 4;
+  const int rr = (tid & 15) * 8;
+  const int kk = k0 + col;
+  const int rbase = r0 + rr;
+  if (kk < K && rbase + 8 <= m) {
+    const T* p = X + (int64_t)kk * ldx + rbase;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) reg[e] = p[e];
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int r = rbase + e;
+      reg[e] = (kk < K && r < m) ? X[(int64_t)kk * ldx + r] : T(0);
+    }
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void store_chunk(T* __restrict__ S, const T (&reg)[8], int tid) {
+  const int col = tid >> 4;
+  const int rr = (tid & 15) * 8;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) S[col * kMT + rr + e] = reg[e];
+}
+
+template <typename T>
+__global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
+  typedef typename Mfma<T>::acc_t acc_t;
+  __shared__ __align__(16) T As[2][kKC * kMT];
+  __shared__ __align__(16) T Bs[2][kKC * kMT];
+  __shared__ int prow[kMT], pcol[kMT];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wr = wave >> 1, wc = wave & 1;
+
+  // triangular decode: blockIdx.x = I(I+1)/2 + J, J <= I
+  const int b = blockIdx.x;
+  int I = (int)((sqrt(8.0 * (double)b + 1.0) - 1.0) * 0.5);
+  while ((I + 1) * (I + 2) / 2 <= b) ++I;
+  while (I * (I + 1) / 2 > b) --I;
+  const int J = b - I * (I + 1) / 2;
+  const int r0 = I * kMT, c0 = J * kMT;
+  const int m = a.m, K = a.K;
+
+  const T* Lx = static_cast<const T*>(a.Lx);
+  const T* Bt = static_cast<const T*>(a.Bt);
+
+  acc_t acc[4][4];
+#pragma unroll
+  for (int x = 0; x < 4; ++x)
+#pragma unroll
+    for (int y = 0; y < 4; ++y) acc[x][y] = acc_t{0, 0, 0, 0};
+
+  T ra[8], rb[8];
+  load_chunk<T>(Lx, a.ldl, m, K, r0, 0, ra, tid);
+  load_chunk<T>(Bt, a.ldb, m, K, c0, 0, rb, tid);
+  store_chunk<T>(As[0], ra, tid);
+  store_chunk<T>(Bs[0], rb, tid);
+  if (tid < kMT) {
+    const int ri = r0 + tid, ci = c0 + tid;
+    prow[tid] = (a.perm && ri < m) ? a.perm[ri] - a.perm_base : ri;
+    pcol[tid] = (a.perm && ci < m) ? a.perm[ci] - a.perm_base : ci;
+  }
+  __syncthreads();
+
+  const int nchunk = (K + kKC - 1) / kKC;
+  for (int ch = 0; ch < nchunk; ++ch) {
+    const int cur = ch & 1;
+    const bool more = ch + 1 < nchunk;
+    if (more) {
+      load_chunk<T>(Lx, a.ldl, m, K, r0, (ch + 1) * kKC, ra, tid);
+      load_chunk<T>(Bt, a.ldb, m, K, c0, (ch + 1) * kKC, rb, tid);
+    }
+    const T* as = As[cur];
+    const T* bs = Bs[cur];
+    const int ksteps = min(kKC, K - ch * kKC);
+    for (int k4 = 0; k4 < ksteps; k4 += 4) {
+      const int kr = k4 + (lane >> 4);
+      T af[4], bf[4];
+#pragma unroll
+      for (int x = 0; x < 4; ++x) af[x] = as[kr * kMT + wr * 64 + x * 16 + (lane & 15)];
+#pragma unroll
+      for (int y = 0; y < 4; ++y) bf[y] = bs[kr * kMT + wc * 64 + y * 16 + (lane & 15)];
+#pragma unroll
+      for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 4; ++y) acc[x][y] = Mfma<T>::run(af[x], bf[y], acc[x][y]);
+    }
+    if (more) {
+      store_chunk<T>(As[cur ^ 1], ra, tid);
+      store_chunk<T>(Bs[cur ^ 1], rb, tid);
+    }
+    __syncthreads();
+  }
+
+  // ---- epilogue: gather old value, add, write lower entry and mirror ----
+  T* C = static_cast<T*>(a.C);
+  const int64_t ldc = a.ldc;
+#pragma unroll
+  for (int x = 0; x < 4; ++x) {
+#pragma unroll
+    for (int y = 0; y < 4; ++y) {
+      const int cl = wc * 64 + y * 16 + (lane & 15);
+      const int c = c0 + cl;
+      const int pc = pcol[cl];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int rl = wr * 64 + x * 16 + Mfma<T>::row(lane, v);
+        const int i = r0 + rl;
+        if (i > c && i < m) {
+          const int pr = prow[rl];
+          // S(pr, pc) from the strict lower triangle: A(pr,pc) or -A(pc,pr)
+          const T old = pr > pc ? C[(int64_t)pr + (int64_t)pc * ldc] : -C[(int64_t)pc + (int64_t)pr * ldc];
+          C[(int64_t)i + (int64_t)c * ldc] = old + acc[x][y][v];
+        }
+      }
+    }
+  }
+}
+
+template <typename T>
+hipError_t launch_update(const UpdateArgs& a, hipStream_t s) {
+  const int tiles = (a.m + kMT - 1) / kMT;
+  const int64_t nblk = (int64_t)tiles * (tiles + 1) / 2;
+  if (nblk <= 0) return hipSuccess;
+  UpdateArgs c = a;
+  c.tiles = tiles;
+  hipLaunchKernelGGL(update_kernel<T>, dim3((unsigned)nblk), dim3(kThreads), 0, s, c);
+  return hipGetLastError();
+}
+
+template hipError_t launch_update<double>(const UpdateArgs&, hipStream_t);
+template hipError_t launch_update<float>(const UpdateArgs&, hipStream_t);
+
+}  // namespace ltlt

@@ -1,0 +1,128 @@
+"""The C-ABI library loads and exports every symbol ``include/ltlt.h``
+declares; host-side argument checks reject bad calls before any GPU work.
+No compute call is made here (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2005_06410_amd as lt
+from paper_2005_06410_amd import build as ltbuild
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ltlt.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(ltlt_\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(lt.LIB_PATH):
+        ltbuild.build()
+    return lt.load()
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for must in ["ltlt_factor", "ltlt_factor_nb", "ltlt_pfaffian", "ltlt_factor_batched",
+                 "ltlt_skew_update", "ltlt_device_status", "ltlt_profile_enable",
+                 "ltlt_profile_read", "ltlt_release_workspace"]:
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+        assert isinstance(getattr(lib, name), ctypes._CFuncPtr)
+
+
+def test_binding_covers_every_declared_symbol():
+    assert set(declared_functions()) == set(lt._SYMBOLS)
+
+
+def test_library_is_built_for_gfx950_only():
+    out = os.popen(f"/opt/rocm/llvm/bin/clang-offload-bundler --list --type=o --input={lt.LIB_PATH} 2>/dev/null"
+                   ).read()
+    if not out.strip():
+        pytest.skip("offload bundle listing unavailable")
+    assert "gfx950" in out
+
+
+NULL = None
+
+
+@pytest.mark.parametrize("args,code", [
+    ((-1, 1, 1, 0, 1, 128, NULL), -1),          # n < 0
+    ((4, NULL, 4, 0, 1, 128, NULL), -2),        # A null
+    ((4, 1, 3, 0, 1, 128, NULL), -3),           # lda < n
+    ((4, 1, 4, 7, 1, 128, NULL), -4),           # bad dtype
+    ((4, 1, 4, 0, NULL, 128, NULL), -5),        # ipiv null
+    ((4, 1, 4, 0, 1, 0, NULL), -6),             # nb < 1
+    ((4, 1, 4, 0, 1, 257, NULL), -6),           # nb too wide
+    ((0, NULL, 1, 0, NULL, 128, NULL), 0),      # n = 0 is a no-op
+])
+def test_factor_argument_checks(lib, args, code):
+    assert lib.ltlt_factor_nb(*args) == code
+
+
+@pytest.mark.parametrize("args,code", [
+    ((65, 1, 1, 65, 65 * 65, 0, 1, 65, 1, 1, NULL), -1),     # n above the batched limit
+    ((4, -1, 1, 4, 16, 0, 1, 4, 1, 1, NULL), -2),            # batch < 0
+    ((4, 2, NULL, 4, 16, 0, 1, 4, 1, 1, NULL), -3),          # A null
+    ((4, 2, 1, 3, 16, 0, 1, 4, 1, 1, NULL), -4),             # lda < n
+    ((4, 2, 1, 4, 15, 0, 1, 4, 1, 1, NULL), -5),             # overlapping matrices
+    ((4, 2, 1, 4, 16, 2, 1, 4, 1, 1, NULL), -6),             # bad dtype
+    ((4, 2, 1, 4, 16, 0, NULL, 4, 1, 1, NULL), -7),          # ipiv null
+    ((4, 2, 1, 4, 16, 0, 1, 3, 1, 1, NULL), -8),             # pivot stride < n
+    ((4, 2, 1, 4, 16, 0, 1, 4, NULL, 1, NULL), -9),          # logabs null
+    ((4, 2, 1, 4, 16, 0, 1, 4, 1, NULL, NULL), -10),         # sign null
+    ((4, 0, NULL, 4, 16, 0, NULL, 4, NULL, NULL, NULL), 0),  # empty batch
+])
+def test_batched_argument_checks(lib, args, code):
+    assert lib.ltlt_factor_batched(*args) == code
+
+
+@pytest.mark.parametrize("args,code", [
+    ((-1, 1, 1, 0, 1, NULL, NULL, NULL), -1),
+    ((4, NULL, 4, 0, 1, 1, 1, NULL), -2),
+    ((4, 1, 2, 0, 1, 1, 1, NULL), -3),
+    ((4, 1, 4, 3, 1, 1, 1, NULL), -4),
+    ((4, 1, 4, 0, NULL, 1, 1, NULL), -5),
+    ((4, 1, 4, 0, 1, NULL, 1, NULL), -6),
+    ((4, 1, 4, 0, 1, 1, NULL, NULL), -7),
+])
+def test_pfaffian_argument_checks(lib, args, code):
+    assert lib.ltlt_pfaffian(*args) == code
+
+
+@pytest.mark.parametrize("args,code", [
+    ((-1, 1, 1, NULL, 1, 1, 1, 1, 1, 0, NULL), -1),
+    ((5, NULL, 5, NULL, 1, 1, 5, 1, 5, 0, NULL), -2),
+    ((5, 1, 4, NULL, 1, 1, 5, 1, 5, 0, NULL), -3),
+    ((5, 1, 5, NULL, -1, 1, 5, 1, 5, 0, NULL), -5),
+    ((5, 1, 5, NULL, 2, NULL, 5, 1, 5, 0, NULL), -6),
+    ((5, 1, 5, NULL, 2, 1, 4, 1, 5, 0, NULL), -7),
+    ((5, 1, 5, NULL, 2, 1, 5, NULL, 5, 0, NULL), -8),
+    ((5, 1, 5, NULL, 2, 1, 5, 1, 4, 0, NULL), -9),
+    ((5, 1, 5, NULL, 2, 1, 5, 1, 5, 9, NULL), -10),
+    ((1, 1, 1, NULL, 2, 1, 1, 1, 1, 0, NULL), 0),            # m < 2: nothing to update
+])
+def test_skew_update_argument_checks(lib, args, code):
+    assert lib.ltlt_skew_update(*args) == code
+
+
+def test_error_messages():
+    assert "argument 3" in str(lt.LtltError("f", -3))
+    assert "HIP runtime error 2" in str(lt.LtltError("f", -1002))
+    assert "not supported" in str(lt.LtltError("f", -2000))
+    assert "bounded wait" in str(lt.LtltError("f", -3000))
+
+
+def test_profile_enable_is_host_only(lib):
+    assert lib.ltlt_profile_enable(1) == 0
+    assert lib.ltlt_profile_enable(0) == 0

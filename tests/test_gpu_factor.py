@@ -1,0 +1,321 @@
+"""GPU parity of the blocked factorization, the Pfaffian and the trailing
+update against the CPU oracle (same seeded inputs, same precision).
+
+Inputs follow the workloads: Gaussian skew matrices (strict upper iid N(0,1)),
+graded ones (N(0,1) * 10^U(-3,3)), 4x4-block-diagonal ones, at sizes that
+span several panels and tiles with ragged tails, plus the full sizes
+n = 8192 and 16384 checked on sampled outputs (the first column steps against
+the oracle run for those steps only) and on size-independent properties."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from gpu_util import compare_factors, device_colmajor, gpu_factor, host_packed, residual_probe
+from truths import pf_closed4
+
+pytestmark = pytest.mark.gpu
+
+
+def lt():
+    import paper_2005_06410_amd as m
+    return m
+
+
+def check_pf(X, packed, ipiv, logabs, sign, dtype, ref_pf=None):
+    if ref_pf is None:
+        ref_pf = oracle.pfaffian_packed(packed.astype(dtype), ipiv)  # same factors, oracle arithmetic
+    rl, rs = ref_pf
+    assert sign == rs
+    if rs != 0:
+        assert abs(logabs - rl) <= 1e-9 * max(abs(rl), 1.0), (logabs, rl)
+
+
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("n,nb", [(3, 1), (4, 1), (5, 2), (8, 3), (17, 4), (33, 8), (64, 16), (100, 32),
+                                  (129, 128), (200, 64), (255, 7), (300, 128), (513, 64)])
+def test_parity_gauss_fp64(n, nb):
+    X = synth.skew_gauss(n, 100 + n)
+    packed, ipiv, logabs, sign, _ = gpu_factor(X, nb=nb)
+    info = compare_factors(X, packed, ipiv, np.float64)
+    assert info["first_pivot_mismatch"] == n
+    assert oracle.residual(X, packed, ipiv) <= 10
+    ref = oracle.pfaffian(X)
+    check_pf(X, packed, ipiv, logabs, sign, np.float64, ref)
+
+
+@pytest.mark.parametrize("n,nb", [(64, 8), (200, 32), (400, 128)])
+def test_parity_graded_fp64(n, nb):
+    X = synth.skew_graded(n, 7 + n)
+    packed, ipiv, logabs, sign, _ = gpu_factor(X, nb=nb)
+    compare_factors(X, packed, ipiv, np.float64)
+    assert oracle.residual(X, packed, ipiv) <= 10
+    check_pf(X, packed, ipiv, logabs, sign, np.float64, oracle.pfaffian(X))
+
+
+@pytest.mark.parametrize("n,nb", [(50, 16), (257, 128), (600, 128)])
+def test_parity_fp32(n, nb):
+    X = synth.skew_gauss(n, 55 + n).astype(np.float32)
+    packed, ipiv, logabs, sign, _ = gpu_factor(X, nb=nb)
+    compare_factors(X, packed, ipiv, np.float32)
+    assert oracle.residual(X, packed, ipiv) <= 10
+    # fp32 factors: log|Pf| against the fp64 oracle on the same (rounded) input
+    rl, rs = oracle.pfaffian(X.astype(np.float64))
+    assert sign == rs
+    if rs != 0:
+        assert abs(logabs - rl) <= 1e-4 * abs(rl)
+    else:
+        assert logabs == -math.inf
+
+
+def test_config_n256_b32():
+    X = synth.skew_gauss(256, 1)
+    packed, ipiv, logabs, sign, _ = gpu_factor(X, nb=32)
+    compare_factors(X, packed, ipiv, np.float64)
+    assert oracle.residual(X, packed, ipiv) <= 10
+    check_pf(X, packed, ipiv, logabs, sign, np.float64, oracle.pfaffian(X))
+
+
+def test_config_n2048_b64():
+    X = synth.skew_gauss(2048, 2)
+    packed, ipiv, logabs, sign, _ = gpu_factor(X, nb=64)
+    compare_factors(X, packed, ipiv, np.float64)
+    assert oracle.residual(X, packed, ipiv) <= 10
+    s, logdet = np.linalg.slogdet(X)
+    assert abs(2 * logabs - logdet) <= 1e-9 * abs(logdet)
+    check_pf(X, packed, ipiv, logabs, sign, np.float64, oracle.pfaffian(X))
+
+
+def test_config_n2048_blockdiag4():
+    n = 2048
+    X = synth.skew_blockdiag4(n, 3)
+    packed, ipiv, logabs, sign, _ = gpu_factor(X, nb=64)
+    compare_factors(X, packed, ipiv, np.float64)
+    ref_log, ref_sign = 0.0, 1
+    for b in range(n // 4):
+        pf = pf_closed4(X[4 * b:4 * b + 4, 4 * b:4 * b + 4])
+        ref_log += math.log(abs(pf))
+        ref_sign *= int(np.sign(pf))
+    assert sign == ref_sign
+    assert abs(logabs - ref_log) <= 1e-9 * abs(ref_log)
+    # zero columns: alpha exactly 0, no exchange, multipliers exactly 0
+    for b in range(n // 4 - 1):
+        k = 4 * b + 3
+        assert packed[k + 1, k] == 0.0 and ipiv[k + 1] == k + 1
+        assert np.all(packed[k + 2:, k] == 0.0)
+
+
+def _full_size_checks(X, nb, dtype, steps):
+    n = X.shape[0]
+    packed, ipiv, logabs, sign, _ = gpu_factor(X, nb=nb, dtype=dtype)
+    Xt = X.astype(dtype)
+    # sampled outputs: the first `steps` column steps against the oracle run for that many steps
+    pre, ipre = oracle.ltlt(Xt, nsteps=steps)
+    assert np.array_equal(ipiv[:steps + 1], ipre[:steps + 1])
+    from gpu_util import carry_rows
+    ref_cols = carry_rows(pre[:, :steps].astype(np.float64), ipiv, steps, n)
+    got = packed[:, :steps].astype(np.float64)
+    tol = 1e-10 if dtype == np.float64 else 1e-4
+    err = np.abs(got - ref_cols).max() / np.abs(ref_cols).max()
+    assert err <= tol, err
+    # properties at full size
+    L = np.tril(packed, -2)
+    assert np.abs(L).max() <= 1.0                      # every pivot was a column maximum
+    assert ipiv[0] == 0 and ipiv[n - 1] == n - 1 and np.all(ipiv >= np.arange(n))
+    assert np.all(np.isfinite(packed))
+    assert residual_probe(Xt, packed, ipiv) <= 10
+    return packed, ipiv, logabs, sign
+
+
+def test_config_n8192_graded_fp64():
+    X = synth.skew_graded(8192, 4)
+    packed, ipiv, logabs, sign = _full_size_checks(X, 128, np.float64, steps=24)
+    s, logdet = np.linalg.slogdet(X)
+    assert sign != 0 and abs(2 * logabs - logdet) <= 1e-9 * abs(logdet)
+
+
+def test_config_n8192_graded_fp32():
+    X = synth.skew_graded(8192, 4)
+    packed, ipiv, logabs, sign = _full_size_checks(X, 128, np.float32, steps=24)
+    s, logdet = np.linalg.slogdet(X.astype(np.float32).astype(np.float64))
+    assert abs(2 * logabs - logdet) <= 1e-4 * abs(logdet)
+
+
+def test_config_n16384_fp64():
+    X = synth.skew_gauss(16384, 5)
+    packed, ipiv, logabs, sign = _full_size_checks(X, 128, np.float64, steps=8)
+    # log|Pf| grows like (n/2)(ln sqrt(n) - 1/2): compare with det through the factors' size
+    assert sign in (-1, 1)
+    assert 2.0e4 < logabs < 5.0e4
+
+
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("n", [0, 1, 2, 3])
+def test_tiny_orders(n):
+    X = synth.skew_gauss(n, 9) if n else np.zeros((0, 0))
+    packed, ipiv, logabs, sign, _ = gpu_factor(X)
+    ref_p, ref_i = oracle.ltlt(X)
+    assert np.array_equal(ipiv, ref_i)
+    assert np.allclose(packed, ref_p, rtol=1e-14, atol=0)
+    if n == 2:
+        assert packed[1, 0] == X[1, 0]
+    ref = oracle.pfaffian(X)
+    assert sign == ref[1]
+    if ref[1]:
+        assert logabs == pytest.approx(ref[0], rel=1e-14, abs=1e-14)
+    else:
+        assert logabs == -math.inf
+
+
+def test_lda_larger_than_n_and_padding_untouched():
+    n, lda = 150, 163
+    X = synth.skew_gauss(n, 17)
+    packed, ipiv, logabs, sign, flat = gpu_factor(X, nb=32, lda=lda, fill=np.nan)
+    buf = flat.cpu().numpy().reshape(n, lda)
+    assert np.all(np.isnan(buf[:, n:]))                # rows n..lda-1 never touched
+    compare_factors(X, packed, ipiv, np.float64)
+
+
+@pytest.mark.parametrize("n,nb", [(130, 32), (700, 128)])
+def test_diagonal_and_upper_never_read_or_written(n, nb):
+    X = synth.skew_gauss(n, 18)
+    flat, A = device_colmajor(X)
+    A.diagonal().fill_(float("nan"))
+    up = torch.triu(torch.ones(n, n, dtype=torch.bool, device="cuda"), 1)
+    A.masked_fill_(up, float("inf"))                   # sentinels: must not be read
+    ipiv = lt().factor(A, nb=nb)
+    torch.cuda.synchronize()
+    assert torch.isnan(A.diagonal()).all()
+    assert torch.isinf(A[up]).all()                     # and not written
+    packed = host_packed(flat, n, n)
+    compare_factors(X, packed, ipiv.cpu().numpy(), np.float64)
+
+
+def test_row_major_tensor_is_rejected():
+    X = torch.zeros(8, 8, dtype=torch.float64, device="cuda")
+    with pytest.raises(ValueError):
+        lt().factor(X.t().contiguous())  # stride(0) = 8: row-major
+    with pytest.raises(ValueError):
+        lt().factor(X[:, :7].t())
+
+
+def test_zero_matrix_and_tridiagonal_input():
+    n = 70
+    packed, ipiv, logabs, sign, _ = gpu_factor(np.zeros((n, n)), nb=16)
+    assert np.all(packed == 0) and list(ipiv) == list(range(n)) and sign == 0
+    rng = synth.rng_for(19)
+    X = np.zeros((n, n))
+    X[np.arange(1, n), np.arange(n - 1)] = rng.standard_normal(n - 1)
+    X = X - X.T
+    packed, ipiv, logabs, sign, _ = gpu_factor(X, nb=16)
+    assert list(ipiv) == list(range(n))
+    assert np.array_equal(packed, np.tril(X, -1))
+
+
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+def test_exact_invariants_scaling_and_negation(dtype):
+    n = 300
+    X = synth.skew_gauss(n, 23).astype(dtype)
+    p0, i0, l0, s0, _ = gpu_factor(X, nb=64)
+    p1, i1, l1, s1, _ = gpu_factor(X * dtype(8.0), nb=64)
+    p2, i2, l2, s2, _ = gpu_factor(-X, nb=64)
+    sub = np.arange(1, n), np.arange(n - 1)
+    low = np.tril(np.ones((n, n), bool), -2)
+    assert np.array_equal(i0, i1) and np.array_equal(i0, i2)
+    assert np.array_equal(p1[sub], p0[sub] * dtype(8.0))
+    assert np.array_equal(p2[sub], -p0[sub])
+    assert np.array_equal(p1[low], p0[low]) and np.array_equal(p2[low], p0[low])
+
+
+def test_bitwise_deterministic():
+    X = synth.skew_graded(700, 29)
+    a = gpu_factor(X, nb=128)
+    b = gpu_factor(X, nb=128)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]) and a[2] == b[2]
+
+
+@pytest.mark.parametrize("nb", [1, 17, 64, 200, 256])
+def test_panel_widths(nb):
+    X = synth.skew_gauss(520, 31)
+    packed, ipiv, logabs, sign, _ = gpu_factor(X, nb=nb)
+    compare_factors(X, packed, ipiv, np.float64)
+
+
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("m,K,off,dtype", [(2, 1, 0, np.float64), (100, 5, 0, np.float64),
+                                           (129, 129, 7, np.float64), (300, 33, 20, np.float64),
+                                           (257, 17, 11, np.float32), (128, 4, 3, np.float32)])
+def test_skew_update_parity(m, K, off, dtype):
+    rng = synth.rng_for(m * 1000 + K)
+    N = m + off
+    S = synth.skew_gauss(N, m + K).astype(dtype)
+    Lx = rng.standard_normal((m, K)).astype(dtype)
+    Bt = rng.standard_normal((m, K)).astype(dtype)
+    # perm: identity on the block except a few rows that read from the `off`
+    # rows/columns before the block (as the panel's displaced indices do)
+    perm = np.arange(m, dtype=np.int32)
+    if off:
+        pos = rng.choice(m, size=min(off, m), replace=False)
+        perm[pos] = rng.choice(np.arange(-off, 0), size=len(pos), replace=False).astype(np.int32)
+    flat, Cv = device_colmajor(S)
+    Ld = torch.from_numpy(np.asfortranarray(Lx)).cuda()
+    Bd = torch.from_numpy(np.asfortranarray(Bt)).cuda()
+    Ld = Ld.t().contiguous().t()
+    Bd = Bd.t().contiguous().t()
+    pd = torch.from_numpy(perm).cuda()
+    lt().skew_update(Cv, Ld, Bd, perm=pd, offset=off)
+    torch.cuda.synchronize()
+    got = flat.cpu().numpy().reshape(N, N).T            # (i, j) indexing
+    Sfull = S.astype(np.float64)
+    ref_blk = oracle.skew_update(Sfull, np.pad(Lx.astype(np.float64), ((off, 0), (0, 0))),
+                                 np.pad(Bt.astype(np.float64), ((off, 0), (0, 0))),
+                                 np.concatenate([np.arange(off), perm + off]).astype(np.int64))
+    g = got[off:, off:].astype(np.float64)
+    r = ref_blk[off:, off:]
+    iu = np.triu_indices(m, 0)
+    il = np.tril_indices(m, -1)
+    tol = 1e-12 if dtype == np.float64 else 2e-5
+    scale = np.abs(r).max()
+    assert np.abs(g[il] - r[il]).max() <= tol * scale * max(1, K) ** 0.5
+    assert np.array_equal(got[off:, off:][iu], S[off:, off:][iu])   # diagonal and upper untouched
+    # outside the block nothing changed
+    assert np.array_equal(got[:off, :], S[:off, :]) and np.array_equal(got[:, :off], S[:, :off])
+
+
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("n,batch,dtype", [(64, 8192, np.float64), (64, 300, np.float32), (1, 5, np.float64),
+                                           (2, 5, np.float64), (7, 33, np.float64), (40, 129, np.float64)])
+def test_batched_parity(n, batch, dtype):
+    Xs = synth.skew_batch(n, batch, 6 << 32 if n == 64 else 99).astype(dtype)
+    ref_p, ref_i, ref_l, ref_s = oracle.ltlt_batched(Xs)
+    buf = np.ascontiguousarray(np.transpose(Xs, (0, 2, 1)))      # column-major per matrix
+    d = torch.from_numpy(buf).cuda()
+    A = d.as_strided((batch, n, n), (n * n, 1, n))
+    ipiv, logabs, sign = lt().factor_batched(A)
+    torch.cuda.synchronize()
+    got = np.tril(np.transpose(d.cpu().numpy(), (0, 2, 1)), -1)
+    gi = ipiv.cpu().numpy()
+    mism = 0
+    for b in range(batch):
+        if not np.array_equal(gi[b], ref_i[b]):
+            mism += 1
+            compare_factors(Xs[b].astype(dtype), got[b], gi[b], dtype)
+            continue
+        tol = 1e-10 if dtype == np.float64 else 1e-4
+        if n >= 2:
+            scale = np.abs(ref_p[b]).max()
+            assert np.abs(got[b].astype(np.float64) - ref_p[b]).max() <= tol * max(scale, 1e-300)
+    assert mism <= max(1, batch // 1000)
+    s = sign.cpu().numpy()
+    la = logabs.cpu().numpy()
+    assert np.array_equal(s, ref_s)
+    ok = ref_s != 0
+    rel = 1e-9 if dtype == np.float64 else 1e-4
+    assert np.all(np.abs(la[ok] - ref_l[ok]) <= rel * np.maximum(np.abs(ref_l[ok]), 1.0))
+    # upper triangle and diagonal untouched by the batched path
+    full = np.transpose(d.cpu().numpy(), (0, 2, 1))
+    iu = np.triu_indices(n, 0)
+    assert np.array_equal(full[:, iu[0], iu[1]], Xs[:, iu[0], iu[1]])
