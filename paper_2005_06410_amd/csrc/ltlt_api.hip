@@ -143,7 +143,7 @@ int factor_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, hipStream
   const size_t o_al = cv.take<T>((size_t)nb);
   const size_t o_T = cv.take<int>((size_t)std::max(nblk, 1) * n);
   const size_t o_GC = cv.take<int>((size_t)std::max(nblk, 1) * n);
-  const size_t o_rec = cv.take<uint64_t>((size_t)4 * (Pmax + 1));
+  const size_t o_rec = cv.take<uint64_t>((size_t)2 * 2 * (Pmax + 1));
   const size_t o_st = cv.take<T>(perm_stage_elems<T>(n, c_end));
 
   void* ws = nullptr;

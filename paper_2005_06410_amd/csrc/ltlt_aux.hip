@@ -100,10 +100,36 @@ __global__ void __launch_bounds__(256) perm_apply_kernel(T* A, int64_t lda, int 
     const int len = n - r0;
     if (len <= 0) continue;                    // uniform across the workgroup
     T* col = A + (int64_t)c * lda + r0;
-    for (int i = threadIdx.x; i < len; i += blockDim.x) buf[i] = col[i];
+    // 8 independent loads in flight per thread per round
+    constexpr int kU = 8;
+    for (int i0 = threadIdx.x; i0 < len; i0 += kU * blockDim.x) {
+      T v[kU];
+#pragma unroll
+      for (int e = 0; e < kU; ++e) {
+        const int i = i0 + e * blockDim.x;
+        v[e] = col[i < len ? i : 0];
+      }
+#pragma unroll
+      for (int e = 0; e < kU; ++e) {
+        const int i = i0 + e * blockDim.x;
+        if (i < len) buf[i] = v[e];
+      }
+    }
     __syncthreads();
     const int* g = G + (int64_t)J * n + r0;
-    for (int i = threadIdx.x; i < len; i += blockDim.x) col[i] = buf[g[i] - r0];
+    for (int i0 = threadIdx.x; i0 < len; i0 += kU * blockDim.x) {
+      int src[kU];
+#pragma unroll
+      for (int e = 0; e < kU; ++e) {
+        const int i = i0 + e * blockDim.x;
+        src[e] = g[i < len ? i : 0] - r0;
+      }
+#pragma unroll
+      for (int e = 0; e < kU; ++e) {
+        const int i = i0 + e * blockDim.x;
+        if (i < len) col[i] = buf[src[e]];
+      }
+    }
     __syncthreads();
   }
 }

@@ -57,4 +57,34 @@ __device__ __forceinline__ void wave_argmax(double& bv, int& bi) {
   }
 }
 
+// One DPP step of a wave-wide (|value|, index) max: every lane merges the
+// pair of the lane selected by CTRL; lanes without a source (row edges,
+// masked rows) merge the identity (-1, INT32_MAX).
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ void dpp_argmax_step(double& v, int& i) {
+  const int lo = __double2loint(v), hi = __double2hiint(v);
+  const int ilo = __double2loint(-1.0), ihi = __double2hiint(-1.0);
+  const int olo = __builtin_amdgcn_update_dpp(ilo, lo, CTRL, ROW_MASK, 0xF, false);
+  const int ohi = __builtin_amdgcn_update_dpp(ihi, hi, CTRL, ROW_MASK, 0xF, false);
+  const int oi = __builtin_amdgcn_update_dpp(INT32_MAX, i, CTRL, ROW_MASK, 0xF, false);
+  const double ov = __hiloint2double(ohi, olo);
+  if (ov > v || (ov == v && oi < i)) { v = ov; i = oi; }
+}
+
+// Wave-wide argmax through DPP row shifts and row broadcasts (no LDS
+// permutes): the result is complete in lane 63 and returned to all lanes.
+// Values must be >= -1 and not NaN (callers map NaN to -1: not a candidate).
+__device__ __forceinline__ void wave_argmax_dpp(double& v, int& i) {
+  dpp_argmax_step<0x111, 0xF>(v, i);   // row_shr:1
+  dpp_argmax_step<0x112, 0xF>(v, i);   // row_shr:2
+  dpp_argmax_step<0x114, 0xF>(v, i);   // row_shr:4
+  dpp_argmax_step<0x118, 0xF>(v, i);   // row_shr:8   -> lane 15 of each row holds the row's result
+  dpp_argmax_step<0x142, 0xA>(v, i);   // row_bcast:15 into rows 1 and 3
+  dpp_argmax_step<0x143, 0xC>(v, i);   // row_bcast:31 into rows 2 and 3 -> lane 63 complete
+  const int lo = __builtin_amdgcn_readlane(__double2loint(v), 63);
+  const int hi = __builtin_amdgcn_readlane(__double2hiint(v), 63);
+  v = __hiloint2double(hi, lo);
+  i = __builtin_amdgcn_readlane(i, 63);
+}
+
 }  // namespace ltlt

@@ -58,7 +58,7 @@ size_t panel_lds_bytes(int bw, int R) {
   const int S = kThreads / R;
   size_t t = 0;
   t += (size_t)S * kCpt * sizeof(T);              // g, split by lane part
-  t += (size_t)(bw + 1) * sizeof(T) * 2;          // alpha, lrow
+  t += (size_t)(bw + 1) * sizeof(T) * 3;          // alpha, lrow, oldrow
   t += (size_t)R * (bw + 1) * sizeof(T);          // multipliers gathered for the outputs
   return t + 64;
 }
@@ -70,6 +70,7 @@ size_t panel_lds_bytes(int bw, int R) {
 // every step of its slot, so a slot holds stamp s or s-2 and the epoch bit
 // alone tells them apart in word A; word B carries the full stamp.
 constexpr uint64_t kIdxNone = 0x1FFFFFull;
+constexpr int kRecWords = 2;    // records packed: 8 per 128-byte line, one wave poll touches few lines
 __device__ __forceinline__ uint64_t rec_a(double absv, int s) {
   return (uint64_t)__double_as_longlong(absv) | ((uint64_t)((s >> 1) & 1) << 63);
 }
@@ -115,12 +116,13 @@ __global__ void __launch_bounds__(kThreads, 1) panel_kernel(PanelArgs a) {
   const T* A = static_cast<const T*>(a.A);
   T* G = static_cast<T*>(a.G);
 
-  T *gp, *alpha, *lrow, *dump;
+  T *gp, *alpha, *lrow, *oldrow, *dump;
   {
     unsigned char* p = smem;
     gp = reinterpret_cast<T*>(p); p += (size_t)S * kCpt * sizeof(T);
     alpha = reinterpret_cast<T*>(p); p += (size_t)(bw + 1) * sizeof(T);
     lrow = reinterpret_cast<T*>(p); p += (size_t)(bw + 1) * sizeof(T);
+    oldrow = reinterpret_cast<T*>(p); p += (size_t)(bw + 1) * sizeof(T);
     dump = reinterpret_cast<T*>(p);
   }
   __shared__ double red_v[kThreads / kWave];
@@ -170,20 +172,23 @@ __global__ void __launch_bounds__(kThreads, 1) panel_kernel(PanelArgs a) {
     // ---- local pivot candidate ----
     double bv = -1.0;
     int bi = INT32_MAX;
-    if (active) { bv = (double)fabs(cv); bi = my_i; }
-    wave_argmax(bv, bi);
+    if (active) {
+      const double av = (double)fabs(cv);
+      if (av == av) { bv = av; bi = my_i; }       // NaN is never a candidate
+    }
+    wave_argmax_dpp(bv, bi);
     if (bi == INT32_MAX) {
       if (lane == 0) { red_v[wave] = -1.0; red_i[wave] = INT32_MAX; }
     } else if (my_i == bi && part == 0) {         // the candidate's own lane
       red_v[wave] = bv; red_i[wave] = bi; red_c[wave] = cv; red_p[wave] = pos;
     }
     const int s = k + 1;
-    uint64_t* recs = a.rec + (size_t)(s & 1) * (size_t)(a.kslot + 1) * 2;
-    if (my_i == k + 1 && my_row && part == 0) {   // owner of position k+1 publishes it
-      st_coh64(&recs[2 * a.kslot + 0], rec_a((double)fabs(cv), s));
-      st_coh64(&recs[2 * a.kslot + 1], rec_b(s, cv < T(0) ? 1 : 0, pos, (uint64_t)(k + 1)));
-    }
+    uint64_t* recs = a.rec + (size_t)(s & 1) * (size_t)(a.kslot + 1) * kRecWords;
     wait_stores();                                // this wave's earlier G stores are complete
+    if (my_i == k + 1 && my_row && part == 0) {   // owner of position k+1 publishes it
+      st_coh64(&recs[kRecWords * a.kslot + 0], rec_a((double)fabs(cv), s));
+      st_coh64(&recs[kRecWords * a.kslot + 1], rec_b(s, cv < T(0) ? 1 : 0, pos, (uint64_t)(k + 1)));
+    }
     __syncthreads();
     // ---- publish this workgroup's candidate (lane 0 of wave 0) ----
     if (tid == 0) {
@@ -195,11 +200,11 @@ __global__ void __launch_bounds__(kThreads, 1) panel_kernel(PanelArgs a) {
         if (ov > cb || (ov == cb && oi < ci)) { cb = ov; ci = oi; cw = wv; }
       }
       if (ci == INT32_MAX) {
-        st_coh64(&recs[2 * w + 0], rec_a(0.0, s));
-        st_coh64(&recs[2 * w + 1], rec_b(s, 0, 0, kIdxNone));
+        st_coh64(&recs[kRecWords * w + 0], rec_a(0.0, s));
+        st_coh64(&recs[kRecWords * w + 1], rec_b(s, 0, 0, kIdxNone));
       } else {
-        st_coh64(&recs[2 * w + 0], rec_a(cb, s));
-        st_coh64(&recs[2 * w + 1], rec_b(s, red_c[cw] < T(0) ? 1 : 0, red_p[cw], (uint64_t)ci));
+        st_coh64(&recs[kRecWords * w + 0], rec_a(cb, s));
+        st_coh64(&recs[kRecWords * w + 1], rec_b(s, red_c[cw] < T(0) ? 1 : 0, red_p[cw], (uint64_t)ci));
       }
     }
     // ---- poll all records and reduce (wave 0); entry u == P is position k+1 ----
@@ -215,8 +220,8 @@ __global__ void __launch_bounds__(kThreads, 1) panel_kernel(PanelArgs a) {
           const int ri = (u < P) ? u : a.kslot;
           uint64_t ra, rb;
           for (;;) {
-            ra = ld_coh64(&recs[2 * ri + 0]);
-            rb = ld_coh64(&recs[2 * ri + 1]);
+            ra = ld_coh64(&recs[kRecWords * ri + 0]);
+            rb = ld_coh64(&recs[kRecWords * ri + 1]);
             if (rec_valid(ra, rb, s)) break;
             if (wall_ticks() - t0 > kWaitLimitTicks || ld_coh(a.status) != 0) {
               atomicOr(a.status, 1);
@@ -242,13 +247,15 @@ __global__ void __launch_bounds__(kThreads, 1) panel_kernel(PanelArgs a) {
       kabs = __shfl(kabs, klane, kWave);
       kpos = __shfl(kpos, klane, kWave);
       ksg = __shfl(ksg, klane, kWave);
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) {
-        const double ov = __shfl_xor(gv, off, kWave);
-        const int oi = __shfl_xor(gi, off, kWave);
-        const int op = __shfl_xor(gpos, off, kWave);
-        const int os = __shfl_xor(gsg, off, kWave);
-        if (ov > gv || (ov == gv && oi < gi)) { gv = ov; gi = oi; gpos = op; gsg = os; }
+      {
+        // wave argmax on (|value|, position); the winning lane then supplies
+        // the block-start index and sign of the winner
+        const int my_gi = gi;
+        wave_argmax_dpp(gv, gi);
+        const unsigned long long hit = __ballot(gi != INT32_MAX && my_gi == gi);
+        const int src = hit ? __ffsll(hit) - 1 : 0;
+        gpos = __shfl(gpos, src, kWave);
+        gsg = __shfl(gsg, src, kWave);
       }
       if (lane == 0) {
         const T ck = ksg ? -(T)kabs : (T)kabs;
@@ -272,26 +279,24 @@ __global__ void __launch_bounds__(kThreads, 1) panel_kernel(PanelArgs a) {
     if (is_p) pos = posk;                         // the row leaving k+1 lands at p
     if (is_k1) pos = posw;
     if (my_row && part == 0 && my_i >= k + 2) lv = skew_at(A, lda, pos, posw);
-    if (tid < t) lrow[tid] = ld_coh_t(&G[(int64_t)(posw - (j + 1)) + (int64_t)tid * ldw]);
+    // the pivot row's multipliers (all workgroups) and, in the workgroup that
+    // owns p, those of the row leaving k+1: one value per thread, one round
+    const bool wg_owns_p = (p != k + 1) && p >= row0 && p < row0 + rows_here;
+    if (tid < t) {
+      lrow[tid] = ld_coh_t(&G[(int64_t)(posw - (j + 1)) + (int64_t)tid * ldw]);
+      if (wg_owns_p) oldrow[tid] = ld_coh_t(&G[(int64_t)(posk - (j + 1)) + (int64_t)tid * ldw]);
+    }
+    __syncthreads();
     if (is_p) {
-      const T* src = G + (int64_t)(posk - (j + 1));
 #pragma unroll
       for (int c = 0; c < kCpt; ++c) {
         const int u = c * S + part;
-        if (u < t) L[c] = ld_coh_t(&src[(int64_t)u * ldw]);
+        L[c] = u < t ? oldrow[u < t ? u : 0] : T(0);
       }
       cv = cvk;
     }
-    __syncthreads();
-    // ---- the pivot row takes position k+1; multipliers of step k ----
-    if (is_k1) {
-#pragma unroll
-      for (int c = 0; c < kCpt; ++c) {
-        const int u = c * S + part;
-        if (u < t) L[c] = lrow[u];
-      }
-      cv = alph;
-    }
+    // ---- multipliers of step k (the row now at k+1 is final: its
+    //      multipliers are taken from G for the output) ----
     if (my_row && my_i >= k + 2) {
       const T l = (alph != T(0)) ? cv / alph : T(0);
       const int cslot = t / S;
@@ -321,21 +326,30 @@ __global__ void __launch_bounds__(kThreads, 1) panel_kernel(PanelArgs a) {
     __syncthreads();
   }
 
-  // ---- outputs: multipliers through LDS (Bt needs neighbouring columns) ----
-  for (int e = tid; e < R * (bw + 1); e += kThreads) dump[e] = T(0);
+  // ---- outputs: multipliers through LDS (Bt needs neighbouring columns).
+  //      Rows still active hold every multiplier in registers; the final
+  //      pivot rows (positions j+1 .. j+bw) read theirs from G, whose entries
+  //      all predate the last exchange. ----
+  wait_stores();
   __syncthreads();
+  const int tr0 = j + bw + 1;                      // first trailing position
   if (my_row) {
+    if (my_i >= tr0) {
 #pragma unroll
-    for (int c = 0; c < kCpt; ++c) {
-      const int u = c * S + part;
-      if (u < bw) dump[u * R + rloc] = L[c];
+      for (int c = 0; c < kCpt; ++c) {
+        const int u = c * S + part;
+        if (u < bw) dump[u * R + rloc] = L[c];
+      }
+      if (part == 0) dump[bw * R + rloc] = cv;    // carry
+    } else {
+      const T* src = G + (int64_t)(pos - (j + 1));
+      for (int u = part; u < bw; u += S) dump[u * R + rloc] = ld_coh_t(&src[(int64_t)u * ldw]);
+      if (part == 0) dump[bw * R + rloc] = T(0);
     }
-    if (part == 0) dump[bw * R + rloc] = cv;      // carry (rows >= j+bw+1)
   }
   __syncthreads();
   T* PO = static_cast<T*>(a.PO);
   T* Bm = static_cast<T*>(a.Bm);
-  const int tr0 = j + bw + 1;                      // first trailing position
   for (int r = tid; r < rows_here; r += kThreads) {
     const int ii = row0 + r;
     const int64_t ro = ii - (j + 1);
@@ -430,14 +444,14 @@ int panel_rows(int bw) { return kThreads / panel_split(bw); }
 // (slot 1 first holds s = 1, epoch 0; slot 0 first holds s = 2, epoch 1).
 __global__ void rec_init_kernel(uint64_t* rec, int nrec) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= 4 * nrec) return;
-  const int slot = i / (2 * nrec);
-  const int word = i & 1;
+  if (i >= 2 * kRecWords * nrec) return;
+  const int slot = i / (kRecWords * nrec);
+  const int word = i % kRecWords;
   rec[i] = (word == 0 && slot == 1) ? (1ull << 63) : 0ull;
 }
 
 hipError_t launch_rec_init(uint64_t* rec, int nrec_per_slot, hipStream_t s) {
-  const int tot = 4 * nrec_per_slot;
+  const int tot = 2 * kRecWords * nrec_per_slot;
   hipLaunchKernelGGL(rec_init_kernel, dim3((tot + 255) / 256), dim3(256), 0, s, rec, nrec_per_slot);
   return hipGetLastError();
 }

@@ -84,11 +84,77 @@ __device__ __forceinline__ void store_chunk(T* __restrict__ S, const T (&reg)[8]
   for (int e = 0; e < 8; ++e) S[col * kMT + rr + e] = reg[e];
 }
 
+// Old values S(perm[i], perm[c]) of one 16-column slice for the lane's row i
+// (strict lower triangle only; other entries read the valid C(1,0) and are
+// discarded).  The sources never change during the update: they are either
+// the tile's own entries or lie outside the block being written.
+template <typename T>
+__device__ __forceinline__ void gather_slice(const T* __restrict__ C, int64_t ldc, int m, int i, int pr,
+                                             const int* pcol, int c0, int cl0, T (&out)[16]) {
+#pragma unroll
+  for (int cc = 0; cc < 16; ++cc) {
+    const int cl = cl0 + cc;
+    const int c = c0 + cl;
+    const int pc = pcol[cl];
+    const bool in = (i > c) && (i < m);
+    const bool low = pr > pc;   // S(pr, pc) = C(pr,pc), or -C(pc,pr) above the diagonal
+    int64_t off = low ? (int64_t)pr + (int64_t)pc * ldc : (int64_t)pc + (int64_t)pr * ldc;
+    off = in ? off : 1;
+    const T val = C[off];
+    out[cc] = low ? val : -val;
+  }
+}
+
+// Tile scheduling.  Workgroups are dispatched round-robin over the 8 XCDs
+// (block b runs on XCD b % 8) and each XCD has its own L2.  The lower-
+// triangular tile set is enumerated in groups of kGrp x kGrp tiles (tiles of
+// a group share kGrp row blocks of Lx and kGrp column blocks of Bt), and XCD x
+// is given the x-th contiguous eighth of that order, so the workgroups resident
+// on one XCD work through the same few groups and their operands stay in
+// that XCD's L2.
+constexpr int kXcd = 8;
+constexpr int kGrp = 8;
+
+__device__ __forceinline__ int tri_index_decode(int b, int& J) {
+  int I = (int)((sqrt(8.0 * (double)b + 1.0) - 1.0) * 0.5);
+  while ((I + 1) * (I + 2) / 2 <= b) ++I;
+  while (I * (I + 1) / 2 > b) --I;
+  J = b - I * (I + 1) / 2;
+  return I;
+}
+
+__device__ __forceinline__ void tile_of_block(int b, int nblocks, int tiles, int& I, int& J) {
+  // position of block b in the XCD-major order
+  const int x = b % kXcd, l = b / kXcd;
+  const int per = nblocks / kXcd, extra = nblocks % kXcd;
+  const int q = x * per + min(x, extra) + l;       // XCD x owns [x*per + min(x,extra), +per + (x<extra))
+  // q-th tile of the grouped order: groups (GI, GJ), GJ <= GI, row-major; full
+  // groups hold kGrp*kGrp tiles, diagonal groups kGrp(kGrp+1)/2, edge groups fewer
+  const int ng = (tiles + kGrp - 1) / kGrp;
+  int rem = q;
+  for (int GI = 0; GI < ng; ++GI) {
+    const int hI = min(kGrp, tiles - GI * kGrp);   // row blocks in this group row
+    for (int GJ = 0; GJ <= GI; ++GJ) {
+      const int wJ = min(kGrp, tiles - GJ * kGrp);
+      const int cnt = (GJ < GI) ? hI * wJ : hI * (hI + 1) / 2;
+      if (rem < cnt) {
+        if (GJ < GI) { I = GI * kGrp + rem / wJ; J = GJ * kGrp + rem % wJ; }
+        else { int jj; const int ii = tri_index_decode(rem, jj); I = GI * kGrp + ii; J = GI * kGrp + jj; }
+        return;
+      }
+      rem -= cnt;
+    }
+  }
+  I = 0; J = 0;                                    // not reached for q < number of tiles
+}
+
 template <typename T>
 __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
   typedef typename Mfma<T>::acc_t acc_t;
-  __shared__ __align__(16) T As[2][kKC * kMT];
-  __shared__ __align__(16) T Bs[2][kKC * kMT];
+  // operand chunks As[2][kKC*kMT], Bs[2][kKC*kMT]; reused by the epilogue
+  __shared__ __align__(16) T lds[4 * kKC * kMT];
+  T (*As)[kKC * kMT] = reinterpret_cast<T (*)[kKC * kMT]>(lds);
+  T (*Bs)[kKC * kMT] = reinterpret_cast<T (*)[kKC * kMT]>(lds + 2 * kKC * kMT);
   __shared__ int prow[kMT], pcol[kMT];
 
   const int tid = threadIdx.x;
@@ -96,12 +162,8 @@ __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
   const int wave = tid >> 6;
   const int wr = wave >> 1, wc = wave & 1;
 
-  // triangular decode: blockIdx.x = I(I+1)/2 + J, J <= I
-  const int b = blockIdx.x;
-  int I = (int)((sqrt(8.0 * (double)b + 1.0) - 1.0) * 0.5);
-  while ((I + 1) * (I + 2) / 2 <= b) ++I;
-  while (I * (I + 1) / 2 > b) --I;
-  const int J = b - I * (I + 1) / 2;
+  int I, J;
+  tile_of_block(blockIdx.x, gridDim.x, a.tiles, I, J);
   const int r0 = I * kMT, c0 = J * kMT;
   const int m = a.m, K = a.K;
 
@@ -125,6 +187,15 @@ __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
     pcol[tid] = (a.perm && ci < m) ? a.perm[ci] - a.perm_base : ci;
   }
   __syncthreads();
+
+  // epilogue geometry: lane l of wave (wr, wc) finishes row wr*64 + l of the tile
+  T* C = static_cast<T*>(a.C);
+  const int64_t ldc = a.ldc;
+  const int rl = wr * 64 + lane;
+  const int i = r0 + rl;
+  const int pr = prow[rl];
+  T oldv[16];
+  gather_slice<T>(C, ldc, m, i, pr, pcol, c0, wc * 64, oldv);   // slice 0, in flight during the K loop
 
   const int nchunk = (K + kKC - 1) / kKC;
   for (int ch = 0; ch < nchunk; ++ch) {
@@ -156,27 +227,36 @@ __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
     __syncthreads();
   }
 
-  // ---- epilogue: gather old value, add, write lower entry and mirror ----
-  T* C = static_cast<T*>(a.C);
-  const int64_t ldc = a.ldc;
+  // ---- epilogue: stage through LDS, then coalesced add/store ----
+  // The MFMA output layout spreads a lane's values over 4 rows x 16 columns,
+  // which would make every global access touch 16 partial lines.  Each wave
+  // instead writes one 16-column slice of its 64x64 sub-tile to LDS
+  // ([column][row], padded), then lane l handles row l of each column: every
+  // load/store instruction covers 64 consecutive rows of one column.  The old
+  // values of slice 0 were gathered before the K loop; those of slice y+1 are
+  // gathered while slice y is finished.
+  constexpr int kEp = 65;                          // padded column stride in LDS
+  static_assert(4 * 16 * kEp <= 4 * kKC * kMT, "epilogue staging must fit the operand LDS");
+  T* stage = lds + wave * (16 * kEp);              // 16 columns x 65 per wave
 #pragma unroll
-  for (int x = 0; x < 4; ++x) {
+  for (int y = 0; y < 4; ++y) {
 #pragma unroll
-    for (int y = 0; y < 4; ++y) {
-      const int cl = wc * 64 + y * 16 + (lane & 15);
-      const int c = c0 + cl;
-      const int pc = pcol[cl];
+    for (int x = 0; x < 4; ++x)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int rl = wr * 64 + x * 16 + Mfma<T>::row(lane, v);
-        const int i = r0 + rl;
-        if (i > c && i < m) {
-          const int pr = prow[rl];
-          // S(pr, pc) from the strict lower triangle: A(pr,pc) or -A(pc,pr)
-          const T old = pr > pc ? C[(int64_t)pr + (int64_t)pc * ldc] : -C[(int64_t)pc + (int64_t)pr * ldc];
-          C[(int64_t)i + (int64_t)c * ldc] = old + acc[x][y][v];
-        }
-      }
+      for (int v = 0; v < 4; ++v)
+        stage[(lane & 15) * kEp + x * 16 + Mfma<T>::row(lane, v)] = acc[x][y][v];
+    __builtin_amdgcn_s_waitcnt(0xc07f);            // lgkmcnt(0): this wave's LDS writes done
+    T nextv[16];
+    if (y < 3) gather_slice<T>(C, ldc, m, i, pr, pcol, c0, wc * 64 + (y + 1) * 16, nextv);
+#pragma unroll
+    for (int cc = 0; cc < 16; ++cc) {
+      const int c = c0 + wc * 64 + y * 16 + cc;
+      if ((i > c) && (i < m)) C[(int64_t)i + (int64_t)c * ldc] = oldv[cc] + stage[cc * kEp + lane];
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);            // reads of this slice done before it is overwritten
+    if (y < 3) {
+#pragma unroll
+      for (int cc = 0; cc < 16; ++cc) oldv[cc] = nextv[cc];
     }
   }
 }
