@@ -130,7 +130,7 @@ int factor_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, hipStream
     if (R == 0) return LTLT_ERR_UNSUPPORTED;
     const size_t lds = panel_lds_bytes<T>(bw0, R);
     Pmax = (n - 1 + R - 1) / R;
-    const int cap = panel_max_blocks<T>(R, lds);
+    const int cap = panel_max_blocks<T>(bw0, lds);
     if (cap <= 0 || Pmax > cap) return LTLT_ERR_UNSUPPORTED;
   }
 
@@ -143,7 +143,8 @@ int factor_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, hipStream
   const size_t o_al = cv.take<T>((size_t)nb);
   const size_t o_T = cv.take<int>((size_t)std::max(nblk, 1) * n);
   const size_t o_GC = cv.take<int>((size_t)std::max(nblk, 1) * n);
-  const size_t o_rec = cv.take<uint64_t>((size_t)2 * 2 * (Pmax + 1));
+  const int nrec = Pmax;                      // exchange records per slot
+  const size_t o_rec = cv.take<uint64_t>((size_t)2 * kRecStride * nrec);
   const size_t o_st = cv.take<T>(perm_stage_elems<T>(n, c_end));
 
   void* ws = nullptr;
@@ -163,7 +164,7 @@ int factor_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, hipStream
   {
     ProfScope ps(3, 0.0, s);
     e = launch_init(ipiv, n, status, s);
-    if (e == hipSuccess && nblk > 0) e = launch_rec_init(rec, Pmax + 1, s);
+    if (e == hipSuccess && nblk > 0) e = launch_rec_init(rec, nrec, s);
   }
   if (e != hipSuccess) return hip_err(e);
 
@@ -175,7 +176,7 @@ int factor_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, hipStream
     pa.A = A; pa.lda = lda; pa.n = n; pa.j = j; pa.bw = bw;
     pa.R = choose_rows<T>(bw);
     pa.P = (m + pa.R - 1) / pa.R;
-    pa.kslot = Pmax;
+    pa.nrec = nrec;
     pa.G = Gm; pa.PO = PO; pa.Bm = Bm; pa.ldw = ldw; pa.alpha = al;
     pa.perm = Tblk + (int64_t)J * n;
     pa.ipiv = ipiv;

@@ -6,8 +6,12 @@
 
 namespace ltlt {
 
-constexpr int kThreads = 256;        // workgroup size of the panel and update kernels
+constexpr int kThreads = 256;        // workgroup size of the update kernel
 constexpr int kMaxNb = 256;          // widest panel
+constexpr int kPanelThreads = 512;          // workgroup size of the panel kernel
+constexpr int kPanelWaves = kPanelThreads / 64;   // waves per panel workgroup
+constexpr int kMaxPanelRecords = 256;       // exchange records one poll covers (4 per lane)
+constexpr int kRecStride = 32;              // 64-bit words from one exchange record to the next (256 bytes)
 
 // Arguments of one panel launch (block of steps k = j .. j+bw-1).
 struct PanelArgs {
@@ -18,7 +22,7 @@ struct PanelArgs {
   int bw;             // steps in the block
   int R;              // rows per workgroup
   int P;              // workgroups
-  int kslot;          // record index of the position-(k+1) record (>= every P of the factorization)
+  int nrec;           // exchange records per slot (>= P of every block)
   void* G;            // multipliers by block-start index: G[(idx - j - 1) + u*ldw]
   void* PO;           // panel out, rows j+1.., columns 0..bw (bw = carry), ld = ldw
   void* Bm;           // Bt = Lx Tx^T for rows >= j+bw+1, columns 0..bw, ld = ldw
@@ -26,7 +30,7 @@ struct PanelArgs {
   void* alpha;        // alpha_{j+t}, t < bw
   int* perm;          // perm[i] for positions i >= j+1: index held at block start
   int* ipiv;
-  uint64_t* rec;      // exchange records [2][kslot+1][2]
+  uint64_t* rec;      // exchange records [2][nrec][kRecStride] (words 0, 1 used)
   int* status;        // nonzero: a bounded wait gave up
 };
 
@@ -62,7 +66,7 @@ template <typename T> hipError_t launch_batched(int n, int batch, T* A, int64_t 
 hipError_t launch_init(int* ipiv, int n, int* status, hipStream_t s);
 hipError_t launch_rec_init(uint64_t* rec, int nrec_per_slot, hipStream_t s);
 hipError_t launch_perm_chain(const int* Tblk, int nb, int nblk, int n, int* G, hipStream_t s);
-template <typename T> int panel_max_blocks(int R, size_t lds);
+template <typename T> int panel_max_blocks(int bw, size_t lds);
 int panel_rows(int bw);
 
 }  // namespace ltlt

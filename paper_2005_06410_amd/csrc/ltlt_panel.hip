@@ -1,19 +1,28 @@
 // Panel kernel: the column steps k = j .. j+bw-1 of one block of the pivoted
 // skew-symmetric reduction P X P^T = L T L^T, run by P co-resident
-// workgroups that each own R consecutive positions (rows) of the block.
+// workgroups that together hold every row of the block (positions j+1..n-1).
 //
-// Thread layout: 256 threads per workgroup, S adjacent lanes per row
-// (R = 256/S rows), lane part p of a row holds the row's multipliers of the
-// steps u with u % S == p in registers (L[c] = multiplier of step j + c*S + p,
-// c < kCpt).  Per-row state (block-start index pos, current column value cv)
-// is replicated in the S lanes of the row.
+// Thread layout: 512 threads (8 waves, two per SIMD) per workgroup, S lanes
+// per row (S = 1, 2, 4 for blocks of up to 64, 128, 256 steps): the wave is
+// split into S parts of 64/S consecutive lanes, part p holds the steps u with
+// u % S == p of the same 64/S rows, so R = 512/S rows per workgroup and every
+// 16-lane row of the wave belongs to one part.  A lane keeps its row's
+// multipliers in registers: L[c] = multiplier of step j + c*S + p, c < 64.
+//
+// Rows never move between lanes.  Lane rows are the rows of the block-start
+// matrix (block-start index `pos`, fixed); an exchange of positions k+1 and p
+// only swaps the logical positions `lp` of the two lanes that hold them.  The
+// row at position k+1 after the exchange is final from then on; the other one
+// keeps its multipliers and column value where they are.
 //
 // A copy of the multipliers also lives in global memory, indexed by the
-// block-start index (so it never needs reordering): G[pos - (j+1)][u].
+// block-start index, G[pos - (j+1)][u]: every lane needs the pivot row's
+// multipliers of the earlier steps, and it is the only data that crosses
+// workgroups besides the exchange records.
 //
 // Column refresh.  The trailing matrix is stored as it was at block start
 // (strict lower triangle), so the current column k is the stored column of
-// index pos[k] gathered through pos[], plus the not-yet-applied updates of
+// the block-start index of position k, plus the not-yet-applied updates of
 // steps j .. k-2.  Step s updates X(i,c) += l_i v_c - v_i l_c with v the
 // column s+1 at step s, and v = alpha_{s+1} * L(:, s+2) below row s+2
 // (column s+1 is the one step s+1 eliminates).  Summed over the block this is
@@ -23,54 +32,60 @@
 //   g_u = alpha_{j+u+1} Lrow[u+1] [u <= t-2] - alpha_{j+u} Lrow[u-1] [u >= 1],
 //   Lrow[w] = Lp[w][k] (w <= t-2), Lrow[t-1] = 1 (unit diagonal of L),
 // with S(a, b) = A(a, b) for a > b and -A(b, a) for a < b.
+// The g coefficients live in registers in "row broadcast" layout: register
+// gr[k], lane l holds g of slot 16k + (l % 16) of the lane's step slice, the
+// same in each 16-lane row of that slice, and the refresh multiplies slot c
+// by lane c % 16 of its own row through a DPP row broadcast, so no lane reads
+// g from LDS.
 //
 // Exchange per step (one grid-wide round, no counters, no fences): every
-// workgroup publishes its local pivot candidate as one 16-byte record of two
-// self-validating 64-bit words (each carries the step stamp), and the owner
-// of position k+1 publishes that position the same way.  Wave 0 of every
-// workgroup polls all records until each carries the current stamp, then
-// reduces them in the same order (largest magnitude, then smallest position:
-// the first maximum in position order), so all agree on the pivot p.  The
-// pivot row's multipliers (and, for the owner of p, those of the row leaving
-// k+1) are read from G together with the next stored column, in one round of
-// loads.  Multipliers written to G at step k are read no earlier than step
-// k+1; each workgroup waits for its own earlier stores to complete before
-// publishing the record of the following step, so any record that validates
-// implies those stores are visible.
+// workgroup merges the candidates of its waves and publishes the result as
+// one record of two self-validating 64-bit words (each carries the step
+// stamp); records sit 256 bytes apart.  Wave 0 of every workgroup polls all
+// records until each carries the current stamp and reduces them (largest
+// magnitude, then smallest position: the first maximum in position order), so
+// all workgroups agree on the pivot p.  A barrier hands the result to the
+// other waves; from there each wave works alone: it loads the pivot row's
+// multipliers from G into its own LDS area, forms the g coefficients of the
+// next step and refreshes its rows.  Multipliers written to G at step k are
+// read no earlier than step k+1; every wave waits for its own earlier stores
+// to complete before the barrier that precedes the publication of the next
+// record, so any record that validates implies that the winning row's
+// multipliers are visible.
 //
 // After the last step the carry column (column j+bw, refreshed) is formed and
-// the block's outputs are written: Lx = [Lp, carry] (rows >= j+bw+1) feeds
-// the trailing update as one rank-(bw+1) product with Bt = Lx Tx^T; the rows
-// inside the block and the alphas are committed into A after that update.
+// every lane writes its row of the block's outputs at its final position:
+// Lx = [Lp, carry] (rows >= j+bw+1) feeds the trailing update as one
+// rank-(bw+1) product with Bt = Lx Tx^T; the rows inside the block and the
+// alphas are committed into A after that update.
 
 #include "ltlt_device.h"
 #include "ltlt_internal.h"
 
 namespace ltlt {
 
-constexpr int kCpt = 64;   // multipliers per lane (register resident)
+constexpr int kPollPerLane = kMaxPanelRecords / kWave;   // records per polling lane
+constexpr int KC = 64;                                   // multiplier slots per lane
 
-// Lanes per row for a block of width bw.
-int panel_split(int bw) { return bw <= kCpt ? 1 : (bw <= 2 * kCpt ? 2 : 4); }
+// Lanes per row and register slots per lane for a block of width bw.
+int panel_split(int bw) { return bw <= KC ? 1 : (bw <= 2 * KC ? 2 : 4); }
+int panel_rows(int bw) { return kPanelThreads / panel_split(bw); }
 
+// LDS: per wave, the alpha history (TOT + 1) and the pivot row's multipliers
+// padded by one entry in front (TOT + 2), TOT = steps a row can hold.
+__host__ __device__ constexpr int panel_wave_lds_elems(int tot) { return (tot + 1) + (tot + 2); }
 template <typename T>
-size_t panel_lds_bytes(int bw, int R) {
-  const int S = kThreads / R;
-  size_t t = 0;
-  t += (size_t)S * kCpt * sizeof(T);              // g, split by lane part
-  t += (size_t)(bw + 1) * sizeof(T) * 3;          // alpha, lrow, oldrow
-  t += (size_t)R * (bw + 1) * sizeof(T);          // multipliers gathered for the outputs
-  return t + 64;
+size_t panel_lds_bytes(int bw, int /*R*/) {
+  return (size_t)kPanelWaves * panel_wave_lds_elems(KC * panel_split(bw)) * sizeof(T);
 }
 
 // Record words.  s = k + 1 is the step stamp (1 <= s < 2^21).
 //   word A = bits(|cv|) | epoch(s) << 63,   epoch(s) = (s >> 1) & 1
-//   word B = (s << 43) | (sign(cv) << 42) | (pos << 21) | idx
+//   word B = (s << 43) | (sign(cv) << 42) | (pos << 21) | lp
 // A record slot alternates with s & 1 and every record location is written at
 // every step of its slot, so a slot holds stamp s or s-2 and the epoch bit
 // alone tells them apart in word A; word B carries the full stamp.
 constexpr uint64_t kIdxNone = 0x1FFFFFull;
-constexpr int kRecWords = 2;    // records packed: 8 per 128-byte line, one wave poll touches few lines
 __device__ __forceinline__ uint64_t rec_a(double absv, int s) {
   return (uint64_t)__double_as_longlong(absv) | ((uint64_t)((s >> 1) & 1) << 63);
 }
@@ -95,319 +110,416 @@ __device__ __forceinline__ T ld_coh_t(const T* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// S(a, b) of the stored (strict lower) skew matrix, a != b.
-template <typename T>
-__device__ __forceinline__ T skew_at(const T* A, int64_t lda, int a, int b) {
-  return a > b ? A[(int64_t)a + (int64_t)b * lda] : -A[(int64_t)b + (int64_t)a * lda];
+// LDS written by some lanes of a wave is read by other lanes of the same wave:
+// wait for the wave's LDS operations and keep the compiler from moving memory
+// accesses across this point.
+__device__ __forceinline__ void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// The 16 slots of one g register: acc[c % 4] += g(lane (lane & ~15) + c) * L[c0 + c]
+// through v_fmac with a DPP row broadcast (row_newbcast, gfx950).  One asm
+// block, led by the two wait states a DPP read needs after a VALU write of its
+// source, so that no compiler-inserted copy of g can sit in between.
+#define LTLT_FMAC16(OP)                                                                                  \
+  asm volatile("s_nop 1\n"                                                                               \
+               OP " %0, %4, %5 row_newbcast:0 row_mask:0xf bank_mask:0xf\n"                              \
+               OP " %1, %4, %6 row_newbcast:1 row_mask:0xf bank_mask:0xf\n"                              \
+               OP " %2, %4, %7 row_newbcast:2 row_mask:0xf bank_mask:0xf\n"                              \
+               OP " %3, %4, %8 row_newbcast:3 row_mask:0xf bank_mask:0xf\n"                              \
+               OP " %0, %4, %9 row_newbcast:4 row_mask:0xf bank_mask:0xf\n"                              \
+               OP " %1, %4, %10 row_newbcast:5 row_mask:0xf bank_mask:0xf\n"                             \
+               OP " %2, %4, %11 row_newbcast:6 row_mask:0xf bank_mask:0xf\n"                             \
+               OP " %3, %4, %12 row_newbcast:7 row_mask:0xf bank_mask:0xf\n"                             \
+               OP " %0, %4, %13 row_newbcast:8 row_mask:0xf bank_mask:0xf\n"                             \
+               OP " %1, %4, %14 row_newbcast:9 row_mask:0xf bank_mask:0xf\n"                             \
+               OP " %2, %4, %15 row_newbcast:10 row_mask:0xf bank_mask:0xf\n"                            \
+               OP " %3, %4, %16 row_newbcast:11 row_mask:0xf bank_mask:0xf\n"                            \
+               OP " %0, %4, %17 row_newbcast:12 row_mask:0xf bank_mask:0xf\n"                            \
+               OP " %1, %4, %18 row_newbcast:13 row_mask:0xf bank_mask:0xf\n"                            \
+               OP " %2, %4, %19 row_newbcast:14 row_mask:0xf bank_mask:0xf\n"                            \
+               OP " %3, %4, %20 row_newbcast:15 row_mask:0xf bank_mask:0xf\n"                            \
+               : "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3])                                  \
+               : "v"(g), "v"(L[c0 + 0]), "v"(L[c0 + 1]), "v"(L[c0 + 2]), "v"(L[c0 + 3]), "v"(L[c0 + 4]), \
+                 "v"(L[c0 + 5]), "v"(L[c0 + 6]), "v"(L[c0 + 7]), "v"(L[c0 + 8]), "v"(L[c0 + 9]),         \
+                 "v"(L[c0 + 10]), "v"(L[c0 + 11]), "v"(L[c0 + 12]), "v"(L[c0 + 13]), "v"(L[c0 + 14]),    \
+                 "v"(L[c0 + 15]))
+template <int K>
+__device__ __forceinline__ void refresh16(double (&acc)[4], double g, const double (&L)[KC]) {
+  constexpr int c0 = 16 * K;
+  LTLT_FMAC16("v_fmac_f64_dpp");
+}
+template <int K>
+__device__ __forceinline__ void refresh16(float (&acc)[4], float g, const float (&L)[KC]) {
+  constexpr int c0 = 16 * K;
+  LTLT_FMAC16("v_fmac_f32_dpp");
+}
+#undef LTLT_FMAC16
+
+// Wave-wide maximum of v (every lane gets it): DPP row shifts and row
+// broadcasts; lanes without a source keep their own value.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ double dpp_max_step(double v) {
+  const int lo = __double2loint(v), hi = __double2hiint(v);
+  const int olo = __builtin_amdgcn_update_dpp(lo, lo, CTRL, ROW_MASK, 0xF, false);
+  const int ohi = __builtin_amdgcn_update_dpp(hi, hi, CTRL, ROW_MASK, 0xF, false);
+  return fmax(v, __hiloint2double(ohi, olo));
+}
+__device__ __forceinline__ double wave_max(double v) {
+  v = dpp_max_step<0x111, 0xF>(v);   // row_shr:1
+  v = dpp_max_step<0x112, 0xF>(v);   // row_shr:2
+  v = dpp_max_step<0x114, 0xF>(v);   // row_shr:4
+  v = dpp_max_step<0x118, 0xF>(v);   // row_shr:8  -> lane 15 of each row holds the row maximum
+  v = dpp_max_step<0x142, 0xA>(v);   // row_bcast:15 into rows 1 and 3
+  v = dpp_max_step<0x143, 0xC>(v);   // row_bcast:31 into rows 2 and 3 -> lane 63 holds the maximum
+  const int lo = __builtin_amdgcn_readlane(__double2loint(v), 63);
+  const int hi = __builtin_amdgcn_readlane(__double2hiint(v), 63);
+  return __hiloint2double(hi, lo);
+}
+// First maximum of (value, key) over the wave: the largest value, and among
+// equal values the smallest key.  Values are >= -1 and not NaN; -1 marks "no
+// candidate".  Returns the lane that holds it (-1 when no lane has a
+// candidate) and sets vmax / kmin to its value and key.
+__device__ __forceinline__ int wave_first_max(double v, int key, double& vmax, int& kmin) {
+  vmax = wave_max(v);
+  unsigned long long hit = __ballot(v == vmax && vmax >= 0.0);
+  if (hit == 0) { kmin = INT32_MAX; return -1; }
+  int src = __ffsll(hit) - 1;
+  kmin = __builtin_amdgcn_readlane(key, src);
+  hit &= hit - 1;
+  while (hit) {                                    // equal values: smallest key (rare)
+    const int l2 = __ffsll(hit) - 1;
+    const int k2 = __builtin_amdgcn_readlane(key, l2);
+    if (k2 < kmin) { kmin = k2; src = l2; }
+    hit &= hit - 1;
+  }
+  return src;
+}
+
+// L[c] = v where `on`, for a wave-uniform slot c: a uniform branch on the
+// group of 16 slots, then selects inside the group, so that register indices
+// stay static and the other 48 slots are untouched.
+#define LTLT_SET_GROUP(G0)                                                       \
+  if ((c >> 4) == (G0) / 16) {                                                  \
+    _Pragma("unroll") for (int i = 0; i < 16; ++i) L[(G0) + i] = (on && c == (G0) + i) ? v : L[(G0) + i]; \
+  }
+
+// Sum of v over the S parts of a row (lanes lane ^ 16, lane ^ 32).
+template <int S, typename T>
+__device__ __forceinline__ T part_sum(T v) {
+  if constexpr (S == 4) v += __shfl_xor(v, 16, kWave);
+  if constexpr (S >= 2) v += __shfl_xor(v, 32, kWave);
+  return v;
 }
 
 template <typename T, int S>
-__global__ void __launch_bounds__(kThreads, 1) panel_kernel(PanelArgs a) {
+__global__ void __launch_bounds__(kPanelThreads, 1) panel_kernel(PanelArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
-  constexpr int R = kThreads / S;
+  constexpr int R = kPanelThreads / S;
+  constexpr int RW = kWave / S;                    // rows per wave
+  constexpr int NG = KC / 16;                      // g registers
+  constexpr int TOT = KC * S;                      // steps a row can hold
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
   const int w = blockIdx.x;
   const int bw = a.bw, n = a.n, j = a.j, P = a.P;
-  const int rloc = tid / S;            // row of this lane
-  const int part = tid % S;            // multiplier slice of this lane
+  const int part = lane / RW;                      // step slice of this lane
+  const int rloc = wave * RW + lane % RW;
   const int64_t lda = a.lda, ldw = a.ldw;
   const T* A = static_cast<const T*>(a.A);
   T* G = static_cast<T*>(a.G);
 
-  T *gp, *alpha, *lrow, *oldrow, *dump;
-  {
-    unsigned char* p = smem;
-    gp = reinterpret_cast<T*>(p); p += (size_t)S * kCpt * sizeof(T);
-    alpha = reinterpret_cast<T*>(p); p += (size_t)(bw + 1) * sizeof(T);
-    lrow = reinterpret_cast<T*>(p); p += (size_t)(bw + 1) * sizeof(T);
-    oldrow = reinterpret_cast<T*>(p); p += (size_t)(bw + 1) * sizeof(T);
-    dump = reinterpret_cast<T*>(p);
-  }
-  __shared__ double red_v[kThreads / kWave];
-  __shared__ int red_i[kThreads / kWave], red_p[kThreads / kWave];
-  __shared__ T red_c[kThreads / kWave];
-  __shared__ int s_p, s_posw, s_posk, s_abort;
-  __shared__ T s_alpha, s_cvk;
+  T* my_alpha = reinterpret_cast<T*>(smem) + wave * panel_wave_lds_elems(TOT);   // alpha_{j+u}
+  T* my_lrowp = my_alpha + (TOT + 1);              // my_lrowp[u + 1] = Lrow[u]
+  __shared__ int s_p, s_posw, s_abort;
+  __shared__ double red_v[kPanelWaves];
+  __shared__ uint64_t red_k[kPanelWaves];
+  __shared__ T s_alpha;
 
-  const int row0 = j + 1 + w * R;                 // first position owned
+  const int row0 = j + 1 + w * R;                 // first block-start index held
   const int rows_here = max(0, min(R, n - row0));
-  const int my_i = row0 + rloc;
   const bool my_row = rloc < rows_here;
+  const int pos = row0 + rloc;                     // block-start index of this lane's row
+  int lp = pos;                                    // its current position
 
-  T L[kCpt];
+  T L[KC], gr[NG];
 #pragma unroll
-  for (int c = 0; c < kCpt; ++c) L[c] = T(0);
-  for (int e = tid; e < S * kCpt; e += kThreads) gp[e] = T(0);
-  int pos = my_i;                                  // block-start index of this row
+  for (int c = 0; c < KC; ++c) L[c] = T(0);
+#pragma unroll
+  for (int k = 0; k < NG; ++k) gr[k] = T(0);
+  if (lane == 0) my_lrowp[0] = T(0);               // Lrow[-1]: only ever multiplied, kept finite
   T cv = T(0);
   if (tid == 0) s_abort = 0;
-  // first stored column: index j, rows >= j+1 (lower part only)
-  T lv = T(0);
-  if (my_row && part == 0) lv = A[(int64_t)my_i + (int64_t)j * lda];
+  // stored column value of this row and its sign (S(a,b) = -A(b,a) above the
+  // diagonal); the sign is applied in the refresh so that no code waits for
+  // the load before then.  First column: index j, rows >= j+1 (lower part).
+  T lv = T(0), lsg = T(1);
+  if (my_row && part == 0) lv = A[(int64_t)pos + (int64_t)j * lda];
   __syncthreads();
 
   for (int t = 0; t <= bw; ++t) {
     const int k = j + t;
-    // ---- column refresh: cv = S(pos, q) + sum_u g_u L_u over rows >= k+1 ----
-    const bool active = my_row && (my_i >= k + 1);
+    // ---- column refresh: cv = S(pos, q) + sum_u g_u L_u over rows at >= k+1 ----
+    const bool active = my_row && lp >= k + 1;
     {
-      const T* gq = gp + part * kCpt;
-      T a0 = T(0), a1 = T(0), a2 = T(0), a3 = T(0);
-#pragma unroll
-      for (int c = 0; c < kCpt; c += 4) {
-        a0 += gq[c] * L[c];
-        a1 += gq[c + 1] * L[c + 1];
-        a2 += gq[c + 2] * L[c + 2];
-        a3 += gq[c + 3] * L[c + 3];
-      }
-      T acc = ((a0 + a1) + (a2 + a3)) + lv;      // lv is nonzero in part 0 only
-      if (S >= 2) acc += __shfl_xor(acc, 1, kWave);
-      if (S >= 4) acc += __shfl_xor(acc, 2, kWave);
-      if (active) cv = acc;
+      T acc[4] = {T(0), T(0), T(0), T(0)};
+      static_assert(NG == 4, "four g registers");
+      if (0 * 16 * S < t) refresh16<0>(acc, gr[0], L);
+      if (1 * 16 * S < t) refresh16<1>(acc, gr[1], L);
+      if (2 * 16 * S < t) refresh16<2>(acc, gr[2], L);
+      if (3 * 16 * S < t) refresh16<3>(acc, gr[3], L);
+      T sum = fma(lsg, lv, (acc[0] + acc[1]) + (acc[2] + acc[3]));   // lv is nonzero in part 0 only
+      sum = part_sum<S>(sum);
+      if (active) cv = sum;
     }
     if (t == bw) break;                           // carry column formed
 
-    // ---- local pivot candidate ----
-    double bv = -1.0;
-    int bi = INT32_MAX;
-    if (active) {
-      const double av = (double)fabs(cv);
-      if (av == av) { bv = av; bi = my_i; }       // NaN is never a candidate
-    }
-    wave_argmax_dpp(bv, bi);
-    if (bi == INT32_MAX) {
-      if (lane == 0) { red_v[wave] = -1.0; red_i[wave] = INT32_MAX; }
-    } else if (my_i == bi && part == 0) {         // the candidate's own lane
-      red_v[wave] = bv; red_i[wave] = bi; red_c[wave] = cv; red_p[wave] = pos;
-    }
-    const int s = k + 1;
-    uint64_t* recs = a.rec + (size_t)(s & 1) * (size_t)(a.kslot + 1) * kRecWords;
-    wait_stores();                                // this wave's earlier G stores are complete
-    if (my_i == k + 1 && my_row && part == 0) {   // owner of position k+1 publishes it
-      st_coh64(&recs[kRecWords * a.kslot + 0], rec_a((double)fabs(cv), s));
-      st_coh64(&recs[kRecWords * a.kslot + 1], rec_b(s, cv < T(0) ? 1 : 0, pos, (uint64_t)(k + 1)));
-    }
-    __syncthreads();
-    // ---- publish this workgroup's candidate (lane 0 of wave 0) ----
-    if (tid == 0) {
-      double cb = red_v[0];
-      int ci = red_i[0], cw = 0;
-      for (int wv = 1; wv < kThreads / kWave; ++wv) {
-        const double ov = red_v[wv];
-        const int oi = red_i[wv];
-        if (ov > cb || (ov == cb && oi < ci)) { cb = ov; ci = oi; cw = wv; }
+    // ---- this wave's pivot candidate: (|cv|, position), first maximum ----
+    {
+      double av = -1.0;
+      if (active) {
+        const double m = (double)fabs(cv);
+        if (m == m) av = m;                        // NaN is never a candidate
       }
-      if (ci == INT32_MAX) {
-        st_coh64(&recs[kRecWords * w + 0], rec_a(0.0, s));
-        st_coh64(&recs[kRecWords * w + 1], rec_b(s, 0, 0, kIdxNone));
-      } else {
-        st_coh64(&recs[kRecWords * w + 0], rec_a(cb, s));
-        st_coh64(&recs[kRecWords * w + 1], rec_b(s, red_c[cw] < T(0) ? 1 : 0, red_p[cw], (uint64_t)ci));
-      }
-    }
-    // ---- poll all records and reduce (wave 0); entry u == P is position k+1 ----
-    if (wave == 0) {
-      double gv = -1.0;
-      int gi = INT32_MAX, gpos = 0, gsg = 0;
-      int kpos = 0, ksg = 0;
-      double kabs = 0.0;
-      const uint64_t t0 = wall_ticks();
-      for (int u0 = 0; u0 <= P; u0 += kWave) {
-        const int u = u0 + lane;
-        if (u <= P) {
-          const int ri = (u < P) ? u : a.kslot;
-          uint64_t ra, rb;
-          for (;;) {
-            ra = ld_coh64(&recs[kRecWords * ri + 0]);
-            rb = ld_coh64(&recs[kRecWords * ri + 1]);
-            if (rec_valid(ra, rb, s)) break;
-            if (wall_ticks() - t0 > kWaitLimitTicks || ld_coh(a.status) != 0) {
-              atomicOr(a.status, 1);
-              s_abort = 1;
-              break;
-            }
-            __builtin_amdgcn_s_sleep(0);
-          }
-          const double av = __longlong_as_double((long long)(ra & 0x7FFFFFFFFFFFFFFFull));
-          const int ix = (int)(rb & kIdxNone);
-          const int px = (int)((rb >> 21) & kIdxNone);
-          const int sg = (int)((rb >> 42) & 1);
-          if (u < P) {
-            if ((uint64_t)ix != kIdxNone && (av > gv || (av == gv && ix < gi))) {
-              gv = av; gi = ix; gpos = px; gsg = sg;
-            }
-          } else {
-            kabs = av; kpos = px; ksg = sg;
-          }
-        }
-      }
-      const int klane = P % kWave;                // lane that read the position-(k+1) record
-      kabs = __shfl(kabs, klane, kWave);
-      kpos = __shfl(kpos, klane, kWave);
-      ksg = __shfl(ksg, klane, kWave);
-      {
-        // wave argmax on (|value|, position); the winning lane then supplies
-        // the block-start index and sign of the winner
-        const int my_gi = gi;
-        wave_argmax_dpp(gv, gi);
-        const unsigned long long hit = __ballot(gi != INT32_MAX && my_gi == gi);
-        const int src = hit ? __ffsll(hit) - 1 : 0;
-        gpos = __shfl(gpos, src, kWave);
-        gsg = __shfl(gsg, src, kWave);
+      double bv;
+      int bi;
+      const int src = wave_first_max(av, active ? lp : INT32_MAX, bv, bi);
+      int wpos = 0, wsg = 0;
+      if (src >= 0) {
+        wpos = __builtin_amdgcn_readlane(pos, src);
+        wsg = __builtin_amdgcn_readlane(cv < T(0) ? 1 : 0, src);
       }
       if (lane == 0) {
-        const T ck = ksg ? -(T)kabs : (T)kabs;
-        s_cvk = ck;
-        s_posk = kpos;
-        if (gi == INT32_MAX) {                    // no finite candidate: keep k+1
-          s_p = k + 1; s_alpha = ck; s_posw = kpos;
+        red_v[wave] = src >= 0 ? bv : -1.0;
+        red_k[wave] = ((uint64_t)(uint32_t)bi << 32) | ((uint64_t)wpos << 1) | (uint64_t)wsg;
+      }
+    }
+    const int s = k + 1;
+    uint64_t* recs = a.rec + (size_t)(s & 1) * (size_t)a.nrec * kRecStride;
+    wait_stores();                                // this wave's earlier G stores are complete
+    __syncthreads();
+    if (wave == 0) {                              // merge the waves, publish (lane 0)
+      double cb = red_v[0];
+      uint64_t ck = red_k[0];
+#pragma unroll
+      for (int wv = 1; wv < kPanelWaves; ++wv) {
+        const double ov = red_v[wv];
+        const uint64_t ok = red_k[wv];
+        const bool take = (ov > cb) | ((ov == cb) & (ok < ck));
+        cb = take ? ov : cb;
+        ck = take ? ok : ck;
+      }
+      if (lane == 0) {
+        const int ci = (int)(ck >> 32);
+        const bool none = ci == INT32_MAX;
+        st_coh64(&recs[(size_t)kRecStride * w + 0], rec_a(none ? 0.0 : cb, s));
+        st_coh64(&recs[(size_t)kRecStride * w + 1],
+                 rec_b(s, (int)(ck & 1), (int)((ck >> 1) & kIdxNone), none ? kIdxNone : (uint64_t)ci));
+      }
+    }
+
+    // ---- poll every record and reduce (wave 0) ----
+    if (wave == 0) {
+      const int q_n = (P + kWave - 1) / kWave;
+      const uint64_t t0 = wall_ticks();
+      uint64_t ra[kPollPerLane], rb[kPollPerLane];
+      for (;;) {
+#pragma unroll
+        for (int q = 0; q < kPollPerLane; ++q) {
+          const int u = q * kWave + lane;
+          if (q < q_n && u < P) {
+            ra[q] = ld_coh64(&recs[(size_t)kRecStride * u + 0]);
+            rb[q] = ld_coh64(&recs[(size_t)kRecStride * u + 1]);
+          }
+        }
+        bool ok = true;
+#pragma unroll
+        for (int q = 0; q < kPollPerLane; ++q) {
+          const int u = q * kWave + lane;
+          if (q < q_n && u < P) ok = ok && rec_valid(ra[q], rb[q], s);
+        }
+        if (__ballot(!ok) == 0) break;
+        if (wall_ticks() - t0 > kWaitLimitTicks || ld_coh(a.status) != 0) {
+          if (lane == 0) { atomicOr(a.status, 1); s_abort = 1; }
+          break;
+        }
+        __builtin_amdgcn_s_sleep(0);
+      }
+      double gv = -1.0;
+      int gi = INT32_MAX, gpos = 0, gsg = 0;
+#pragma unroll
+      for (int q = 0; q < kPollPerLane; ++q) {
+        const int u = q * kWave + lane;
+        if (q < q_n && u < P) {
+          const double av = __longlong_as_double((long long)(ra[q] & 0x7FFFFFFFFFFFFFFFull));
+          const int ix = (int)(rb[q] & kIdxNone);
+          const bool take = ((uint64_t)ix != kIdxNone) & ((av > gv) | ((av == gv) & (ix < gi)));
+          gv = take ? av : gv;
+          gi = take ? ix : gi;
+          gpos = take ? (int)((rb[q] >> 21) & kIdxNone) : gpos;
+          gsg = take ? (int)((rb[q] >> 42) & 1) : gsg;
+        }
+      }
+      double vmax;
+      int kmin;
+      const int src = wave_first_max(gv, gi, vmax, kmin);
+      if (lane == 0) {
+        if (src < 0) {                            // no finite candidate: no exchange
+          s_p = k + 1; s_posw = k + 1; s_alpha = T(NAN);
         } else {
-          s_p = gi; s_alpha = gsg ? -(T)gv : (T)gv; s_posw = gpos;
+          s_p = kmin;
+          s_posw = __builtin_amdgcn_readlane(gpos, src);
+          s_alpha = __builtin_amdgcn_readlane(gsg, src) ? -(T)vmax : (T)vmax;
         }
       }
     }
     __syncthreads();
     if (s_abort) return;
     const int p = s_p;
-    const int posw = s_posw, posk = s_posk;
-    const T alph = s_alpha, cvk = s_cvk;
-    // ---- one round of loads: next stored column, pivot row, leaving row ----
-    const bool is_k1 = my_row && my_i == k + 1;
-    const bool is_p = my_row && p != k + 1 && my_i == p;
-    if (is_p) pos = posk;                         // the row leaving k+1 lands at p
-    if (is_k1) pos = posw;
-    if (my_row && part == 0 && my_i >= k + 2) lv = skew_at(A, lda, pos, posw);
-    // the pivot row's multipliers (all workgroups) and, in the workgroup that
-    // owns p, those of the row leaving k+1: one value per thread, one round
-    const bool wg_owns_p = (p != k + 1) && p >= row0 && p < row0 + rows_here;
-    if (tid < t) {
-      lrow[tid] = ld_coh_t(&G[(int64_t)(posw - (j + 1)) + (int64_t)tid * ldw]);
-      if (wg_owns_p) oldrow[tid] = ld_coh_t(&G[(int64_t)(posk - (j + 1)) + (int64_t)tid * ldw]);
+    const int posw = s_posw;                      // block-start index of the pivot row
+    const T alph = s_alpha;
+
+    // ---- exchange positions k+1 and p (logical only) ----
+    if (my_row && p != k + 1) {
+      if (lp == p) lp = k + 1;
+      else if (lp == k + 1) lp = p;
     }
-    __syncthreads();
-    if (is_p) {
+    const bool next = my_row && lp >= k + 2;      // rows still to be eliminated
+
+    // ---- one round of loads: next stored column, pivot row multipliers.
+    //      Every lane issues the same number of multiplier loads (addresses
+    //      clamped to steps < t) so that waiting for them is exact. ----
+    if (next && part == 0) {
+      // S(pos, posw) = +A(pos, posw) below the diagonal, -A(posw, pos) above:
+      // element (max, min) of the stored triangle
+      lv = A[(int64_t)max(pos, posw) + (int64_t)min(pos, posw) * lda];
+      lsg = pos > posw ? T(1) : T(-1);
+    }
+    constexpr int NLQ = TOT / kWave;              // multiplier loads per lane
+    T lr[NLQ];
+    {
+      const T* grow = G + (int64_t)(posw - (j + 1));
+      const int umax = t > 0 ? t - 1 : 0;
 #pragma unroll
-      for (int c = 0; c < kCpt; ++c) {
-        const int u = c * S + part;
-        L[c] = u < t ? oldrow[u < t ? u : 0] : T(0);
-      }
-      cv = cvk;
+      for (int q = 0; q < NLQ; ++q) lr[q] = ld_coh_t(&grow[(int64_t)min(q * kWave + lane, umax) * ldw]);
     }
-    // ---- multipliers of step k (the row now at k+1 is final: its
-    //      multipliers are taken from G for the output) ----
-    if (my_row && my_i >= k + 2) {
-      const T l = (alph != T(0)) ? cv / alph : T(0);
-      const int cslot = t / S;
-      if (part == t % S) {
+
+    // ---- multipliers of step k (registers now, G after the loads are used) ----
+    T l = T(0);
+    if (next) l = (alph != T(0)) ? cv / alph : T(0);
+    {
+      const int c = t / S;
+      const bool on = next && part == t % S;
+      const T v = l;
+      static_assert(KC == 64, "four groups of 16 slots");
+      LTLT_SET_GROUP(0) LTLT_SET_GROUP(16) LTLT_SET_GROUP(32) LTLT_SET_GROUP(48)
+    }
+
+    // ---- g coefficients for step k+1 (t+1 terms), row broadcast layout ----
 #pragma unroll
-        for (int c = 0; c < kCpt; ++c)
-          if (c == cslot) L[c] = l;
-        st_coh_t(&G[(int64_t)(pos - (j + 1)) + (int64_t)t * ldw], l);
+    for (int q = 0; q < NLQ; ++q) {
+      const int u = q * kWave + lane;
+      if (u < t) my_lrowp[u + 1] = lr[q];
+    }
+    if (lane == 0) { my_alpha[t] = alph; my_lrowp[t + 1] = T(1); }   // Lrow[t] = 1: unit diagonal
+    wave_lds_sync();
+    {
+      const int c = lane & 15;
+#pragma unroll
+      for (int kk = 0; kk < NG; ++kk) {
+        if (kk * 16 * S <= t) {
+          const int u = (16 * kk + c) * S + part;  // < TOT
+          const T a0 = my_alpha[u], a1 = my_alpha[u + 1];
+          const T lm = my_lrowp[u], l1 = my_lrowp[u + 2];
+          const T up = (u <= t - 1) ? a1 * l1 : T(0);
+          const T g = (u >= 1) ? up - a0 * lm : up;
+          gr[kk] = (u <= t) ? g : T(0);
+        }
       }
     }
-    // g coefficients for step k+1 (t+1 terms); alpha_{j+t} and Lrow[t] = 1 are new
-    if (tid <= t) {
-      const int u = tid;
-      T gu = T(0);
-      if (u <= t - 1) {
-        const T an = (u + 1 == t) ? alph : alpha[u + 1];
-        const T ln = (u + 1 == t) ? T(1) : lrow[u + 1];
-        gu += an * ln;
-      }
-      if (u >= 1) {
-        const T am = (u == t) ? alph : alpha[u];
-        gu -= am * lrow[u - 1];
-      }
-      gp[(u % S) * kCpt + u / S] = gu;
+    {
+      // recompute the row offset here instead of keeping a 64-bit pointer
+      // live across the step loop (the kernel runs at the register limit)
+      int ro = pos - (j + 1);
+      asm volatile("" : "+v"(ro));
+      if (next && part == t % S) st_coh_t(&G[(int64_t)ro + (int64_t)t * ldw], l);
     }
-    if (tid == 0) { alpha[t] = alph; if (w == 0) a.ipiv[k + 1] = p; }
-    __syncthreads();
+    if (tid == 0 && w == 0) a.ipiv[k + 1] = p;
+    wave_lds_sync();
   }
 
-  // ---- outputs: multipliers through LDS (Bt needs neighbouring columns).
-  //      Rows still active hold every multiplier in registers; the final
-  //      pivot rows (positions j+1 .. j+bw) read theirs from G, whose entries
-  //      all predate the last exchange. ----
-  wait_stores();
-  __syncthreads();
-  const int tr0 = j + bw + 1;                      // first trailing position
-  if (my_row) {
-    if (my_i >= tr0) {
-#pragma unroll
-      for (int c = 0; c < kCpt; ++c) {
-        const int u = c * S + part;
-        if (u < bw) dump[u * R + rloc] = L[c];
-      }
-      if (part == 0) dump[bw * R + rloc] = cv;    // carry
-    } else {
-      const T* src = G + (int64_t)(pos - (j + 1));
-      for (int u = part; u < bw; u += S) dump[u * R + rloc] = ld_coh_t(&src[(int64_t)u * ldw]);
-      if (part == 0) dump[bw * R + rloc] = T(0);
-    }
-  }
-  __syncthreads();
+#undef LTLT_SET_GROUP
+
+  // ---- outputs, by final position, straight from registers.  Rows at
+  //      positions j+1 .. j+bw hold the multipliers of the steps before they
+  //      became final (zeros after); trailing rows hold all of them and the
+  //      carry. ----
   T* PO = static_cast<T*>(a.PO);
   T* Bm = static_cast<T*>(a.Bm);
-  for (int r = tid; r < rows_here; r += kThreads) {
-    const int ii = row0 + r;
-    const int64_t ro = ii - (j + 1);
-    for (int u = 0; u < bw; ++u) PO[ro + u * ldw] = dump[u * R + r];
-    if (ii >= tr0) {
-      const T carry = dump[bw * R + r];
-      PO[ro + (int64_t)bw * ldw] = carry;
-      const int64_t rb = ii - tr0;
-      // Bt = Lx Tx^T: column u = a_u Lx_{u+1} - a_{u-1} Lx_{u-1},
-      // a_u = alpha_{j+u+1} (u <= bw-2), a_{bw-1} = 1, Lx_bw = carry.
-      for (int u = 0; u <= bw; ++u) {
-        T v = T(0);
-        if (u <= bw - 1) {
-          const T au = (u <= bw - 2) ? alpha[u + 1] : T(1);
-          v += au * dump[(u + 1) * R + r];
-        }
-        if (u >= 1) {
-          const T am = (u - 1 <= bw - 2) ? alpha[u] : T(1);
-          v -= am * dump[(u - 1) * R + r];
-        }
-        Bm[rb + u * ldw] = v;
+  const int tr0 = j + bw + 1;                      // first trailing position
+  const bool trailing = my_row && lp >= tr0;
+  const T carry = trailing ? cv : T(0);
+  const T* alpha = my_alpha;                       // alpha_{j+u}, u < bw
+  if (my_row) {
+    const int64_t ro = lp - (j + 1);
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
+      const int u = c * S + part;
+      if (u < bw) PO[ro + (int64_t)u * ldw] = L[c];
+    }
+    if (part == 0) PO[ro + (int64_t)bw * ldw] = carry;
+  }
+  // Bt = Lx Tx^T: column u = a_u Lx_{u+1} - a_{u-1} Lx_{u-1},
+  // a_u = alpha_{j+u+1} (u <= bw-2), a_{bw-1} = 1, Lx_bw = carry.
+  // Step u = c*S + part; step u+1 lives in the next part (lane + RW), slot c
+  // (slot c+1 when this is the last part), step u-1 in the previous part
+  // (lane - RW), slot c (slot c-1 when this is part 0).  The owner lane hands
+  // out the slot its requester needs.
+  const int up_src = (lane + RW) % kWave, dn_src = (lane + kWave - RW) % kWave;
+#pragma unroll
+  for (int c = 0; c < KC; ++c) {
+    const T give_up = (part == 0 && c + 1 < KC) ? L[c + 1 < KC ? c + 1 : c] : (part == 0 ? T(0) : L[c]);
+    const T give_dn = (part == S - 1) ? (c >= 1 ? L[c >= 1 ? c - 1 : 0] : T(0)) : L[c];
+    const T xp0 = S == 1 ? give_up : __shfl(give_up, up_src, kWave);
+    const T xm = S == 1 ? give_dn : __shfl(give_dn, dn_src, kWave);
+    const int u = c * S + part;
+    if (trailing && u <= bw) {
+      T v = T(0);
+      if (u <= bw - 1) {
+        const T au = (u <= bw - 2) ? alpha[u + 1] : T(1);
+        v += au * (u + 1 == bw ? carry : xp0);
       }
+      if (u >= 1) {
+        const T am = (u - 1 <= bw - 2) ? alpha[u] : T(1);
+        v -= am * xm;
+      }
+      Bm[(int64_t)(lp - tr0) + (int64_t)u * ldw] = v;
     }
   }
-  if (my_row && part == 0) a.perm[my_i] = pos;
-  if (w == 0) {
-    T* al = static_cast<T*>(a.alpha);
-    for (int u = tid; u < bw; u += kThreads) al[u] = alpha[u];
+  // column bw when it lies past the slots (bw == TOT): -Lx_{bw-1}, step TOT-1
+  // is slot KC-1 of the last part
+  {
+    const T last = __shfl(L[KC - 1], (lane % RW) + (S - 1) * RW, kWave);
+    if (trailing && bw == TOT && part == 0) Bm[(int64_t)(lp - tr0) + (int64_t)bw * ldw] = -last;
   }
-}
-
-template <typename T, int S>
-hipError_t allow_panel_lds() {
-  static bool done = false;
-  if (done) return hipSuccess;
-  hipFuncAttributes fa;
-  hipError_t e = hipFuncGetAttributes(&fa, (const void*)panel_kernel<T, S>);
-  if (e != hipSuccess) return e;
-  e = hipFuncSetAttribute((const void*)panel_kernel<T, S>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                          (int)(160 * 1024 - fa.sharedSizeBytes));
-  if (e != hipSuccess) return e;
-  done = true;
-  return hipSuccess;
+  if (my_row && part == 0) a.perm[lp] = pos;
+  if (w == 0 && wave == 0) {
+    T* al = static_cast<T*>(a.alpha);
+    for (int u = lane; u < bw; u += kWave) al[u] = alpha[u];
+  }
 }
 
 template <typename T, int S>
 hipError_t launch_panel_s(const PanelArgs& a, size_t lds, hipStream_t st) {
-  hipError_t e = allow_panel_lds<T, S>();
-  if (e != hipSuccess) return e;
   PanelArgs copy = a;
   void* args[] = {&copy};
-  return hipLaunchCooperativeKernel((const void*)panel_kernel<T, S>, dim3(a.P), dim3(kThreads), args,
+  return hipLaunchCooperativeKernel((const void*)panel_kernel<T, S>, dim3(a.P), dim3(kPanelThreads), args,
                                     (unsigned)lds, st);
 }
 
 template <typename T>
 hipError_t launch_panel(const PanelArgs& a, size_t lds, hipStream_t st) {
-  switch (kThreads / a.R) {
+  if (a.P > kMaxPanelRecords || a.P > a.nrec || a.R != panel_rows(a.bw)) return hipErrorInvalidValue;
+  switch (panel_split(a.bw)) {
     case 1: return launch_panel_s<T, 1>(a, lds, st);
     case 2: return launch_panel_s<T, 2>(a, lds, st);
     case 4: return launch_panel_s<T, 4>(a, lds, st);
@@ -420,38 +532,39 @@ int panel_max_blocks_s(size_t lds) {
   int dev = 0, per_cu = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-  if (allow_panel_lds<T, S>() != hipSuccess) return 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)panel_kernel<T, S>, kThreads, lds) !=
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)panel_kernel<T, S>, kPanelThreads, lds) !=
       hipSuccess)
     return 0;
   return per_cu * cus;
 }
 
+// Co-resident workgroups for a block of width bw (capped by the records one
+// poll covers).
 template <typename T>
-int panel_max_blocks(int R, size_t lds) {
-  switch (kThreads / R) {
-    case 1: return panel_max_blocks_s<T, 1>(lds);
-    case 2: return panel_max_blocks_s<T, 2>(lds);
-    case 4: return panel_max_blocks_s<T, 4>(lds);
+int panel_max_blocks(int bw, size_t lds) {
+  int cap;
+  switch (panel_split(bw)) {
+    case 1: cap = panel_max_blocks_s<T, 1>(lds); break;
+    case 2: cap = panel_max_blocks_s<T, 2>(lds); break;
+    case 4: cap = panel_max_blocks_s<T, 4>(lds); break;
     default: return 0;
   }
+  return cap < kMaxPanelRecords ? cap : kMaxPanelRecords;
 }
-
-int panel_rows(int bw) { return kThreads / panel_split(bw); }
 
 // Exchange records start with stamps that can never validate: word B stamp 0,
 // and word A epoch opposite to that of the first stamp using the slot
 // (slot 1 first holds s = 1, epoch 0; slot 0 first holds s = 2, epoch 1).
 __global__ void rec_init_kernel(uint64_t* rec, int nrec) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= 2 * kRecWords * nrec) return;
-  const int slot = i / (kRecWords * nrec);
-  const int word = i % kRecWords;
+  if (i >= 2 * kRecStride * nrec) return;
+  const int slot = i / (kRecStride * nrec);
+  const int word = i % kRecStride;
   rec[i] = (word == 0 && slot == 1) ? (1ull << 63) : 0ull;
 }
 
 hipError_t launch_rec_init(uint64_t* rec, int nrec_per_slot, hipStream_t s) {
-  const int tot = 2 * kRecWords * nrec_per_slot;
+  const int tot = 2 * kRecStride * nrec_per_slot;
   hipLaunchKernelGGL(rec_init_kernel, dim3((tot + 255) / 256), dim3(256), 0, s, rec, nrec_per_slot);
   return hipGetLastError();
 }
