@@ -87,7 +87,7 @@ size_t panel_lds_bytes(int bw, int /*R*/) {
 // alone tells them apart in word A; word B carries the full stamp.
 constexpr uint64_t kIdxNone = 0x1FFFFFull;
 __device__ __forceinline__ uint64_t rec_a(double absv, int s) {
-  return (uint64_t)__double_as_longlong(absv) | ((uint64_t)((s >> 1) & 1) << 63);
+  return ((uint64_t)__double_as_longlong(absv) & 0x7FFFFFFFFFFFFFFFull) | ((uint64_t)((s >> 1) & 1) << 63);
 }
 __device__ __forceinline__ uint64_t rec_b(int s, int sgn, int pos, uint64_t idx) {
   return ((uint64_t)s << 43) | ((uint64_t)sgn << 42) | ((uint64_t)pos << 21) | idx;
@@ -154,43 +154,46 @@ __device__ __forceinline__ void refresh16(float (&acc)[4], float g, const float 
 }
 #undef LTLT_FMAC16
 
-// Wave-wide maximum of v (every lane gets it): DPP row shifts and row
-// broadcasts; lanes without a source keep their own value.
+// Wave-wide maximum of an unsigned key (every lane gets it): DPP row shifts
+// and row broadcasts; lanes without a source keep their own key.
 template <int CTRL, int ROW_MASK>
-__device__ __forceinline__ double dpp_max_step(double v) {
-  const int lo = __double2loint(v), hi = __double2hiint(v);
-  const int olo = __builtin_amdgcn_update_dpp(lo, lo, CTRL, ROW_MASK, 0xF, false);
-  const int ohi = __builtin_amdgcn_update_dpp(hi, hi, CTRL, ROW_MASK, 0xF, false);
-  return fmax(v, __hiloint2double(ohi, olo));
+__device__ __forceinline__ unsigned dpp_umax_step(unsigned x) {
+  const unsigned o = (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, CTRL, ROW_MASK, 0xF, false);
+  return o > x ? o : x;
 }
-__device__ __forceinline__ double wave_max(double v) {
-  v = dpp_max_step<0x111, 0xF>(v);   // row_shr:1
-  v = dpp_max_step<0x112, 0xF>(v);   // row_shr:2
-  v = dpp_max_step<0x114, 0xF>(v);   // row_shr:4
-  v = dpp_max_step<0x118, 0xF>(v);   // row_shr:8  -> lane 15 of each row holds the row maximum
-  v = dpp_max_step<0x142, 0xA>(v);   // row_bcast:15 into rows 1 and 3
-  v = dpp_max_step<0x143, 0xC>(v);   // row_bcast:31 into rows 2 and 3 -> lane 63 holds the maximum
-  const int lo = __builtin_amdgcn_readlane(__double2loint(v), 63);
-  const int hi = __builtin_amdgcn_readlane(__double2hiint(v), 63);
-  return __hiloint2double(hi, lo);
+__device__ __forceinline__ unsigned wave_umax(unsigned x) {
+  x = dpp_umax_step<0x111, 0xF>(x);   // row_shr:1
+  x = dpp_umax_step<0x112, 0xF>(x);   // row_shr:2
+  x = dpp_umax_step<0x114, 0xF>(x);   // row_shr:4
+  x = dpp_umax_step<0x118, 0xF>(x);   // row_shr:8  -> lane 15 of each row holds the row maximum
+  x = dpp_umax_step<0x142, 0xA>(x);   // row_bcast:15 into rows 1 and 3
+  x = dpp_umax_step<0x143, 0xC>(x);   // row_bcast:31 into rows 2 and 3 -> lane 63 holds the maximum
+  return (unsigned)__builtin_amdgcn_readlane((int)x, 63);
 }
 // First maximum of (value, key) over the wave: the largest value, and among
-// equal values the smallest key.  Values are >= -1 and not NaN; -1 marks "no
-// candidate".  Returns the lane that holds it (-1 when no lane has a
-// candidate) and sets vmax / kmin to its value and key.
+// equal values the smallest key.  Values are >= 0 for candidates and -1 for
+// lanes without one (NaN is never passed).  The wave maximum is found on the
+// high 32 bits of the value (order-preserving for non-negative doubles, +1 so
+// that 0 means "no candidate"); lanes that tie there are resolved exactly
+// (full value, then key) one by one, which is rare.  Returns the winning lane
+// (-1 when no lane has a candidate) and sets vmax / kmin to its value and key.
 __device__ __forceinline__ int wave_first_max(double v, int key, double& vmax, int& kmin) {
-  vmax = wave_max(v);
-  unsigned long long hit = __ballot(v == vmax && vmax >= 0.0);
-  if (hit == 0) { kmin = INT32_MAX; return -1; }
+  const unsigned hk = v >= 0.0 ? (unsigned)__double2hiint(v) + 1u : 0u;
+  const unsigned mh = wave_umax(hk);
+  if (mh == 0) { vmax = -1.0; kmin = INT32_MAX; return -1; }
+  unsigned long long hit = __ballot(hk == mh);
   int src = __ffsll(hit) - 1;
+  unsigned blo = (unsigned)__builtin_amdgcn_readlane(__double2loint(v), src);
   kmin = __builtin_amdgcn_readlane(key, src);
   hit &= hit - 1;
-  while (hit) {                                    // equal values: smallest key (rare)
+  while (hit) {                                    // equal high words (rare)
     const int l2 = __ffsll(hit) - 1;
+    const unsigned lo2 = (unsigned)__builtin_amdgcn_readlane(__double2loint(v), l2);
     const int k2 = __builtin_amdgcn_readlane(key, l2);
-    if (k2 < kmin) { kmin = k2; src = l2; }
+    if (lo2 > blo || (lo2 == blo && k2 < kmin)) { blo = lo2; kmin = k2; src = l2; }
     hit &= hit - 1;
   }
+  vmax = __hiloint2double((int)(mh - 1u), (int)blo);
   return src;
 }
 
@@ -331,6 +334,7 @@ __global__ void __launch_bounds__(kPanelThreads, 1) panel_kernel(PanelArgs a) {
             rb[q] = ld_coh64(&recs[(size_t)kRecStride * u + 1]);
           }
         }
+        const int stv = ld_coh(a.status);         // same round trip as the records
         bool ok = true;
 #pragma unroll
         for (int q = 0; q < kPollPerLane; ++q) {
@@ -338,7 +342,7 @@ __global__ void __launch_bounds__(kPanelThreads, 1) panel_kernel(PanelArgs a) {
           if (q < q_n && u < P) ok = ok && rec_valid(ra[q], rb[q], s);
         }
         if (__ballot(!ok) == 0) break;
-        if (wall_ticks() - t0 > kWaitLimitTicks || ld_coh(a.status) != 0) {
+        if (stv != 0 || wall_ticks() - t0 > kWaitLimitTicks) {
           if (lane == 0) { atomicOr(a.status, 1); s_abort = 1; }
           break;
         }

@@ -8,9 +8,9 @@
 // alphas, so only the lower triangle is computed, once).
 //
 // gfx950 mapping:
-//  * one 256-thread workgroup per 128x128 tile of the LOWER triangle only
-//    (tile row >= tile column); the triangular tile index is decoded once per
-//    workgroup;
+//  * 256-thread workgroups on 128x128 tiles of the LOWER triangle only
+//    (tile row >= tile column), a persistent grid of two workgroups per CU
+//    walking an XCD-aware tile order;
 //  * each of the 4 waves owns a 64x64 sub-tile = 4x4 MFMA blocks of 16x16
 //    (v_mfma_f64_16x16x4_f64, or v_mfma_f32_16x16x4_f32 for fp32),
 //    accumulating in registers;
@@ -33,6 +33,7 @@ namespace ltlt {
 
 constexpr int kMT = 128;     // tile edge
 constexpr int kKC = 16;      // K chunk
+constexpr int kUpdateGrid = 512;   // persistent grid: two workgroups on each of 256 CUs
 
 typedef double v4d __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
@@ -123,13 +124,9 @@ __device__ __forceinline__ int tri_index_decode(int b, int& J) {
   return I;
 }
 
-__device__ __forceinline__ void tile_of_block(int b, int nblocks, int tiles, int& I, int& J) {
-  // position of block b in the XCD-major order
-  const int x = b % kXcd, l = b / kXcd;
-  const int per = nblocks / kXcd, extra = nblocks % kXcd;
-  const int q = x * per + min(x, extra) + l;       // XCD x owns [x*per + min(x,extra), +per + (x<extra))
-  // q-th tile of the grouped order: groups (GI, GJ), GJ <= GI, row-major; full
-  // groups hold kGrp*kGrp tiles, diagonal groups kGrp(kGrp+1)/2, edge groups fewer
+// q-th tile of the grouped order: groups (GI, GJ), GJ <= GI, row-major; full
+// groups hold kGrp*kGrp tiles, diagonal groups kGrp(kGrp+1)/2, edge groups fewer.
+__device__ __forceinline__ void grouped_tile(int q, int tiles, int& I, int& J) {
   const int ng = (tiles + kGrp - 1) / kGrp;
   int rem = q;
   for (int GI = 0; GI < ng; ++GI) {
@@ -148,6 +145,19 @@ __device__ __forceinline__ void tile_of_block(int b, int nblocks, int tiles, int
   I = 0; J = 0;                                    // not reached for q < number of tiles
 }
 
+// The grid is persistent (at most two workgroups per CU).  XCD x owns the
+// x-th contiguous eighth [lo, hi) of the grouped order and its workgroups
+// (blocks b with b % 8 == x) take those tiles in turn.
+struct TileRange { int q, hi, step; };
+__device__ __forceinline__ TileRange tiles_of_block(int b, int nblocks, int ntiles) {
+  const int x = b % kXcd, l = b / kXcd;
+  const int per = ntiles / kXcd, extra = ntiles % kXcd;
+  const int lo = x * per + min(x, extra);
+  const int hi = lo + per + (x < extra ? 1 : 0);
+  const int cx = (nblocks - x + kXcd - 1) / kXcd;  // workgroups on XCD x
+  return TileRange{lo + l, hi, cx};
+}
+
 template <typename T>
 __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
   typedef typename Mfma<T>::acc_t acc_t;
@@ -162,8 +172,11 @@ __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
   const int wave = tid >> 6;
   const int wr = wave >> 1, wc = wave & 1;
 
+  const TileRange tr = tiles_of_block(blockIdx.x, gridDim.x, a.tiles * (a.tiles + 1) / 2);
+  for (int q = tr.q; q < tr.hi; q += tr.step) {
+  __syncthreads();                                 // LDS of the previous tile is free
   int I, J;
-  tile_of_block(blockIdx.x, gridDim.x, a.tiles, I, J);
+  grouped_tile(q, a.tiles, I, J);
   const int r0 = I * kMT, c0 = J * kMT;
   const int m = a.m, K = a.K;
 
@@ -259,6 +272,7 @@ __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
       for (int cc = 0; cc < 16; ++cc) oldv[cc] = nextv[cc];
     }
   }
+  }
 }
 
 template <typename T>
@@ -268,7 +282,8 @@ hipError_t launch_update(const UpdateArgs& a, hipStream_t s) {
   if (nblk <= 0) return hipSuccess;
   UpdateArgs c = a;
   c.tiles = tiles;
-  hipLaunchKernelGGL(update_kernel<T>, dim3((unsigned)nblk), dim3(kThreads), 0, s, c);
+  const int64_t grid = nblk < kUpdateGrid ? nblk : kUpdateGrid;
+  hipLaunchKernelGGL(update_kernel<T>, dim3((unsigned)grid), dim3(kThreads), 0, s, c);
   return hipGetLastError();
 }
 
