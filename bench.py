@@ -71,6 +71,27 @@ def cpu_baseline(X, n, target_s):
     }
 
 
+def update_traffic():
+    """HBM bytes per trailing-update launch from the committed counter summary
+    (two rocprofv3 --pmc passes, FETCH_SIZE and WRITE_SIZE, scaled by a copy of
+    known size), or None when the kernel source has changed since."""
+    import hashlib
+    summ = os.path.join(ROOT, "profiles", "update_kernel_hbm_traffic_n16384_f64_nb128.md")
+    src = os.path.join(ROOT, "paper_2005_06410_amd", "csrc", "ltlt_update.hip")
+    try:
+        fields = {}
+        for line in open(summ):
+            if ":" in line and not line.startswith(("|", "#", " ", "-", "`")):
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip()
+        h = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        if not h.startswith(fields.get("source_sha256_prefix", "-")):
+            return None
+        return float(fields["traffic_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -169,7 +190,7 @@ def main():
             "peak": peak_tf,
             "unit": "TFLOP/s",
             "frac": round(achieved_tf / peak_tf, 4),
-            "traffic": None,
+            "traffic": update_traffic(),
             "launches_per_step": up_launches // max(args.steps, 1),
             "avg_launch_ms": round(up_ms / max(up_launches, 1), 5),
         },
