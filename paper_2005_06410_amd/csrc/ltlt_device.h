@@ -87,4 +87,91 @@ __device__ __forceinline__ void wave_argmax_dpp(double& v, int& i) {
   i = __builtin_amdgcn_readlane(i, 63);
 }
 
+// ---------------------------------------------------------------------------
+// Register-resident column refresh and first-maximum search, shared by the
+// panel and the batched kernels.
+// ---------------------------------------------------------------------------
+
+// The 16 slots of one g register: acc[c % 4] += g(lane (lane & ~15) + c) * L[c0 + c]
+// through v_fmac with a DPP row broadcast (row_newbcast, gfx950).  One asm
+// block, led by the two wait states a DPP read needs after a VALU write of its
+// source, so that no compiler-inserted copy of g can sit in between.
+#define LTLT_FMAC16(OP)                                                                                  \
+  asm volatile("s_nop 1\n"                                                                               \
+               OP " %0, %4, %5 row_newbcast:0 row_mask:0xf bank_mask:0xf\n"                              \
+               OP " %1, %4, %6 row_newbcast:1 row_mask:0xf bank_mask:0xf\n"                              \
+               OP " %2, %4, %7 row_newbcast:2 row_mask:0xf bank_mask:0xf\n"                              \
+               OP " %3, %4, %8 row_newbcast:3 row_mask:0xf bank_mask:0xf\n"                              \
+               OP " %0, %4, %9 row_newbcast:4 row_mask:0xf bank_mask:0xf\n"                              \
+               OP " %1, %4, %10 row_newbcast:5 row_mask:0xf bank_mask:0xf\n"                             \
+               OP " %2, %4, %11 row_newbcast:6 row_mask:0xf bank_mask:0xf\n"                             \
+               OP " %3, %4, %12 row_newbcast:7 row_mask:0xf bank_mask:0xf\n"                             \
+               OP " %0, %4, %13 row_newbcast:8 row_mask:0xf bank_mask:0xf\n"                             \
+               OP " %1, %4, %14 row_newbcast:9 row_mask:0xf bank_mask:0xf\n"                             \
+               OP " %2, %4, %15 row_newbcast:10 row_mask:0xf bank_mask:0xf\n"                            \
+               OP " %3, %4, %16 row_newbcast:11 row_mask:0xf bank_mask:0xf\n"                            \
+               OP " %0, %4, %17 row_newbcast:12 row_mask:0xf bank_mask:0xf\n"                            \
+               OP " %1, %4, %18 row_newbcast:13 row_mask:0xf bank_mask:0xf\n"                            \
+               OP " %2, %4, %19 row_newbcast:14 row_mask:0xf bank_mask:0xf\n"                            \
+               OP " %3, %4, %20 row_newbcast:15 row_mask:0xf bank_mask:0xf\n"                            \
+               : "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3])                                  \
+               : "v"(g), "v"(L[c0 + 0]), "v"(L[c0 + 1]), "v"(L[c0 + 2]), "v"(L[c0 + 3]), "v"(L[c0 + 4]), \
+                 "v"(L[c0 + 5]), "v"(L[c0 + 6]), "v"(L[c0 + 7]), "v"(L[c0 + 8]), "v"(L[c0 + 9]),         \
+                 "v"(L[c0 + 10]), "v"(L[c0 + 11]), "v"(L[c0 + 12]), "v"(L[c0 + 13]), "v"(L[c0 + 14]),    \
+                 "v"(L[c0 + 15]))
+template <int K, int NS>
+__device__ __forceinline__ void refresh16(double (&acc)[4], double g, const double (&L)[NS]) {
+  constexpr int c0 = 16 * K;
+  LTLT_FMAC16("v_fmac_f64_dpp");
+}
+template <int K, int NS>
+__device__ __forceinline__ void refresh16(float (&acc)[4], float g, const float (&L)[NS]) {
+  constexpr int c0 = 16 * K;
+  LTLT_FMAC16("v_fmac_f32_dpp");
+}
+#undef LTLT_FMAC16
+
+// Wave-wide maximum of an unsigned key (every lane gets it): DPP row shifts
+// and row broadcasts; lanes without a source keep their own key.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ unsigned dpp_umax_step(unsigned x) {
+  const unsigned o = (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, CTRL, ROW_MASK, 0xF, false);
+  return o > x ? o : x;
+}
+__device__ __forceinline__ unsigned wave_umax(unsigned x) {
+  x = dpp_umax_step<0x111, 0xF>(x);   // row_shr:1
+  x = dpp_umax_step<0x112, 0xF>(x);   // row_shr:2
+  x = dpp_umax_step<0x114, 0xF>(x);   // row_shr:4
+  x = dpp_umax_step<0x118, 0xF>(x);   // row_shr:8  -> lane 15 of each row holds the row maximum
+  x = dpp_umax_step<0x142, 0xA>(x);   // row_bcast:15 into rows 1 and 3
+  x = dpp_umax_step<0x143, 0xC>(x);   // row_bcast:31 into rows 2 and 3 -> lane 63 holds the maximum
+  return (unsigned)__builtin_amdgcn_readlane((int)x, 63);
+}
+// First maximum of (value, key) over the wave: the largest value, and among
+// equal values the smallest key.  Values are >= 0 for candidates and -1 for
+// lanes without one (NaN is never passed).  The wave maximum is found on the
+// high 32 bits of the value (order-preserving for non-negative doubles, +1 so
+// that 0 means "no candidate"); lanes that tie there are resolved exactly
+// (full value, then key) one by one, which is rare.  Returns the winning lane
+// (-1 when no lane has a candidate) and sets vmax / kmin to its value and key.
+__device__ __forceinline__ int wave_first_max(double v, int key, double& vmax, int& kmin) {
+  const unsigned hk = v >= 0.0 ? (unsigned)__double2hiint(v) + 1u : 0u;
+  const unsigned mh = wave_umax(hk);
+  if (mh == 0) { vmax = -1.0; kmin = INT32_MAX; return -1; }
+  unsigned long long hit = __ballot(hk == mh);
+  int src = __ffsll(hit) - 1;
+  unsigned blo = (unsigned)__builtin_amdgcn_readlane(__double2loint(v), src);
+  kmin = __builtin_amdgcn_readlane(key, src);
+  hit &= hit - 1;
+  while (hit) {                                    // equal high words (rare)
+    const int l2 = __ffsll(hit) - 1;
+    const unsigned lo2 = (unsigned)__builtin_amdgcn_readlane(__double2loint(v), l2);
+    const int k2 = __builtin_amdgcn_readlane(key, l2);
+    if (lo2 > blo || (lo2 == blo && k2 < kmin)) { blo = lo2; kmin = k2; src = l2; }
+    hit &= hit - 1;
+  }
+  vmax = __hiloint2double((int)(mh - 1u), (int)blo);
+  return src;
+}
+
 }  // namespace ltlt

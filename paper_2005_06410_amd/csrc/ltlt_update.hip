@@ -33,6 +33,7 @@ namespace ltlt {
 
 constexpr int kMT = 128;     // tile edge
 constexpr int kKC = 16;      // K chunk
+constexpr int kLd = kMT + 16;   // LDS row stride of an operand chunk (bank spread)
 constexpr int kUpdateGrid = 512;   // persistent grid: two workgroups on each of 256 CUs
 
 typedef double v4d __attribute__((ext_vector_type(4)));
@@ -56,33 +57,36 @@ template <> struct Mfma<float> {
   static __device__ __forceinline__ int row(int l, int v) { return 4 * (l >> 4) + v; }
 };
 
+// One 128 x kKC chunk of an operand, thread -> column tid / 16, rows
+// (tid % 16) + 16 e, e < 8: each load instruction reads 16 consecutive rows of
+// a column per 16 lanes, and each LDS store writes 16 consecutive entries.
 template <typename T>
 __device__ __forceinline__ void load_chunk(const T* __restrict__ X, int64_t ldx, int m, int K, int r0, int k0,
                                            T (&reg)[8], int tid) {
-  // thread -> column (tid / 16), rows (tid % 16) * 8 .. +8 of a 128 x 16 chunk
   const int col = tid >> 4;
-  const int rr = (tid & 15) * 8;
   const int kk = k0 + col;
-  const int rbase = r0 + rr;
-  if (kk < K && rbase + 8 <= m) {
+  const int rbase = r0 + (tid & 15);
+  if (kk < K && r0 + kMT <= m) {
     const T* p = X + (int64_t)kk * ldx + rbase;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) reg[e] = p[e];
+    for (int e = 0; e < 8; ++e) reg[e] = p[16 * e];
   } else {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const int r = rbase + e;
+      const int r = rbase + 16 * e;
       reg[e] = (kk < K && r < m) ? X[(int64_t)kk * ldx + r] : T(0);
     }
   }
 }
 
+// LDS chunk rows are kLd apart (128 + 16): the four k-rows one fragment read
+// touches then fall on different banks.
 template <typename T>
 __device__ __forceinline__ void store_chunk(T* __restrict__ S, const T (&reg)[8], int tid) {
   const int col = tid >> 4;
-  const int rr = (tid & 15) * 8;
+  const int rr = tid & 15;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) S[col * kMT + rr + e] = reg[e];
+  for (int e = 0; e < 8; ++e) S[col * kLd + rr + 16 * e] = reg[e];
 }
 
 // Old values S(perm[i], perm[c]) of one 16-column slice for the lane's row i
@@ -161,10 +165,10 @@ __device__ __forceinline__ TileRange tiles_of_block(int b, int nblocks, int ntil
 template <typename T>
 __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
   typedef typename Mfma<T>::acc_t acc_t;
-  // operand chunks As[2][kKC*kMT], Bs[2][kKC*kMT]; reused by the epilogue
-  __shared__ __align__(16) T lds[4 * kKC * kMT];
-  T (*As)[kKC * kMT] = reinterpret_cast<T (*)[kKC * kMT]>(lds);
-  T (*Bs)[kKC * kMT] = reinterpret_cast<T (*)[kKC * kMT]>(lds + 2 * kKC * kMT);
+  // operand chunks As[2][kKC*kLd], Bs[2][kKC*kLd]; reused by the epilogue
+  __shared__ __align__(16) T lds[4 * kKC * kLd];
+  T (*As)[kKC * kLd] = reinterpret_cast<T (*)[kKC * kLd]>(lds);
+  T (*Bs)[kKC * kLd] = reinterpret_cast<T (*)[kKC * kLd]>(lds + 2 * kKC * kLd);
   __shared__ int prow[kMT], pcol[kMT];
 
   const int tid = threadIdx.x;
@@ -225,9 +229,9 @@ __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
       const int kr = k4 + (lane >> 4);
       T af[4], bf[4];
 #pragma unroll
-      for (int x = 0; x < 4; ++x) af[x] = as[kr * kMT + wr * 64 + x * 16 + (lane & 15)];
+      for (int x = 0; x < 4; ++x) af[x] = as[kr * kLd + wr * 64 + x * 16 + (lane & 15)];
 #pragma unroll
-      for (int y = 0; y < 4; ++y) bf[y] = bs[kr * kMT + wc * 64 + y * 16 + (lane & 15)];
+      for (int y = 0; y < 4; ++y) bf[y] = bs[kr * kLd + wc * 64 + y * 16 + (lane & 15)];
 #pragma unroll
       for (int x = 0; x < 4; ++x)
 #pragma unroll
@@ -249,7 +253,7 @@ __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
   // values of slice 0 were gathered before the K loop; those of slice y+1 are
   // gathered while slice y is finished.
   constexpr int kEp = 65;                          // padded column stride in LDS
-  static_assert(4 * 16 * kEp <= 4 * kKC * kMT, "epilogue staging must fit the operand LDS");
+  static_assert(4 * 16 * kEp <= 4 * kKC * kLd, "epilogue staging must fit the operand LDS");
   T* stage = lds + wave * (16 * kEp);              // 16 columns x 65 per wave
 #pragma unroll
   for (int y = 0; y < 4; ++y) {
