@@ -9,7 +9,9 @@ device copy (outside the timed events: the factorization works in place).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--nb 128]
                        [--n 16384] [--dtype f64|f32] [--no-cpu-baseline]
-Prints one JSON line.
+                       [--workload factor|batched]
+Prints one JSON line.  `--workload batched` instead times the batched path
+(8192 independent n=64 matrices, factors + Pfaffians) against HBM bandwidth.
 """
 from __future__ import annotations
 
@@ -38,6 +40,8 @@ def parse():
     ap.add_argument("--seed", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--workload", choices=["factor", "batched"], default="factor")
+    ap.add_argument("--batch", type=int, default=8192)
     return ap.parse_args()
 
 
@@ -71,13 +75,13 @@ def cpu_baseline(X, n, target_s):
     }
 
 
-def update_traffic():
-    """HBM bytes per trailing-update launch from the committed counter summary
+def measured_traffic(summary, source):
+    """HBM bytes per launch from a committed counter summary under profiles/
     (two rocprofv3 --pmc passes, FETCH_SIZE and WRITE_SIZE, scaled by a copy of
     known size), or None when the kernel source has changed since."""
     import hashlib
-    summ = os.path.join(ROOT, "profiles", "update_kernel_hbm_traffic_n16384_f64_nb128.md")
-    src = os.path.join(ROOT, "paper_2005_06410_amd", "csrc", "ltlt_update.hip")
+    summ = os.path.join(ROOT, "profiles", summary)
+    src = os.path.join(ROOT, "paper_2005_06410_amd", "csrc", source)
     try:
         fields = {}
         for line in open(summ):
@@ -90,6 +94,82 @@ def update_traffic():
         return float(fields["traffic_bytes_per_launch"])
     except (OSError, KeyError, ValueError):
         return None
+
+
+def run_batched(args):
+    """Batched path: `batch` independent skew-symmetric matrices of order 64
+    (contiguous, column-major), factored and their Pfaffians taken in one
+    call.  HBM-bound: the algorithmic bytes are one read and one write of each
+    strict lower triangle plus ipiv, log|Pf| and sign."""
+    import numpy as np
+    import torch
+
+    import paper_2005_06410_amd as lt
+    import synth
+
+    n, batch = 64, args.batch
+    np_dt = np.float64 if args.dtype == "f64" else np.float32
+    Xs = synth.skew_batch(n, batch, 6 << 32)
+    buf = np.stack([synth.to_colmajor(X) for X in Xs]).astype(np_dt)
+    dev = torch.device("cuda:0")
+    pristine = torch.from_numpy(buf.reshape(-1)).to(dev)
+    work = torch.empty_like(pristine)
+    A = work.as_strided((batch, n, n), (n * n, 1, n))
+    ipiv = torch.empty((batch, n), dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step():
+        work.copy_(pristine)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        lt.factor_batched(A, ipiv=ipiv)
+        e1.record(stream)
+        return e0, e1
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [step() for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    ms = sorted(a.elapsed_time(b) for a, b in evs)
+    ms_step = sum(ms) / len(ms)
+    esz = 8 if args.dtype == "f64" else 4
+    alg_bytes = batch * (2 * esz * n * (n - 1) / 2 + 4 * n + 8 + 4)
+    gbs = alg_bytes / (ms_step * 1e-3) / 1e9
+    out = {
+        "metric": "batched LTL^T + Pfaffian, 8192 x n=64: GB/s of algorithmic HBM bytes",
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": args.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": f"{batch} independent skew-symmetric n=64 {args.dtype} matrices, strict upper iid N(0,1) "
+                        "(per-matrix seeds), factors + Pfaffians",
+            "n": n,
+            "batch": batch,
+        },
+        "roofline": {
+            "kernel": "batched_kernel",
+            "bound": "hbm",
+            "achieved": round(gbs, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(gbs / HBM_PEAK_GBS, 4),
+            "traffic": (measured_traffic("batched_kernel_8192x64_f64.md", "ltlt_batched.hip")
+                        if args.dtype == "f64" and batch == 8192 else None),
+            "algorithmic_bytes": alg_bytes,
+        },
+        "nominal_gflops": round(batch * n ** 3 / 3.0 / (ms_step * 1e-3) / 1e9, 2),
+    }
+    print(json.dumps(out), flush=True)
 
 
 def main():
@@ -109,6 +189,9 @@ def main():
         from paper_2005_06410_amd import build as ltbuild
         ltbuild.build()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.workload == "batched":
+        run_batched(args)
+        return
     dev = torch.device("cuda:0")
     n, nb = args.n, args.nb
     np_dt = np.float64 if args.dtype == "f64" else np.float32
@@ -190,7 +273,7 @@ def main():
             "peak": peak_tf,
             "unit": "TFLOP/s",
             "frac": round(achieved_tf / peak_tf, 4),
-            "traffic": update_traffic(),
+            "traffic": measured_traffic("update_kernel_hbm_traffic_n16384_f64_nb128.md", "ltlt_update.hip"),
             "launches_per_step": up_launches // max(args.steps, 1),
             "avg_launch_ms": round(up_ms / max(up_launches, 1), 5),
         },
