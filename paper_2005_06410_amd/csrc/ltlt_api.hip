@@ -202,6 +202,7 @@ int factor_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, hipStream
       ua.ldl = ldw;
       ua.Bt = Bm;
       ua.ldb = ldw;
+      ua.pad_row = 1;      // bw + m2 + 1 <= n <= ldw: row m2 of each column lies inside the workspace
       ProfScope ps(1, (double)m2 * (double)m2 * (double)bw, s);
       e = launch_update<T>(ua, s);
       if (e != hipSuccess) return hip_err(e);

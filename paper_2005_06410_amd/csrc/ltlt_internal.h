@@ -46,6 +46,7 @@ struct UpdateArgs {
   int64_t ldl;
   const void* Bt;
   int64_t ldb;
+  int pad_row;        // nonzero: row m of every Lx / Bt column is readable (workspace padding)
   int tiles;          // number of 128-row tile rows
 };
 

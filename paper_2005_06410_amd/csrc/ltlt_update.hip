@@ -15,8 +15,11 @@
 //    (v_mfma_f64_16x16x4_f64, or v_mfma_f32_16x16x4_f32 for fp32),
 //    accumulating in registers;
 //  * Lx and Bt are streamed through LDS in K-chunks of 16 columns, double
-//    buffered, with 16-byte coalesced global loads (128 contiguous rows per
-//    column chunk);
+//    buffered.  In fp64 each 128-row column of a chunk goes straight from
+//    global memory into LDS with one global_load_lds_dwordx4 per wave (no
+//    register staging; the copy of chunk k+1 runs under the MFMAs of chunk
+//    k); fp32, and operands whose columns are not 16-byte aligned, take
+//    16-byte coalesced loads staged through registers;
 //  * the epilogue reads the old value through perm (the exchanges of the
 //    panel, applied as a gather: every displaced source lies outside the
 //    block being written, so tiles never race), adds, and writes the lower
@@ -28,6 +31,8 @@
 
 #include "ltlt_device.h"
 #include "ltlt_internal.h"
+
+#include <type_traits>
 
 namespace ltlt {
 
@@ -87,6 +92,29 @@ __device__ __forceinline__ void store_chunk(T* __restrict__ S, const T (&reg)[8]
   const int rr = tid & 15;
 #pragma unroll
   for (int e = 0; e < 8; ++e) S[col * kLd + rr + 16 * e] = reg[e];
+}
+
+// Direct global -> LDS copy of one 128 x kKC chunk (fp64): wave w moves
+// columns 4w .. 4w+3; one global_load_lds_dwordx4 fills one 1 KB LDS column
+// (lane l -> rows 2l, 2l+1).  Rows are clamped into [0, mr2) (mr2 = m rounded
+// up to even: the caller guarantees that range is readable); rows >= m only
+// feed outputs that are masked.  Columns in [K, K4) are zeroed so the last
+// 4-wide MFMA step adds nothing.
+__device__ __forceinline__ void dma_chunk(const double* __restrict__ X, int64_t ldx, int mr2, int K, int K4, int r0,
+                                          int k0, double* S, int wave, int lane) {
+  const int r = min(r0 + 2 * lane, mr2 - 2);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int cl = wave * 4 + j;
+    const int kk = k0 + cl;
+    if (kk < K) {
+      __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)(X + (int64_t)kk * ldx + r),
+                                       (void __attribute__((address_space(3)))*)(S + cl * kLd), 16, 0, 0);
+    } else if (kk < K4) {
+      S[cl * kLd + 2 * lane] = 0.0;
+      S[cl * kLd + 2 * lane + 1] = 0.0;
+    }
+  }
 }
 
 // Old values S(perm[i], perm[c]) of one 16-column slice for the lane's row i
@@ -162,7 +190,7 @@ __device__ __forceinline__ TileRange tiles_of_block(int b, int nblocks, int ntil
   return TileRange{lo + l, hi, cx};
 }
 
-template <typename T>
+template <typename T, bool DMA>
 __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
   typedef typename Mfma<T>::acc_t acc_t;
   // operand chunks As[2][kKC*kLd], Bs[2][kKC*kLd]; reused by the epilogue
@@ -173,7 +201,7 @@ __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wr = wave >> 1, wc = wave & 1;
 
   const TileRange tr = tiles_of_block(blockIdx.x, gridDim.x, a.tiles * (a.tiles + 1) / 2);
@@ -193,16 +221,23 @@ __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
 #pragma unroll
     for (int y = 0; y < 4; ++y) acc[x][y] = acc_t{0, 0, 0, 0};
 
+  const int mr2 = (m + 1) & ~1, K4 = (K + 3) & ~3;
   T ra[8], rb[8];
-  load_chunk<T>(Lx, a.ldl, m, K, r0, 0, ra, tid);
-  load_chunk<T>(Bt, a.ldb, m, K, c0, 0, rb, tid);
-  store_chunk<T>(As[0], ra, tid);
-  store_chunk<T>(Bs[0], rb, tid);
+  if constexpr (DMA) {
+    dma_chunk((const double*)Lx, a.ldl, mr2, K, K4, r0, 0, (double*)As[0], wave, lane);
+    dma_chunk((const double*)Bt, a.ldb, mr2, K, K4, c0, 0, (double*)Bs[0], wave, lane);
+  } else {
+    load_chunk<T>(Lx, a.ldl, m, K, r0, 0, ra, tid);
+    load_chunk<T>(Bt, a.ldb, m, K, c0, 0, rb, tid);
+    store_chunk<T>(As[0], ra, tid);
+    store_chunk<T>(Bs[0], rb, tid);
+  }
   if (tid < kMT) {
     const int ri = r0 + tid, ci = c0 + tid;
     prow[tid] = (a.perm && ri < m) ? a.perm[ri] - a.perm_base : ri;
     pcol[tid] = (a.perm && ci < m) ? a.perm[ci] - a.perm_base : ci;
   }
+  if constexpr (DMA) __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0): this wave's chunk copies landed
   __syncthreads();
 
   // epilogue geometry: lane l of wave (wr, wc) finishes row wr*64 + l of the tile
@@ -219,8 +254,13 @@ __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
     const int cur = ch & 1;
     const bool more = ch + 1 < nchunk;
     if (more) {
-      load_chunk<T>(Lx, a.ldl, m, K, r0, (ch + 1) * kKC, ra, tid);
-      load_chunk<T>(Bt, a.ldb, m, K, c0, (ch + 1) * kKC, rb, tid);
+      if constexpr (DMA) {
+        dma_chunk((const double*)Lx, a.ldl, mr2, K, K4, r0, (ch + 1) * kKC, (double*)As[cur ^ 1], wave, lane);
+        dma_chunk((const double*)Bt, a.ldb, mr2, K, K4, c0, (ch + 1) * kKC, (double*)Bs[cur ^ 1], wave, lane);
+      } else {
+        load_chunk<T>(Lx, a.ldl, m, K, r0, (ch + 1) * kKC, ra, tid);
+        load_chunk<T>(Bt, a.ldb, m, K, c0, (ch + 1) * kKC, rb, tid);
+      }
     }
     const T* as = As[cur];
     const T* bs = Bs[cur];
@@ -237,7 +277,9 @@ __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
 #pragma unroll
         for (int y = 0; y < 4; ++y) acc[x][y] = Mfma<T>::run(af[x], bf[y], acc[x][y]);
     }
-    if (more) {
+    if constexpr (DMA) {
+      __builtin_amdgcn_s_waitcnt(0x0f70);          // vmcnt(0): next chunk landed
+    } else if (more) {
       store_chunk<T>(As[cur ^ 1], ra, tid);
       store_chunk<T>(Bs[cur ^ 1], rb, tid);
     }
@@ -287,7 +329,18 @@ hipError_t launch_update(const UpdateArgs& a, hipStream_t s) {
   UpdateArgs c = a;
   c.tiles = tiles;
   const int64_t grid = nblk < kUpdateGrid ? nblk : kUpdateGrid;
-  hipLaunchKernelGGL(update_kernel<T>, dim3((unsigned)grid), dim3(kThreads), 0, s, c);
+  // direct-to-LDS operand copies need 16-byte aligned column pairs and one
+  // readable row past m when m is odd
+  const bool dma = std::is_same<T, double>::value && (reinterpret_cast<uintptr_t>(a.Lx) % 16 == 0) &&
+             (reinterpret_cast<uintptr_t>(a.Bt) % 16 == 0) && (a.ldl % 2 == 0) && (a.ldb % 2 == 0) &&
+             ((a.m % 2 == 0) || a.pad_row);
+  if constexpr (std::is_same<T, double>::value) {
+    if (dma) {
+      hipLaunchKernelGGL((update_kernel<T, true>), dim3((unsigned)grid), dim3(kThreads), 0, s, c);
+      return hipGetLastError();
+    }
+  }
+  hipLaunchKernelGGL((update_kernel<T, false>), dim3((unsigned)grid), dim3(kThreads), 0, s, c);
   return hipGetLastError();
 }
 

@@ -285,6 +285,41 @@ def test_skew_update_parity(m, K, off, dtype):
     assert np.array_equal(got[:off, :], S[:off, :]) and np.array_equal(got[:, :off], S[:, :off])
 
 
+@pytest.mark.parametrize("layout", ["aligned", "offset1", "odd_ld"])
+def test_skew_update_operand_layouts(layout):
+    """fp64 operands whose columns start 16-byte aligned are copied straight
+    into LDS; an odd start or an odd leading dimension takes the register
+    path.  Both must give the oracle's result (m = 258: three tile rows and a
+    ragged last one; K = 130: a ragged last K chunk)."""
+    m, K = 258, 130
+    rng = synth.rng_for(4242)
+    S = synth.skew_gauss(m, 77)
+    Lx = rng.standard_normal((m, K))
+    Bt = rng.standard_normal((m, K))
+    flat, Cv = device_colmajor(S)
+
+    def place(X):
+        if layout == "aligned":
+            return torch.from_numpy(np.asfortranarray(X)).cuda().t().contiguous().t()
+        ld = m + 1 if layout == "odd_ld" else m
+        start = 1 if layout == "offset1" else 0
+        buf = torch.zeros(start + ld * K + 1, dtype=torch.float64, device="cuda")
+        v = buf[start:start + ld * K].view(K, ld)[:, :m]
+        v.copy_(torch.from_numpy(np.ascontiguousarray(X.T)).cuda())
+        return v.t()
+
+    Ld, Bd = place(Lx), place(Bt)
+    assert Ld.stride() == (1, m + 1 if layout == "odd_ld" else m)
+    lt().skew_update(Cv, Ld, Bd)
+    torch.cuda.synchronize()
+    got = flat.cpu().numpy().reshape(m, m).T
+    ref = oracle.skew_update(S, Lx, Bt, np.arange(m, dtype=np.int64))
+    il = np.tril_indices(m, -1)
+    iu = np.triu_indices(m, 0)
+    assert np.abs(got[il] - ref[il]).max() <= 1e-12 * np.abs(ref).max() * K ** 0.5
+    assert np.array_equal(got[iu], S[iu])
+
+
 # --------------------------------------------------------------------------
 @pytest.mark.parametrize("n,batch,dtype", [(64, 8192, np.float64), (64, 300, np.float32), (1, 5, np.float64),
                                            (2, 5, np.float64), (7, 33, np.float64), (40, 129, np.float64)])
