@@ -9,17 +9,19 @@
 //
 // gfx950 mapping:
 //  * 256-thread workgroups on 128x128 tiles of the LOWER triangle only
-//    (tile row >= tile column), a persistent grid of two workgroups per CU
-//    walking an XCD-aware tile order;
+//    (tile row >= tile column), a persistent grid of three workgroups per CU
+//    walking an XCD-aware tile order (while one drains its epilogue to HBM,
+//    the other two keep the matrix cores busy);
 //  * each of the 4 waves owns a 64x64 sub-tile = 4x4 MFMA blocks of 16x16
 //    (v_mfma_f64_16x16x4_f64, or v_mfma_f32_16x16x4_f32 for fp32),
 //    accumulating in registers;
-//  * Lx and Bt are streamed through LDS in K-chunks of 16 columns, double
-//    buffered.  In fp64 each 128-row column of a chunk goes straight from
-//    global memory into LDS with one global_load_lds_dwordx4 per wave (no
-//    register staging; the copy of chunk k+1 runs under the MFMAs of chunk
-//    k); fp32, and operands whose columns are not 16-byte aligned, take
-//    16-byte coalesced loads staged through registers;
+//  * Lx and Bt are streamed through LDS in K-chunks of 8 columns, double
+//    buffered (37 KB of LDS per workgroup).  In fp64 each 128-row column of
+//    a chunk goes straight from global memory into LDS with one
+//    global_load_lds_dwordx4 per wave (no register staging; the copy of
+//    chunk k+1 runs under the MFMAs of chunk k); fp32, and operands whose
+//    columns are not 16-byte aligned, take coalesced loads staged through
+//    registers;
 //  * the epilogue reads the old value through perm (the exchanges of the
 //    panel, applied as a gather: every displaced source lies outside the
 //    block being written, so tiles never race), adds, and writes the lower
@@ -37,9 +39,10 @@
 namespace ltlt {
 
 constexpr int kMT = 128;     // tile edge
-constexpr int kKC = 16;      // K chunk
+constexpr int kKC = 8;       // K chunk
 constexpr int kLd = kMT + 16;   // LDS row stride of an operand chunk (bank spread)
-constexpr int kUpdateGrid = 512;   // persistent grid: two workgroups on each of 256 CUs
+constexpr int kUpdateGrid = 768;   // persistent grid: three workgroups on each of 256 CUs
+constexpr int kUpdateWgPerCu = 3;
 
 typedef double v4d __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
@@ -62,23 +65,26 @@ template <> struct Mfma<float> {
   static __device__ __forceinline__ int row(int l, int v) { return 4 * (l >> 4) + v; }
 };
 
-// One 128 x kKC chunk of an operand, thread -> column tid / 16, rows
-// (tid % 16) + 16 e, e < 8: each load instruction reads 16 consecutive rows of
-// a column per 16 lanes, and each LDS store writes 16 consecutive entries.
+// One 128 x kKC chunk of an operand, thread -> column tid / kTpc, rows
+// (tid % kTpc) + kTpc e, e < kRpt: each load instruction reads kTpc
+// consecutive rows of a column, and each LDS store writes kTpc consecutive
+// entries.
+constexpr int kTpc = kThreads / kKC;           // threads per chunk column
+constexpr int kRpt = kMT / kTpc;                 // rows per thread
 template <typename T>
 __device__ __forceinline__ void load_chunk(const T* __restrict__ X, int64_t ldx, int m, int K, int r0, int k0,
-                                           T (&reg)[8], int tid) {
-  const int col = tid >> 4;
+                                           T (&reg)[kRpt], int tid) {
+  const int col = tid / kTpc;
   const int kk = k0 + col;
-  const int rbase = r0 + (tid & 15);
+  const int rbase = r0 + (tid % kTpc);
   if (kk < K && r0 + kMT <= m) {
     const T* p = X + (int64_t)kk * ldx + rbase;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) reg[e] = p[16 * e];
+    for (int e = 0; e < kRpt; ++e) reg[e] = p[kTpc * e];
   } else {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int r = rbase + 16 * e;
+    for (int e = 0; e < kRpt; ++e) {
+      const int r = rbase + kTpc * e;
       reg[e] = (kk < K && r < m) ? X[(int64_t)kk * ldx + r] : T(0);
     }
   }
@@ -87,15 +93,16 @@ __device__ __forceinline__ void load_chunk(const T* __restrict__ X, int64_t ldx,
 // LDS chunk rows are kLd apart (128 + 16): the four k-rows one fragment read
 // touches then fall on different banks.
 template <typename T>
-__device__ __forceinline__ void store_chunk(T* __restrict__ S, const T (&reg)[8], int tid) {
-  const int col = tid >> 4;
-  const int rr = tid & 15;
+__device__ __forceinline__ void store_chunk(T* __restrict__ S, const T (&reg)[kRpt], int tid) {
+  const int col = tid / kTpc;
+  const int rr = tid % kTpc;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) S[col * kLd + rr + 16 * e] = reg[e];
+  for (int e = 0; e < kRpt; ++e) S[col * kLd + rr + kTpc * e] = reg[e];
 }
 
 // Direct global -> LDS copy of one 128 x kKC chunk (fp64): wave w moves
-// columns 4w .. 4w+3; one global_load_lds_dwordx4 fills one 1 KB LDS column
+// columns w kKC/4 .. (w+1) kKC/4 - 1; one global_load_lds_dwordx4 fills one
+// 1 KB LDS column
 // (lane l -> rows 2l, 2l+1).  Rows are clamped into [0, mr2) (mr2 = m rounded
 // up to even: the caller guarantees that range is readable); rows >= m only
 // feed outputs that are masked.  Columns in [K, K4) are zeroed so the last
@@ -104,8 +111,8 @@ __device__ __forceinline__ void dma_chunk(const double* __restrict__ X, int64_t 
                                           int k0, double* S, int wave, int lane) {
   const int r = min(r0 + 2 * lane, mr2 - 2);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int cl = wave * 4 + j;
+  for (int j = 0; j < kKC / 4; ++j) {
+    const int cl = wave * (kKC / 4) + j;
     const int kk = k0 + cl;
     if (kk < K) {
       __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)(X + (int64_t)kk * ldx + r),
@@ -156,30 +163,47 @@ __device__ __forceinline__ int tri_index_decode(int b, int& J) {
   return I;
 }
 
-// q-th tile of the grouped order: groups (GI, GJ), GJ <= GI, row-major; full
-// groups hold kGrp*kGrp tiles, diagonal groups kGrp(kGrp+1)/2, edge groups fewer.
-__device__ __forceinline__ void grouped_tile(int q, int tiles, int& I, int& J) {
-  const int ng = (tiles + kGrp - 1) / kGrp;
-  int rem = q;
-  for (int GI = 0; GI < ng; ++GI) {
-    const int hI = min(kGrp, tiles - GI * kGrp);   // row blocks in this group row
-    for (int GJ = 0; GJ <= GI; ++GJ) {
-      const int wJ = min(kGrp, tiles - GJ * kGrp);
-      const int cnt = (GJ < GI) ? hI * wJ : hI * (hI + 1) / 2;
-      if (rem < cnt) {
-        if (GJ < GI) { I = GI * kGrp + rem / wJ; J = GJ * kGrp + rem % wJ; }
-        else { int jj; const int ii = tri_index_decode(rem, jj); I = GI * kGrp + ii; J = GI * kGrp + jj; }
-        return;
-      }
-      rem -= cnt;
-    }
-  }
-  I = 0; J = 0;                                    // not reached for q < number of tiles
+// The grouped order: groups (GI, GJ), GJ <= GI, row-major; full groups hold
+// kGrp*kGrp tiles, diagonal groups hI(hI+1)/2, edge groups fewer.  Group row
+// GI holds GI off-diagonal groups of hI x kGrp tiles (hI = row blocks in the
+// group row) and one diagonal group.  A workgroup's tile indices only grow,
+// so it keeps a cursor on the group row of its last tile: locating the next
+// tile moves over a group row or two instead of walking all groups from the
+// start (that walk ran on the scalar unit that the CU's waves share).
+struct TileCursor { int GI, rowbase; };
+
+__device__ __forceinline__ int group_row_tiles(int GI, int tiles) {
+  const int hI = min(kGrp, tiles - GI * kGrp);
+  return GI * hI * kGrp + hI * (hI + 1) / 2;
 }
 
-// The grid is persistent (at most two workgroups per CU).  XCD x owns the
+__device__ __forceinline__ void grouped_tile(TileCursor& cs, int q, int tiles, int& I, int& J) {
+  const int ng = (tiles + kGrp - 1) / kGrp;
+  while (cs.GI < ng && q >= cs.rowbase + group_row_tiles(cs.GI, tiles)) {
+    cs.rowbase += group_row_tiles(cs.GI, tiles);
+    ++cs.GI;
+  }
+  const int GI = cs.GI;
+  const int hI = min(kGrp, tiles - GI * kGrp);
+  const int off = q - cs.rowbase;
+  const int full = GI * hI * kGrp;               // tiles of the off-diagonal groups
+  if (off < full) {
+    const int GJ = off / (hI * kGrp), rem = off - GJ * (hI * kGrp);
+    I = GI * kGrp + rem / kGrp;
+    J = GJ * kGrp + rem % kGrp;
+  } else {
+    int jj;
+    const int ii = tri_index_decode(off - full, jj);
+    I = GI * kGrp + ii;
+    J = GI * kGrp + jj;
+  }
+}
+
+// The grid is persistent (at most three workgroups per CU).  XCD x owns the
 // x-th contiguous eighth [lo, hi) of the grouped order and its workgroups
-// (blocks b with b % 8 == x) take those tiles in turn.
+// (blocks b with b % 8 == x) take those tiles in turn.  Every tile is covered
+// when the grid has at least 8 blocks or one block per tile (the launch uses
+// min(tiles, kUpdateGrid) blocks).
 struct TileRange { int q, hi, step; };
 __device__ __forceinline__ TileRange tiles_of_block(int b, int nblocks, int ntiles) {
   const int x = b % kXcd, l = b / kXcd;
@@ -191,7 +215,7 @@ __device__ __forceinline__ TileRange tiles_of_block(int b, int nblocks, int ntil
 }
 
 template <typename T, bool DMA>
-__global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
+__global__ void __launch_bounds__(kThreads, kUpdateWgPerCu) update_kernel(UpdateArgs a) {
   typedef typename Mfma<T>::acc_t acc_t;
   // operand chunks As[2][kKC*kLd], Bs[2][kKC*kLd]; reused by the epilogue
   __shared__ __align__(16) T lds[4 * kKC * kLd];
@@ -205,10 +229,11 @@ __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
   const int wr = wave >> 1, wc = wave & 1;
 
   const TileRange tr = tiles_of_block(blockIdx.x, gridDim.x, a.tiles * (a.tiles + 1) / 2);
+  TileCursor cursor{0, 0};
   for (int q = tr.q; q < tr.hi; q += tr.step) {
   __syncthreads();                                 // LDS of the previous tile is free
   int I, J;
-  grouped_tile(q, a.tiles, I, J);
+  grouped_tile(cursor, q, a.tiles, I, J);
   const int r0 = I * kMT, c0 = J * kMT;
   const int m = a.m, K = a.K;
 
@@ -222,7 +247,7 @@ __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
     for (int y = 0; y < 4; ++y) acc[x][y] = acc_t{0, 0, 0, 0};
 
   const int mr2 = (m + 1) & ~1, K4 = (K + 3) & ~3;
-  T ra[8], rb[8];
+  T ra[kRpt], rb[kRpt];
   if constexpr (DMA) {
     dma_chunk((const double*)Lx, a.ldl, mr2, K, K4, r0, 0, (double*)As[0], wave, lane);
     dma_chunk((const double*)Bt, a.ldb, mr2, K, K4, c0, 0, (double*)Bs[0], wave, lane);
@@ -246,8 +271,6 @@ __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
   const int rl = wr * 64 + lane;
   const int i = r0 + rl;
   const int pr = prow[rl];
-  T oldv[16];
-  gather_slice<T>(C, ldc, m, i, pr, pcol, c0, wc * 64, oldv);   // slice 0, in flight during the K loop
 
   const int nchunk = (K + kKC - 1) / kKC;
   for (int ch = 0; ch < nchunk; ++ch) {
@@ -292,8 +315,9 @@ __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
   // instead writes one 16-column slice of its 64x64 sub-tile to LDS
   // ([column][row], padded), then lane l handles row l of each column: every
   // load/store instruction covers 64 consecutive rows of one column.  The old
-  // values of slice 0 were gathered before the K loop; those of slice y+1 are
-  // gathered while slice y is finished.
+  // values of a slice are gathered after it is staged (at 168 VGPRs there is
+  // no room to hold them across the K loop); their latency is covered by the
+  // other workgroups on the CU.
   constexpr int kEp = 65;                          // padded column stride in LDS
   static_assert(4 * 16 * kEp <= 4 * kKC * kLd, "epilogue staging must fit the operand LDS");
   T* stage = lds + wave * (16 * kEp);              // 16 columns x 65 per wave
@@ -305,18 +329,14 @@ __global__ void __launch_bounds__(kThreads, 2) update_kernel(UpdateArgs a) {
       for (int v = 0; v < 4; ++v)
         stage[(lane & 15) * kEp + x * 16 + Mfma<T>::row(lane, v)] = acc[x][y][v];
     __builtin_amdgcn_s_waitcnt(0xc07f);            // lgkmcnt(0): this wave's LDS writes done
-    T nextv[16];
-    if (y < 3) gather_slice<T>(C, ldc, m, i, pr, pcol, c0, wc * 64 + (y + 1) * 16, nextv);
+    T oldv[16];
+    gather_slice<T>(C, ldc, m, i, pr, pcol, c0, wc * 64 + y * 16, oldv);
 #pragma unroll
     for (int cc = 0; cc < 16; ++cc) {
       const int c = c0 + wc * 64 + y * 16 + cc;
       if ((i > c) && (i < m)) C[(int64_t)i + (int64_t)c * ldc] = oldv[cc] + stage[cc * kEp + lane];
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);            // reads of this slice done before it is overwritten
-    if (y < 3) {
-#pragma unroll
-      for (int cc = 0; cc < 16; ++cc) oldv[cc] = nextv[cc];
-    }
   }
   }
 }
