@@ -220,6 +220,8 @@ def main():
         step_events()
     torch.cuda.synchronize()
     lt.device_status()
+    # measured matrix-core ceiling of this device (register-only MFMA loop)
+    loop_peak_tf = lt.mfma_probe(args.dtype)
 
     lt.profile_enable(True)
     torch.cuda.synchronize()
@@ -273,6 +275,8 @@ def main():
             "peak": peak_tf,
             "unit": "TFLOP/s",
             "frac": round(achieved_tf / peak_tf, 4),
+            "measured_loop_peak": round(loop_peak_tf, 2),
+            "frac_of_measured_loop_peak": round(achieved_tf / loop_peak_tf, 4) if loop_peak_tf > 0 else None,
             "traffic": measured_traffic("update_kernel_hbm_traffic_n16384_f64_nb128.md", "ltlt_update.hip"),
             "launches_per_step": up_launches // max(args.steps, 1),
             "avg_launch_ms": round(up_ms / max(up_launches, 1), 5),

@@ -177,6 +177,21 @@ int ltlt_profile_read(int nkinds, int64_t* launches, double* ms, double* flops);
 /* Frees the cached workspace of every device (host call; synchronizes). */
 int ltlt_release_workspace(void);
 
+/*
+ * ltlt_mfma_probe -- measured matrix-core rate of the current device.  A
+ * diagnostic, not part of the factorization: it runs, on `stream`, one
+ * kernel in which every wave executes `iters` iterations of 16 independent
+ * 16x16x4 MFMAs (fp64 for LTLT_F64, fp32 for LTLT_F32) from registers, two
+ * workgroups of four waves per CU, times it with HIP events and writes the
+ * sustained TFLOP/s into the HOST double *tflops.  This is the ceiling an
+ * MFMA kernel can reach on the device, used to state a kernel's rate as a
+ * fraction of it next to the published peak.  Allocates and frees a small
+ * device buffer; synchronizes the stream.
+ * Returns 0, -1 (bad dtype), -2 (iters outside [1, 1e8]), -3 (tflops NULL)
+ * or a runtime error.
+ */
+int ltlt_mfma_probe(int dtype, int64_t iters, double* tflops, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -60,6 +60,7 @@ _SYMBOLS = {
     "ltlt_profile_enable": ([ctypes.c_int], ctypes.c_int),
     "ltlt_profile_read": ([ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "ltlt_release_workspace": ([], ctypes.c_int),
+    "ltlt_mfma_probe": ([ctypes.c_int, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
 }
 
 
@@ -256,3 +257,14 @@ def profile_read():
 
 def release_workspace():
     _check("ltlt_release_workspace", load().ltlt_release_workspace())
+
+
+def mfma_probe(dtype: str = "f64", iters: int = 20000, device=None) -> float:
+    """Sustained TFLOP/s of a register-only MFMA loop on the device (see
+    ``ltlt_mfma_probe``)."""
+    torch = _torch()
+    dev = device if device is not None else torch.cuda.current_device()
+    out = ctypes.c_double(0.0)
+    code = load().ltlt_mfma_probe(0 if dtype == "f64" else 1, int(iters), ctypes.addressof(out), _stream_ptr(dev))
+    _check("ltlt_mfma_probe", code)
+    return float(out.value)

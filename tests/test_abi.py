@@ -31,7 +31,7 @@ def test_header_declares_the_entry_points():
     names = declared_functions()
     for must in ["ltlt_factor", "ltlt_factor_nb", "ltlt_pfaffian", "ltlt_factor_batched",
                  "ltlt_skew_update", "ltlt_device_status", "ltlt_profile_enable",
-                 "ltlt_profile_read", "ltlt_release_workspace"]:
+                 "ltlt_profile_read", "ltlt_release_workspace", "ltlt_mfma_probe"]:
         assert must in names
 
 
@@ -114,6 +114,18 @@ def test_pfaffian_argument_checks(lib, args, code):
 ])
 def test_skew_update_argument_checks(lib, args, code):
     assert lib.ltlt_skew_update(*args) == code
+
+
+@pytest.mark.parametrize("args,code", [
+    ((7, 10, "ok"), -1),           # bad dtype
+    ((0, 0, "ok"), -2),            # iters < 1
+    ((0, 100000001, "ok"), -2),    # iters > 1e8
+    ((1, 10, None), -3),           # tflops NULL
+])
+def test_mfma_probe_argument_checks(lib, args, code):
+    dtype, iters, ptr = args
+    out = ctypes.c_double(0.0)
+    assert lib.ltlt_mfma_probe(dtype, iters, ctypes.addressof(out) if ptr else None, None) == code
 
 
 def test_error_messages():

@@ -354,3 +354,12 @@ def test_batched_parity(n, batch, dtype):
     full = np.transpose(d.cpu().numpy(), (0, 2, 1))
     iu = np.triu_indices(n, 0)
     assert np.array_equal(full[:, iu[0], iu[1]], Xs[:, iu[0], iu[1]])
+
+
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("dtype,published", [("f64", 78.6), ("f32", 157.3)])
+def test_mfma_probe_rate(dtype, published):
+    """The measured register-only MFMA loop rate lies between half of the
+    published dense peak and the peak itself (plus clock headroom)."""
+    rate = lt().mfma_probe(dtype, iters=4000)
+    assert 0.5 * published <= rate <= 1.1 * published, rate
