@@ -13,6 +13,10 @@ What it computes (textbook definitions, written out plainly):
   trailing strict lower triangle.
 * ``pfaffian`` -- Pf(X) = det(P) * prod_j T(2j, 2j+1), returned as
   (log|Pf|, sign), from Pf(B X B^T) = det(B) Pf(X).
+* ``pfaffian_direct`` -- the same Pfaffian from the even column steps only
+  (pivot, exchange, multipliers and rank-2 update at k = 0, 2, 4, ...; the
+  odd columns are never eliminated because after step k row k has one
+  nonzero entry and the Pfaffian expands along it).
 * ``skew_update`` -- the definition of one trailing-matrix block update of
   the blocked method: new(i, c) = S(perm[i], perm[c]) + (Lx @ B^T)(i, c) on
   the strict lower triangle, with the mirrored upper entry, via one numpy
@@ -71,6 +75,9 @@ def _load():
             lib.oracle_swap_f64.restype = None
             for name in ("oracle_pfaffian_f64", "oracle_pfaffian_f32"):
                 getattr(lib, name).argtypes = [i64, p, i64, p, p, p]
+                getattr(lib, name).restype = None
+            for name in ("oracle_pfaffian_direct_f64", "oracle_pfaffian_direct_f32"):
+                getattr(lib, name).argtypes = [i64, p, i64, p]
                 getattr(lib, name).restype = None
             for name in ("oracle_ltlt_batched_f64", "oracle_ltlt_batched_f32"):
                 getattr(lib, name).argtypes = [i64, i64, p, i64, i64, p, i64, p, p]
@@ -134,6 +141,26 @@ def pfaffian(X: np.ndarray):
     """(log|Pf(X)|, sign) of a skew matrix via the factorization."""
     packed, ipiv = ltlt(X)
     return pfaffian_packed(packed, ipiv)
+
+
+def pfaffian_direct(X: np.ndarray):
+    """Pfaffian by the even column steps only (the odd columns are never
+    eliminated: after step k, row k has the single entry T(k, k+1), and the
+    Pfaffian expands along it).
+
+    Returns ``(logabs, sign, alpha, ipiv)``: alpha[i] = alpha_{2i} of the even
+    steps (n/2 values), ipiv the 0-based pivots with ipiv[k+1] = p_k for even
+    k and ipiv[i] = i elsewhere.  Odd n gives (-inf, 0, [], identity)."""
+    lib = _load()
+    n = X.shape[0]
+    buf = np.ascontiguousarray(X.T)          # column-major image of X
+    ipiv = np.zeros(max(n, 1), dtype=np.int32)
+    getattr(lib, "oracle_pfaffian_direct_" + _sfx(buf.dtype))(n, buf.ctypes.data, n, ipiv.ctypes.data)
+    ipiv = ipiv[:n]
+    out = np.tril(buf.T, -1)
+    alpha = np.array([out[k + 1, k] for k in range(0, n - 1, 2)] if n % 2 == 0 else [], dtype=buf.dtype)
+    logabs, sign = pfaffian_packed(np.ascontiguousarray(out), ipiv)
+    return logabs, sign, alpha, ipiv
 
 
 def ltlt_batched(Xs: np.ndarray):

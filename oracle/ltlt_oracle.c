@@ -53,6 +53,12 @@ void oracle_pfaffian_f32(int64_t n, const float* A, int64_t lda, const int32_t* 
                          double* logabs, int32_t* sign)
 { pfaffian_f32(n, A, lda, ipiv, logabs, sign); }
 
+void oracle_pfaffian_direct_f64(int64_t n, double* A, int64_t lda, int32_t* ipiv)
+{ pfaffian_direct_f64(n, A, lda, ipiv); }
+
+void oracle_pfaffian_direct_f32(int64_t n, float* A, int64_t lda, int32_t* ipiv)
+{ pfaffian_direct_f32(n, A, lda, ipiv); }
+
 /* Batched: `batch` matrices, matrix b at A + b*strideA, pivots at
  * ipiv + b*strideIpiv, one after the other. */
 void oracle_ltlt_batched_f64(int64_t n, int64_t batch, double* A, int64_t lda, int64_t strideA,

@@ -114,3 +114,52 @@ static void CAT(pfaffian, SFX)(int64_t n, const REAL* A, int64_t lda, const int3
     *logabs = acc;
     *sign = s;
 }
+
+/* Pfaffian by the even column steps only (no factorization output).
+ * Step k = 0, 2, 4, ..., n-2 on the current matrix:
+ *   1. p = first index r >= k+1 maximising |X(r, k)|; ipiv[k+1] = p;
+ *      exchange indices k+1 and p
+ *   2. alpha_k = X(k+1, k); l_r = X(r, k) / alpha_k for r >= k+2
+ *      (l = 0 when alpha_k = 0)
+ *   3. X <- M X M^T, M = I - l e_{k+1}^T: the same skew rank-2 update of the
+ *      trailing strict lower triangle as a full step,
+ *      X(i, j) += l_i v_j - v_i l_j (i > j >= k+2),  v = X(k+2:, k+1).
+ * After step 3, row k of X has the single nonzero X(k, k+1) = -alpha_k, so
+ * expanding the Pfaffian along row k gives Pf = X(k, k+1) Pf(X without k and
+ * k+1): column k+1 is never eliminated and the next step is k+2.  With
+ * det(M) = 1 and one sign flip per exchange,
+ *   Pf(X) = (-1)^(#exchanges) prod_{k even} (-alpha_k).
+ * On exit A(k+1, k) = alpha_k for even k (other entries hold intermediate
+ * values), ipiv[k+1] = p_k for even k and ipiv[i] = i otherwise; the
+ * Pfaffian of the result is read by `pfaffian` above.  Odd n: no steps
+ * (Pf = 0). */
+static void CAT(pfaffian_direct, SFX)(int64_t n, REAL* A, int64_t lda, int32_t* ipiv)
+{
+    int64_t i, j, k, r, p;
+    REAL best, alpha;
+    REAL* v;
+
+    for (i = 0; i < n; ++i) ipiv[i] = (int32_t)i;
+    if (n % 2 != 0 || n < 2) return;
+    v = (REAL*)malloc((size_t)n * sizeof(REAL));
+    if (!v) return;
+    for (k = 0; k + 1 < n; k += 2) {
+        p = k + 1;
+        best = FABS(AT(k + 1, k));
+        for (r = k + 2; r < n; ++r) {
+            if (FABS(AT(r, k)) > best) { best = FABS(AT(r, k)); p = r; }
+        }
+        ipiv[k + 1] = (int32_t)p;
+        if (p != k + 1) CAT(swap_indices, SFX)(n, A, lda, k + 1, p);
+        alpha = AT(k + 1, k);
+        for (r = k + 2; r < n; ++r) AT(r, k) = (alpha != (REAL)0) ? AT(r, k) / alpha : (REAL)0;
+        for (r = k + 2; r < n; ++r) v[r] = AT(r, k + 1);
+        for (j = k + 2; j < n; ++j) {
+            REAL lj = AT(j, k), vj = v[j];
+            for (i = j + 1; i < n; ++i) {
+                AT(i, j) = AT(i, j) + (AT(i, k) * vj - v[i] * lj);
+            }
+        }
+    }
+    free(v);
+}
