@@ -101,6 +101,32 @@ int ltlt_pfaffian(int64_t n, const void* A, int64_t lda, int dtype, const int32_
                   double* logabs, int32_t* sign, hipStream_t stream);
 
 /*
+ * ltlt_pfaffian_direct -- Pf(X) without the factors: the pivoted reduction
+ * run on the even column steps only.  After column k is eliminated with
+ * pivot row k+1, row k of the transformed matrix has the single entry
+ * T(k, k+1) = -alpha_k, so the Pfaffian expands along it into -alpha_k times
+ * the Pfaffian of the matrix without indices k and k+1; column k+1 is never
+ * eliminated.  With Pf(B X B^T) = det(B) Pf(X) for the unit lower
+ * elimination matrices and the exchanges,
+ *   Pf(X) = (-1)^(#exchanges) prod_{k even} (-alpha_k),
+ * from half the pivot searches of ltlt_factor (the paper does not treat
+ * Pfaffians; this follows from the two identities above).
+ *   n, A, lda, dtype: as ltlt_factor.  A is used as workspace: on exit
+ *       A(k+1, k) = alpha_k for even k; every other entry of the strict lower
+ *       triangle is unspecified; diagonal and upper triangle untouched.
+ *   ipiv (device int32[n]): ipiv[k+1] = pivot of even step k (first index of
+ *       the largest magnitude in the current column k, rows >= k+1),
+ *       ipiv[i] = i elsewhere.
+ *   nb: columns per block, even, 2 .. 256; 0 selects the default (128).
+ *   logabs, sign: DEVICE double / int32 outputs as in ltlt_pfaffian (odd n:
+ *       sign 0, logabs -inf; n = 0: sign 1, logabs 0).
+ * Returns 0, -i when argument i is invalid (nb odd or out of range: -6), or
+ * a runtime / device-wait error as ltlt_factor.  Stream-ordered.
+ */
+int ltlt_pfaffian_direct(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, int64_t nb,
+                         double* logabs, int32_t* sign, hipStream_t stream);
+
+/*
  * ltlt_factor_batched -- independent factorizations and Pfaffians of `batch`
  * matrices of order n <= LTLT_BATCHED_MAX_N, one workgroup per matrix.
  *   n          (1) order, 0 <= n <= LTLT_BATCHED_MAX_N.

@@ -61,6 +61,8 @@ _SYMBOLS = {
     "ltlt_profile_read": ([ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "ltlt_release_workspace": ([], ctypes.c_int),
     "ltlt_mfma_probe": ([ctypes.c_int, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
+    "ltlt_pfaffian_direct": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
+                              ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
 }
 
 
@@ -176,6 +178,25 @@ def pfaffian(A, ipiv):
                              sign.data_ptr(), _stream_ptr(A.device))
     _check("ltlt_pfaffian", code)
     return logabs, sign
+
+
+def pfaffian_direct(A, nb: int = 0, ipiv=None):
+    """Pf(X) of the column-major skew matrix ``A`` from the even column steps
+    only (see ``ltlt_pfaffian_direct``); ``A`` is used as workspace.
+
+    Returns (ipiv int32 (n,), logabs f64 (1,), sign int32 (1,)) device tensors."""
+    torch = _torch()
+    _require_gpu(A)
+    lda = _colmajor_lda(A)
+    n = A.shape[0]
+    if ipiv is None:
+        ipiv = torch.empty(max(n, 1), dtype=torch.int32, device=A.device)
+    logabs = torch.empty(1, dtype=torch.float64, device=A.device)
+    sign = torch.empty(1, dtype=torch.int32, device=A.device)
+    code = load().ltlt_pfaffian_direct(n, A.data_ptr(), lda, _dtype_code(A), ipiv.data_ptr(), int(nb),
+                                       logabs.data_ptr(), sign.data_ptr(), _stream_ptr(A.device))
+    _check("ltlt_pfaffian_direct", code)
+    return ipiv[:n], logabs, sign
 
 
 def factor_batched(A, ipiv=None):

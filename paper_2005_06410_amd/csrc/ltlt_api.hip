@@ -223,6 +223,109 @@ int factor_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, hipStream
   return 0;
 }
 
+// Pfaffian by the even column steps only (see ltlt_pair.hip): blocks of nb
+// columns, nb/2 steps each; every block is a pair panel, a rank-nb trailing
+// update of positions >= j+nb (no carry column), then the block's alphas into
+// A(k+1, k).  The Pfaffian is read off at the end from those alphas and the
+// pivots, by the same kernel as for the full factorization.
+template <typename T>
+int pfaffian_direct_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, double* logabs, int32_t* sign,
+                         hipStream_t s) {
+  if (n64 >= kMaxOrder) return LTLT_ERR_UNSUPPORTED;
+  const int n = (int)n64;
+  hipError_t e = hipSuccess;
+  if (n == 0 || (n & 1)) {                       // Pf = 1 (n = 0) or 0 (odd n): no steps
+    void* ws = nullptr;
+    int* status = nullptr;
+    e = workspace(256, &ws, &status);
+    if (e == hipSuccess && n > 0) e = launch_init(ipiv, n, status, s);
+    if (e == hipSuccess) e = launch_pfaffian<T>(n, A, lda, ipiv, logabs, sign, s);
+    return e == hipSuccess ? 0 : hip_err(e);
+  }
+  const int bw0 = std::min(nb, n);
+  const int R = panel_rows(bw0);
+  if (pair_lds_bytes<T>(bw0, R) > kLdsBudget) return LTLT_ERR_UNSUPPORTED;
+  const int Pmax = (n - 1 + R - 1) / R;
+  const int cap = pair_max_blocks<T>(bw0, pair_lds_bytes<T>(bw0, R));
+  if (cap <= 0 || Pmax > cap) return LTLT_ERR_UNSUPPORTED;
+
+  const int64_t ldw = ((int64_t)n + 63) / 64 * 64;
+  Carve cv;
+  const size_t o_PO = cv.take<T>((size_t)ldw * nb);
+  const size_t o_Bm = cv.take<T>((size_t)ldw * nb);
+  const size_t o_G = cv.take<T>((size_t)ldw * nb);
+  const size_t o_al = cv.take<T>((size_t)nb);
+  const size_t o_T = cv.take<int>((size_t)n);
+  const int nrec = Pmax;
+  const size_t o_rec = cv.take<uint64_t>((size_t)2 * kRecStride * nrec);
+  void* ws = nullptr;
+  int* status = nullptr;
+  e = workspace(cv.off, &ws, &status);
+  if (e != hipSuccess) return hip_err(e);
+  char* base = static_cast<char*>(ws);
+  T* PO = reinterpret_cast<T*>(base + o_PO);
+  T* Bm = reinterpret_cast<T*>(base + o_Bm);
+  T* Gm = reinterpret_cast<T*>(base + o_G);
+  T* al = reinterpret_cast<T*>(base + o_al);
+  int* Tperm = reinterpret_cast<int*>(base + o_T);
+  uint64_t* rec = reinterpret_cast<uint64_t*>(base + o_rec);
+  {
+    ProfScope ps(3, 0.0, s);
+    e = launch_init(ipiv, n, status, s);
+    if (e == hipSuccess) e = launch_rec_init(rec, nrec, s);
+  }
+  if (e != hipSuccess) return hip_err(e);
+
+  for (int j = 0; j < n; j += nb) {
+    const int bw = std::min(nb, n - j);          // even: n and nb are
+    const int m = n - j - 1;                     // rows at positions j+1 .. n-1
+    PanelArgs pa{};
+    pa.A = A; pa.lda = lda; pa.n = n; pa.j = j; pa.bw = bw;
+    pa.R = panel_rows(bw);
+    pa.P = (m + pa.R - 1) / pa.R;
+    pa.nrec = nrec;
+    pa.G = Gm; pa.PO = PO; pa.Bm = Bm; pa.ldw = ldw; pa.alpha = al;
+    pa.perm = Tperm;
+    pa.ipiv = ipiv;
+    pa.rec = rec;
+    pa.status = status;
+    {
+      ProfScope ps(0, 0.0, s);
+      e = launch_pair_panel<T>(pa, pair_lds_bytes<T>(bw, pa.R), s);
+    }
+    if (e != hipSuccess) return hip_err(e);
+    const int i0 = j + bw;
+    const int m2 = n - i0;
+    if (m2 >= 2) {
+      UpdateArgs ua{};
+      ua.C = A + (int64_t)i0 + (int64_t)i0 * lda;
+      ua.ldc = lda;
+      ua.m = m2;
+      ua.perm = Tperm + i0;
+      ua.perm_base = i0;
+      ua.K = bw;
+      ua.Lx = PO;
+      ua.ldl = ldw;
+      ua.Bt = Bm;
+      ua.ldb = ldw;
+      ua.pad_row = 1;      // m2 < n <= ldw: row m2 of each column lies inside the workspace
+      ProfScope ps(1, (double)m2 * (double)m2 * (double)bw, s);
+      e = launch_update<T>(ua, s);
+      if (e != hipSuccess) return hip_err(e);
+    }
+    {
+      ProfScope ps(2, 0.0, s);
+      e = launch_pair_commit<T>(A, lda, j, bw / 2, al, s);
+    }
+    if (e != hipSuccess) return hip_err(e);
+  }
+  {
+    ProfScope ps(3, 0.0, s);
+    e = launch_pfaffian<T>(n, A, lda, ipiv, logabs, sign, s);
+  }
+  return e == hipSuccess ? 0 : hip_err(e);
+}
+
 bool bad_dtype(int d) { return d != LTLT_F64 && d != LTLT_F32; }
 
 }  // namespace
@@ -260,6 +363,22 @@ int ltlt_pfaffian(int64_t n, const void* A, int64_t lda, int dtype, const int32_
   else
     e = launch_pfaffian<float>((int)n, static_cast<const float*>(A), lda, ipiv, logabs, sign, stream);
   return e == hipSuccess ? 0 : hip_err(e);
+}
+
+int ltlt_pfaffian_direct(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, int64_t nb, double* logabs,
+                         int32_t* sign, hipStream_t stream) {
+  if (n < 0 || n > (int64_t)INT32_MAX / 2) return -1;
+  if (A == nullptr && n > 0) return -2;
+  if (lda < std::max<int64_t>(1, n)) return -3;
+  if (bad_dtype(dtype)) return -4;
+  if (ipiv == nullptr && n > 0) return -5;
+  if (nb == 0) nb = kDefaultNb;
+  if (nb < 2 || nb > kMaxNb || (nb & 1)) return -6;
+  if (logabs == nullptr) return -7;
+  if (sign == nullptr) return -8;
+  if (dtype == LTLT_F64)
+    return pfaffian_direct_impl<double>(n, static_cast<double*>(A), lda, ipiv, (int)nb, logabs, sign, stream);
+  return pfaffian_direct_impl<float>(n, static_cast<float*>(A), lda, ipiv, (int)nb, logabs, sign, stream);
 }
 
 int ltlt_factor_batched(int64_t n, int64_t batch, void* A, int64_t lda, int64_t strideA, int dtype,

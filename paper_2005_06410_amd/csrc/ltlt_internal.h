@@ -70,4 +70,11 @@ hipError_t launch_perm_chain(const int* Tblk, int nb, int nblk, int n, int* G, h
 template <typename T> int panel_max_blocks(int bw, size_t lds);
 int panel_rows(int bw);
 
+// Pfaffian-only path (even column steps): the pair panel and the commit of
+// its alphas.
+template <typename T> size_t pair_lds_bytes(int bw, int R);
+template <typename T> int pair_max_blocks(int bw, size_t lds);
+template <typename T> hipError_t launch_pair_panel(const PanelArgs& a, size_t lds, hipStream_t s);
+template <typename T> hipError_t launch_pair_commit(T* A, int64_t lda, int j, int nt, const T* alpha, hipStream_t s);
+
 }  // namespace ltlt

@@ -1,0 +1,392 @@
+// Pfaffian-only path: the even column steps of the pivoted reduction.
+//
+// After column k is eliminated with pivot row k+1 (pivot search, exchange,
+// multipliers l = column k / alpha_k, skew rank-2 update of the trailing
+// matrix with l and v = column k+1), row k of the matrix has the single
+// nonzero -alpha_k at column k+1, so the Pfaffian expands along it:
+//   Pf(X) = det(P) (-alpha_k) Pf(X without indices k and k+1).
+// Column k+1 is therefore never eliminated; the next step is column k+2, and
+// Pf(X) = (-1)^(#exchanges) prod_{k even} (-alpha_k).  Half the column steps,
+// so half the grid-wide pivot agreements of the full reduction.
+//
+// Pair panel (one block of bw columns, bw/2 steps, rows at positions >= j+1),
+// same thread layout, register slots and exchange as the full panel.  Step u
+// leaves two slots in every row still in play: slot 2u = l_u (multiplier)
+// and slot 2u+1 = w_u (column k+1 below row k+1, refreshed: the v of the
+// rank-2 update).  The updates pending within the block are
+//   sum_u l_u w_u^T - w_u l_u^T = Lp J Lp^T,   J = diag([[0, 1], [-1, 0]]),
+// so column c of the current matrix at row i is
+//   S(pos[i], q_c) + sum_s Lp[s][i] g_s,   g_{2u} = w_u(row c), g_{2u+1} = -l_u(row c),
+// with q_c the block-start index of the row at position c.  Per step k:
+//   1. pivot of column k (rows at positions >= k+1), exchange;
+//   2. l = cv / alpha_k (slot 2u);
+//   3. loads: S(pos, posw) and S(pos, q) for the stored parts of columns k+1
+//      and k+2 (q = row now at position k+2), the slots of rows posw and q;
+//   4. the two newest slots of row q (its l_u and w_u), which every lane needs
+//      in the g of column k+2, are recomputed by every wave from row q's slots
+//      and the g's of columns k and k+1 (two short dot products), so no
+//      second agreement per step is needed;
+//   5. one pass over the slots forms w (column k+1, slot 2u+1) and the next
+//      column k+2.
+// Outputs of the block for the trailing rows (positions >= j+bw): Lx = Lp in
+// slot order and Bt = Lp J^T (Bt column 2u = w_u, 2u+1 = -l_u), one rank-bw
+// product for the trailing update; alpha_k and the pivots.
+
+#include "ltlt_device.h"
+#include "ltlt_exchange.h"
+#include "ltlt_internal.h"
+
+namespace ltlt {
+
+// LDS per wave (elements of T, then ints): the slots of the pivot row (TOT),
+// of row q (TOT), the g of the current column by slot (TOT), and the list of
+// positions that received a displaced row: (position, block-start index).
+__host__ __device__ constexpr int pair_wave_lds_bytes(int tot, int tsize) {
+  return 3 * tot * tsize + 2 * tot * 4;
+}
+template <typename T>
+size_t pair_lds_bytes(int bw, int /*R*/) {
+  return (size_t)kPanelWaves * pair_wave_lds_bytes(KC * panel_split(bw), (int)sizeof(T));
+}
+
+// Row g of the slots held in buf (slot s of a row: s = 2u -> l_u, 2u+1 -> w_u):
+// g_{2u} = w_u, g_{2u+1} = -l_u, for slots s < ns; 0 elsewhere.
+template <typename T>
+__device__ __forceinline__ T g_of(const T* buf, int s, int ns) {
+  if (s >= ns) return T(0);
+  return (s & 1) ? -buf[s - 1] : buf[s + 1];
+}
+
+// Wave-wide sum (every lane gets it), fixed order.
+template <typename T>
+__device__ __forceinline__ T wave_sum(T v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+template <typename T, int S>
+__global__ void __launch_bounds__(kPanelThreads, 1) pair_panel_kernel(PanelArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  constexpr int R = kPanelThreads / S;
+  constexpr int RW = kWave / S;                    // rows per wave
+  constexpr int NG = KC / 16;                      // g registers
+  constexpr int TOT = KC * S;                      // slots a row can hold
+  constexpr int NLQ = TOT / kWave;                 // slot loads per lane and row
+  static_assert(NG == 4, "four g registers");
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const int w = blockIdx.x;
+  const int bw = a.bw, n = a.n, j = a.j;
+  const int nt = bw / 2;                           // steps of this block
+  const int part = lane / RW;
+  const int rloc = wave * RW + lane % RW;
+  const int64_t lda = a.lda, ldw = a.ldw;
+  const T* A = static_cast<const T*>(a.A);
+  T* G = static_cast<T*>(a.G);
+
+  unsigned char* wl = smem + (size_t)wave * pair_wave_lds_bytes(TOT, (int)sizeof(T));
+  T* bufB = reinterpret_cast<T*>(wl);              // slots of the pivot row
+  T* bufQ = bufB + TOT;                            // slots of row q
+  T* gcol = bufQ + TOT;                            // g of the current column, by slot
+  int* moved_pos = reinterpret_cast<int*>(gcol + TOT);
+  int* moved_idx = moved_pos + TOT;
+  __shared__ int s_p, s_posw, s_abort;
+  __shared__ double red_v[kPanelWaves];
+  __shared__ uint64_t red_k[kPanelWaves];
+  __shared__ T s_alpha;
+
+  const int row0 = j + 1 + w * R;
+  const int rows_here = max(0, min(R, n - row0));
+  const bool my_row = rloc < rows_here;
+  const int pos = row0 + rloc;
+  int lp = pos;
+
+  T L[KC], grA[NG], grB[NG];
+#pragma unroll
+  for (int c = 0; c < KC; ++c) L[c] = T(0);
+#pragma unroll
+  for (int k4 = 0; k4 < NG; ++k4) { grA[k4] = T(0); grB[k4] = T(0); }
+  for (int s = lane; s < TOT; s += kWave) gcol[s] = T(0);
+  if (tid == 0) s_abort = 0;
+  int nmoved = 0;                                  // entries in this wave's moved list
+  int qk = j;                                      // block-start index of the row at position k
+  // column j: S(pos, j) = A(pos, j), every held row is below j
+  T cv = T(0);
+  {
+    T lv = T(0);
+    if (my_row && part == 0) lv = A[(int64_t)pos + (int64_t)j * lda];
+    cv = part_sum<S>(lv);
+  }
+  __syncthreads();
+
+  for (int t = 0; t < nt; ++t) {
+    const int k = j + 2 * t;
+    const int ns = 2 * t;                          // slots filled so far
+    const bool last = t + 1 == nt;
+    const bool active = my_row && lp >= k + 1;
+
+    // ---- pivot of column k ----
+    {
+      double av = -1.0;
+      if (active) {
+        const double m = (double)fabs(cv);
+        if (m == m) av = m;
+      }
+      double bv;
+      int bi;
+      const int src = wave_first_max(av, active ? lp : INT32_MAX, bv, bi);
+      int wpos = 0, wsg = 0;
+      if (src >= 0) {
+        wpos = __builtin_amdgcn_readlane(pos, src);
+        wsg = __builtin_amdgcn_readlane(cv < T(0) ? 1 : 0, src);
+      }
+      if (lane == 0) {
+        red_v[wave] = src >= 0 ? bv : -1.0;
+        red_k[wave] = ((uint64_t)(uint32_t)bi << 32) | ((uint64_t)wpos << 1) | (uint64_t)wsg;
+      }
+    }
+    exchange_pivot<T>(a, k / 2 + 1, k, wave, lane, w, red_v, red_k, s_p, s_posw, s_alpha, s_abort);
+    if (s_abort) return;
+    const int p = s_p;
+    const int posw = s_posw;
+    const T alph = s_alpha;
+
+    // ---- exchange positions k+1 and p; track the displaced row ----
+    // moved list: the last entry with position x names the row at x; a
+    // position never listed holds the row of its own block-start index.
+    auto lookup = [&](int x) -> int {
+      int found = x;
+      for (int e0 = 0; e0 < nmoved; e0 += kWave) {
+        const int e = e0 + lane;
+        const bool hit = e < nmoved && moved_pos[e] == x;
+        const unsigned long long b = __ballot(hit);
+        if (b) found = __builtin_amdgcn_readlane(moved_idx[e0 + lane], 63 - __clzll(b));
+      }
+      return found;
+    };
+    if (p != k + 1) {
+      const int displaced = lookup(k + 1);         // row that was at position k+1
+      if (lane == 0) { moved_pos[nmoved] = p; moved_idx[nmoved] = displaced; }
+      ++nmoved;
+      wave_lds_sync();
+      if (my_row) {
+        if (lp == p) lp = k + 1;
+        else if (lp == k + 1) lp = p;
+      }
+    }
+    const int q = last ? 0 : lookup(k + 2);        // block-start index of the row at position k+2
+    const bool next2 = my_row && lp >= k + 2;      // rows that get l and w
+    const bool next3 = !last && my_row && lp >= k + 3;   // rows of the next column
+
+    // ---- one round of loads ----
+    T lvB = T(0), lsgB = T(1), lvA = T(0), lsgA = T(1);
+    if (next2 && part == 0) {
+      lvB = A[(int64_t)max(pos, posw) + (int64_t)min(pos, posw) * lda];
+      lsgB = pos > posw ? T(1) : T(-1);
+    }
+    if (next3 && part == 0) {
+      lvA = A[(int64_t)max(pos, q) + (int64_t)min(pos, q) * lda];
+      lsgA = pos > q ? T(1) : T(-1);
+    }
+    T lrB[NLQ], lrQ[NLQ];
+    {
+      const int umax = ns > 0 ? ns - 1 : 0;
+      const T* growB = G + (int64_t)(posw - (j + 1));
+#pragma unroll
+      for (int qq = 0; qq < NLQ; ++qq) lrB[qq] = ld_coh_t(&growB[(int64_t)min(qq * kWave + lane, umax) * ldw]);
+      const T* growQ = G + (int64_t)((last ? posw : q) - (j + 1));
+#pragma unroll
+      for (int qq = 0; qq < NLQ; ++qq) lrQ[qq] = ld_coh_t(&growQ[(int64_t)min(qq * kWave + lane, umax) * ldw]);
+    }
+    T sA = T(0), sB = T(0);                        // S(q, q_k), S(q, posw)
+    if (!last) {
+      sA = A[(int64_t)max(q, qk) + (int64_t)min(q, qk) * lda];
+      if (q < qk) sA = -sA;
+      sB = A[(int64_t)max(q, posw) + (int64_t)min(q, posw) * lda];
+      if (q < posw) sB = -sB;
+    }
+
+    // ---- multiplier of column k into slot 2t ----
+    T l = T(0);
+    if (next2) l = (alph != T(0)) ? cv / alph : T(0);
+    {
+      const int c = ns / S;
+      const bool on = next2 && part == ns % S;
+      const T v = l;
+      LTLT_SET_GROUP(0) LTLT_SET_GROUP(16) LTLT_SET_GROUP(32) LTLT_SET_GROUP(48)
+    }
+
+    // ---- slots of the pivot row and of row q into LDS ----
+#pragma unroll
+    for (int qq = 0; qq < NLQ; ++qq) {
+      const int s = qq * kWave + lane;
+      if (s < ns) { bufB[s] = lrB[qq]; bufQ[s] = lrQ[qq]; }
+    }
+    wave_lds_sync();
+
+    // ---- the two newest slots of row q, and the g of column k+2 ----
+    T gq0 = T(0), gq1 = T(0);                      // g_{2t} = w_t(q), g_{2t+1} = -l_t(q)
+    if (!last) {
+      T dA = T(0), dB = T(0);
+#pragma unroll
+      for (int qq = 0; qq < NLQ; ++qq) {
+        const int s = qq * kWave + lane;
+        if (s < ns) {
+          dA = fma(bufQ[s], gcol[s], dA);
+          dB = fma(bufQ[s], g_of(bufB, s, ns), dB);
+        }
+      }
+      const T cA = sA + wave_sum(dA);              // column k at row q
+      const T cB = sB + wave_sum(dB);              // column k+1 at row q
+      const T lq = (alph != T(0)) ? cA / alph : T(0);
+      gq0 = cB;
+      gq1 = -lq;
+    }
+    // g registers (row broadcast layout): grB from the pivot row, grA from
+    // row q, both over the slots filled before this step
+    {
+      const int c16 = lane & 15;
+#pragma unroll
+      for (int kk = 0; kk < NG; ++kk) {
+        const int s = (16 * kk + c16) * S + part;
+        grB[kk] = g_of(bufB, s, ns);
+        grA[kk] = last ? T(0) : g_of(bufQ, s, ns);
+      }
+    }
+    // g of column k+2 by slot, for the next step's dot products
+    if (!last) {
+      wave_lds_sync();                             // gcol reads above are done
+#pragma unroll
+      for (int qq = 0; qq < NLQ; ++qq) {
+        const int s = qq * kWave + lane;
+        const T gv = s < ns ? g_of(bufQ, s, ns) : (s == ns ? gq0 : (s == ns + 1 ? gq1 : T(0)));
+        gcol[s] = gv;
+      }
+    }
+
+    // ---- one pass over the slots: column k+1 (w) and column k+2 ----
+    {
+      T accB[4] = {T(0), T(0), T(0), T(0)};
+      T accA[4] = {T(0), T(0), T(0), T(0)};
+      if (0 * 16 * S < ns) { refresh16<0>(accB, grB[0], L); refresh16<0>(accA, grA[0], L); }
+      if (1 * 16 * S < ns) { refresh16<1>(accB, grB[1], L); refresh16<1>(accA, grA[1], L); }
+      if (2 * 16 * S < ns) { refresh16<2>(accB, grB[2], L); refresh16<2>(accA, grA[2], L); }
+      if (3 * 16 * S < ns) { refresh16<3>(accB, grB[3], L); refresh16<3>(accA, grA[3], L); }
+      const T wsum = part_sum<S>(fma(lsgB, lvB, (accB[0] + accB[1]) + (accB[2] + accB[3])));
+      const T wv = next2 ? wsum : T(0);
+      const T asum = part_sum<S>(fma(lsgA, lvA, (accA[0] + accA[1]) + (accA[2] + accA[3])));
+      cv = next3 ? fma(wv, gq1, fma(l, gq0, asum)) : T(0);
+      // w into slot 2t+1
+      {
+        const int c = (ns + 1) / S;
+        const bool on = next2 && part == (ns + 1) % S;
+        const T v = wv;
+        LTLT_SET_GROUP(0) LTLT_SET_GROUP(16) LTLT_SET_GROUP(32) LTLT_SET_GROUP(48)
+      }
+      // both new slots to G (read by other waves as a pivot row or row q)
+      int ro = pos - (j + 1);
+      asm volatile("" : "+v"(ro));
+      if (next2 && part == ns % S) st_coh_t(&G[(int64_t)ro + (int64_t)ns * ldw], l);
+      if (next2 && part == (ns + 1) % S) st_coh_t(&G[(int64_t)ro + (int64_t)(ns + 1) * ldw], wv);
+    }
+    if (tid == 0 && w == 0) {
+      a.ipiv[k + 1] = p;
+      static_cast<T*>(a.alpha)[t] = alph;
+    }
+    qk = q;
+    wave_lds_sync();
+  }
+
+#undef LTLT_SET_GROUP
+
+  // ---- outputs for the trailing rows (positions >= j+bw): Lx in slot order,
+  //      Bt = Lx J^T (column s+1 = -slot s for even s, column s-1 = slot s
+  //      for odd s) ----
+  T* PO = static_cast<T*>(a.PO);
+  T* Bm = static_cast<T*>(a.Bm);
+  const int tr0 = j + bw;
+  if (my_row && lp >= tr0) {
+    const int64_t ro = lp - tr0;
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
+      const int s = c * S + part;
+      if (s < bw) {
+        PO[ro + (int64_t)s * ldw] = L[c];
+        if (s & 1) Bm[ro + (int64_t)(s - 1) * ldw] = L[c];
+        else Bm[ro + (int64_t)(s + 1) * ldw] = -L[c];
+      }
+    }
+  }
+  if (my_row && part == 0) a.perm[lp] = pos;
+}
+
+template <typename T, int S>
+hipError_t launch_pair_panel_s(const PanelArgs& a, size_t lds, hipStream_t st) {
+  PanelArgs copy = a;
+  void* args[] = {&copy};
+  return hipLaunchCooperativeKernel((const void*)pair_panel_kernel<T, S>, dim3(a.P), dim3(kPanelThreads), args,
+                                    (unsigned)lds, st);
+}
+
+template <typename T>
+hipError_t launch_pair_panel(const PanelArgs& a, size_t lds, hipStream_t st) {
+  if (a.P > kMaxPanelRecords || a.P > a.nrec || a.R != kPanelThreads / panel_split(a.bw) || (a.bw & 1))
+    return hipErrorInvalidValue;
+  switch (panel_split(a.bw)) {
+    case 1: return launch_pair_panel_s<T, 1>(a, lds, st);
+    case 2: return launch_pair_panel_s<T, 2>(a, lds, st);
+    case 4: return launch_pair_panel_s<T, 4>(a, lds, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <typename T, int S>
+int pair_max_blocks_s(size_t lds) {
+  int dev = 0, per_cu = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)pair_panel_kernel<T, S>, kPanelThreads,
+                                                   lds) != hipSuccess)
+    return 0;
+  return per_cu * cus;
+}
+
+template <typename T>
+int pair_max_blocks(int bw, size_t lds) {
+  int cap;
+  switch (panel_split(bw)) {
+    case 1: cap = pair_max_blocks_s<T, 1>(lds); break;
+    case 2: cap = pair_max_blocks_s<T, 2>(lds); break;
+    case 4: cap = pair_max_blocks_s<T, 4>(lds); break;
+    default: return 0;
+  }
+  return cap < kMaxPanelRecords ? cap : kMaxPanelRecords;
+}
+
+// alpha_k of the block's steps into A(k+1, k) (after the block's trailing
+// update, which may still read the block's original entries).
+template <typename T>
+__global__ void pair_commit_kernel(T* A, int64_t lda, int j, int nt, const T* alpha) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < nt) A[(int64_t)(j + 2 * t + 1) + (int64_t)(j + 2 * t) * lda] = alpha[t];
+}
+
+template <typename T>
+hipError_t launch_pair_commit(T* A, int64_t lda, int j, int nt, const T* alpha, hipStream_t s) {
+  if (nt <= 0) return hipSuccess;
+  hipLaunchKernelGGL(pair_commit_kernel<T>, dim3((nt + 255) / 256), dim3(256), 0, s, A, lda, j, nt, alpha);
+  return hipGetLastError();
+}
+
+template size_t pair_lds_bytes<double>(int, int);
+template size_t pair_lds_bytes<float>(int, int);
+template int pair_max_blocks<double>(int, size_t);
+template int pair_max_blocks<float>(int, size_t);
+template hipError_t launch_pair_panel<double>(const PanelArgs&, size_t, hipStream_t);
+template hipError_t launch_pair_panel<float>(const PanelArgs&, size_t, hipStream_t);
+template hipError_t launch_pair_commit<double>(double*, int64_t, int, int, const double*, hipStream_t);
+template hipError_t launch_pair_commit<float>(float*, int64_t, int, int, const float*, hipStream_t);
+
+}  // namespace ltlt

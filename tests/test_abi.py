@@ -31,7 +31,8 @@ def test_header_declares_the_entry_points():
     names = declared_functions()
     for must in ["ltlt_factor", "ltlt_factor_nb", "ltlt_pfaffian", "ltlt_factor_batched",
                  "ltlt_skew_update", "ltlt_device_status", "ltlt_profile_enable",
-                 "ltlt_profile_read", "ltlt_release_workspace", "ltlt_mfma_probe"]:
+                 "ltlt_profile_read", "ltlt_release_workspace", "ltlt_mfma_probe",
+                 "ltlt_pfaffian_direct"]:
         assert must in names
 
 
@@ -126,6 +127,22 @@ def test_mfma_probe_argument_checks(lib, args, code):
     dtype, iters, ptr = args
     out = ctypes.c_double(0.0)
     assert lib.ltlt_mfma_probe(dtype, iters, ctypes.addressof(out) if ptr else None, None) == code
+
+
+@pytest.mark.parametrize("args,code", [
+    ((-1, 1, 1, 0, 1, 0, 1, 1, NULL), -1),
+    ((4, NULL, 4, 0, 1, 0, 1, 1, NULL), -2),
+    ((4, 1, 3, 0, 1, 0, 1, 1, NULL), -3),
+    ((4, 1, 4, 5, 1, 0, 1, 1, NULL), -4),
+    ((4, 1, 4, 0, NULL, 0, 1, 1, NULL), -5),
+    ((4, 1, 4, 0, 1, 3, 1, 1, NULL), -6),       # odd nb
+    ((4, 1, 4, 0, 1, 258, 1, 1, NULL), -6),     # nb above the widest panel
+    ((4, 1, 4, 0, 1, -2, 1, 1, NULL), -6),
+    ((4, 1, 4, 0, 1, 0, NULL, 1, NULL), -7),
+    ((4, 1, 4, 0, 1, 0, 1, NULL, NULL), -8),
+])
+def test_pfaffian_direct_argument_checks(lib, args, code):
+    assert lib.ltlt_pfaffian_direct(*args) == code
 
 
 def test_error_messages():
