@@ -243,7 +243,7 @@ int pfaffian_direct_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, 
     return e == hipSuccess ? 0 : hip_err(e);
   }
   const int bw0 = std::min(nb, n);
-  const int R = panel_rows(bw0);
+  const int R = pair_panel_rows(bw0);
   if (pair_lds_bytes<T>(bw0, R) > kLdsBudget) return LTLT_ERR_UNSUPPORTED;
   const int Pmax = (n - 1 + R - 1) / R;
   const int cap = pair_max_blocks<T>(bw0, pair_lds_bytes<T>(bw0, R));
@@ -281,7 +281,7 @@ int pfaffian_direct_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, 
     const int m = n - j - 1;                     // rows at positions j+1 .. n-1
     PanelArgs pa{};
     pa.A = A; pa.lda = lda; pa.n = n; pa.j = j; pa.bw = bw;
-    pa.R = panel_rows(bw);
+    pa.R = pair_panel_rows(bw);
     pa.P = (m + pa.R - 1) / pa.R;
     pa.nrec = nrec;
     pa.G = Gm; pa.PO = PO; pa.Bm = Bm; pa.ldw = ldw; pa.alpha = al;

@@ -67,25 +67,25 @@ __device__ __forceinline__ T part_sum(T v) {
   return v;
 }
 
-// One grid-wide pivot agreement (called by every thread of the workgroup).
+// One grid-wide pivot agreement, in two halves called by every thread of the
+// workgroup (work that does not depend on the pivot may run in between).
 // Each wave has put its first-maximum candidate in red_v / red_k (lane 0:
-// |cv|, key = position << 32 | block-start index << 1 | sign).  Wave 0 merges
-// the waves, publishes the workgroup's record for stamp s, polls every
-// record until all carry stamp s, and reduces them (largest magnitude, then
-// smallest position); the result lands in s_p (pivot position), s_posw (its
-// block-start index) and s_alpha (signed pivot value; NaN and p = k+1 when
-// no finite candidate exists).  A wait that exceeds its bound sets the
-// status flag and s_abort.  Every wave first waits for its own earlier
-// stores, so a validated record implies they are visible.
-template <typename T>
-__device__ __forceinline__ void exchange_pivot(const PanelArgs& a, int s, int k, int wave, int lane, int w,
-                                               const double* red_v, const uint64_t* red_k, int& s_p,
-                                               int& s_posw, T& s_alpha, int& s_abort) {
-  const int P = a.P;
+// |cv|, key = position << 32 | block-start index << 1 | sign).
+// exchange_publish: every wave waits for its own earlier stores (so a
+// validated record implies they are visible), a barrier, then wave 0 merges
+// the waves and publishes the workgroup's record for stamp s.
+// exchange_collect: wave 0 polls every record until all carry stamp s and
+// reduces them (largest magnitude, then smallest position); the result lands
+// in s_p (pivot position), s_posw (its block-start index) and s_alpha
+// (signed pivot value; NaN and p = k+1 when no finite candidate exists),
+// handed to the other waves by a barrier.  A wait that exceeds its bound sets
+// the status flag and s_abort.
+__device__ __forceinline__ void exchange_publish(const PanelArgs& a, int s, int wave, int lane, int w,
+                                                 const double* red_v, const uint64_t* red_k) {
   uint64_t* recs = a.rec + (size_t)(s & 1) * (size_t)a.nrec * kRecStride;
   wait_stores();
   __syncthreads();
-  if (wave == 0) {                                // merge the waves, publish (lane 0)
+  if (wave == 0) {
     double cb = red_v[0];
     uint64_t ck = red_k[0];
 #pragma unroll
@@ -104,7 +104,14 @@ __device__ __forceinline__ void exchange_pivot(const PanelArgs& a, int s, int k,
                rec_b(s, (int)(ck & 1), (int)((ck >> 1) & kIdxNone), none ? kIdxNone : (uint64_t)ci));
     }
   }
-  if (wave == 0) {                                // poll every record and reduce
+}
+
+template <typename T>
+__device__ __forceinline__ void exchange_collect(const PanelArgs& a, int s, int k, int wave, int lane, int& s_p,
+                                                 int& s_posw, T& s_alpha, int& s_abort) {
+  const int P = a.P;
+  const uint64_t* recs = a.rec + (size_t)(s & 1) * (size_t)a.nrec * kRecStride;
+  if (wave == 0) {
     const int q_n = (P + kWave - 1) / kWave;
     const uint64_t t0 = wall_ticks();
     uint64_t ra[kPollPerLane], rb[kPollPerLane];
@@ -160,6 +167,15 @@ __device__ __forceinline__ void exchange_pivot(const PanelArgs& a, int s, int k,
     }
   }
   __syncthreads();
+}
+
+// Both halves back to back.
+template <typename T>
+__device__ __forceinline__ void exchange_pivot(const PanelArgs& a, int s, int k, int wave, int lane, int w,
+                                               const double* red_v, const uint64_t* red_k, int& s_p,
+                                               int& s_posw, T& s_alpha, int& s_abort) {
+  exchange_publish(a, s, wave, lane, w, red_v, red_k);
+  exchange_collect<T>(a, s, k, wave, lane, s_p, s_posw, s_alpha, s_abort);
 }
 
 }  // namespace ltlt

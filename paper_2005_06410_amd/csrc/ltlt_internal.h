@@ -72,6 +72,7 @@ int panel_rows(int bw);
 
 // Pfaffian-only path (even column steps): the pair panel and the commit of
 // its alphas.
+int pair_panel_rows(int bw);                     // rows per pair-panel workgroup
 template <typename T> size_t pair_lds_bytes(int bw, int R);
 template <typename T> int pair_max_blocks(int bw, size_t lds);
 template <typename T> hipError_t launch_pair_panel(const PanelArgs& a, size_t lds, hipStream_t s);

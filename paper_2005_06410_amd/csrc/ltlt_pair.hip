@@ -10,7 +10,10 @@
 // so half the grid-wide pivot agreements of the full reduction.
 //
 // Pair panel (one block of bw columns, bw/2 steps, rows at positions >= j+1),
-// same thread layout, register slots and exchange as the full panel.  Step u
+// the register slots and exchange of the full panel; wave 0 of each
+// workgroup holds no rows and only publishes and polls, so that the other
+// seven waves' work on the next column overlaps its round trip (R = 7*64/S
+// rows per workgroup).  Step u
 // leaves two slots in every row still in play: slot 2u = l_u (multiplier)
 // and slot 2u+1 = w_u (column k+1 below row k+1, refreshed: the v of the
 // rank-2 update).  The updates pending within the block are
@@ -28,6 +31,20 @@
 //      second agreement per step is needed;
 //   5. one pass over the slots forms w (column k+1, slot 2u+1) and the next
 //      column k+2.
+// Unlike the full reduction, whose next column is the pivot's own, the next
+// column here belongs to the row at position k+2, which is known before the
+// pivot is (it changes only when the pivot comes from position k+2).  Its
+// loads, its dot product with the g of column k and the pass over its slots
+// for column k+2 therefore run while wave 0 waits for the other workgroups'
+// records -- over the slots older than the previous step only: the previous
+// step's two slots of that row are guaranteed visible in G only once every
+// record of this step has arrived (each workgroup waits for its G stores
+// before publishing), so they are loaded with the pivot row's data and their
+// two terms added then (each row keeps its own newest l and w, and the g of
+// column k at those two slots, in registers).  After the agreement only the
+// pivot row's part remains (its slots, S(pos, posw), the g of column k+1,
+// one pass, two scalars); the speculative part is redone in the rare case
+// that the row at k+2 changed.
 // Outputs of the block for the trailing rows (positions >= j+bw): Lx = Lp in
 // slot order and Bt = Lp J^T (Bt column 2u = w_u, 2u+1 = -l_u), one rank-bw
 // product for the trailing update; alpha_k and the pivots.
@@ -38,12 +55,9 @@
 
 namespace ltlt {
 
-// LDS per wave (elements of T, then ints): the slots of the pivot row (TOT),
-// of row q (TOT), the g of the current column by slot (TOT), and the list of
-// positions that received a displaced row: (position, block-start index).
-__host__ __device__ constexpr int pair_wave_lds_bytes(int tot, int tsize) {
-  return 3 * tot * tsize + 2 * tot * 4;
-}
+// LDS per wave: the slots of the pivot row (TOT), of row q (TOT) and the g
+// of the current column by slot (TOT).
+__host__ __device__ constexpr int pair_wave_lds_bytes(int tot, int tsize) { return 3 * tot * tsize; }
 template <typename T>
 size_t pair_lds_bytes(int bw, int /*R*/) {
   return (size_t)kPanelWaves * pair_wave_lds_bytes(KC * panel_split(bw), (int)sizeof(T));
@@ -57,18 +71,42 @@ __device__ __forceinline__ T g_of(const T* buf, int s, int ns) {
   return (s & 1) ? -buf[s - 1] : buf[s + 1];
 }
 
-// Wave-wide sum (every lane gets it), fixed order.
+// Wave-wide sum in a fixed order (every lane gets it): DPP row shifts give
+// each 16-lane row's sum in its lane 15, row broadcasts carry rows 0-2 into
+// lane 63.  Lanes without a source add 0.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ double dpp_add_step(double v) {
+  const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), CTRL, ROW_MASK, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), CTRL, ROW_MASK, 0xF, false);
+  return v + __hiloint2double(hi, lo);
+}
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_add_step(float v) {
+  return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, 0xF, false));
+}
 template <typename T>
 __device__ __forceinline__ T wave_sum(T v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
-  return v;
+  v = dpp_add_step<0x111, 0xF>(v);   // row_shr:1
+  v = dpp_add_step<0x112, 0xF>(v);   // row_shr:2
+  v = dpp_add_step<0x114, 0xF>(v);   // row_shr:4
+  v = dpp_add_step<0x118, 0xF>(v);   // row_shr:8  -> lane 15 of each row: the row's sum
+  v = dpp_add_step<0x142, 0xA>(v);   // row_bcast:15 into rows 1 and 3
+  v = dpp_add_step<0x143, 0xC>(v);   // row_bcast:31 into rows 2 and 3 -> lane 63: the total
+  if constexpr (sizeof(T) == 8) {
+    const int lo = __builtin_amdgcn_readlane(__double2loint(v), 63);
+    const int hi = __builtin_amdgcn_readlane(__double2hiint(v), 63);
+    return __hiloint2double(hi, lo);
+  } else {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+  }
 }
+
+int pair_panel_rows(int bw) { return (kPanelWaves - 1) * (kWave / panel_split(bw)); }
 
 template <typename T, int S>
 __global__ void __launch_bounds__(kPanelThreads, 1) pair_panel_kernel(PanelArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
-  constexpr int R = kPanelThreads / S;
+  constexpr int R = (kPanelWaves - 1) * (kWave / S);
   constexpr int RW = kWave / S;                    // rows per wave
   constexpr int NG = KC / 16;                      // g registers
   constexpr int TOT = KC * S;                      // slots a row can hold
@@ -76,12 +114,13 @@ __global__ void __launch_bounds__(kPanelThreads, 1) pair_panel_kernel(PanelArgs 
   static_assert(NG == 4, "four g registers");
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
-  const int wave = tid / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const bool rowwave = wave != 0;                  // wave 0: exchange only
   const int w = blockIdx.x;
   const int bw = a.bw, n = a.n, j = a.j;
   const int nt = bw / 2;                           // steps of this block
   const int part = lane / RW;
-  const int rloc = wave * RW + lane % RW;
+  const int rloc = (wave - 1) * RW + lane % RW;
   const int64_t lda = a.lda, ldw = a.ldw;
   const T* A = static_cast<const T*>(a.A);
   T* G = static_cast<T*>(a.G);
@@ -90,8 +129,6 @@ __global__ void __launch_bounds__(kPanelThreads, 1) pair_panel_kernel(PanelArgs 
   T* bufB = reinterpret_cast<T*>(wl);              // slots of the pivot row
   T* bufQ = bufB + TOT;                            // slots of row q
   T* gcol = bufQ + TOT;                            // g of the current column, by slot
-  int* moved_pos = reinterpret_cast<int*>(gcol + TOT);
-  int* moved_idx = moved_pos + TOT;
   __shared__ int s_p, s_posw, s_abort;
   __shared__ double red_v[kPanelWaves];
   __shared__ uint64_t red_k[kPanelWaves];
@@ -99,19 +136,30 @@ __global__ void __launch_bounds__(kPanelThreads, 1) pair_panel_kernel(PanelArgs 
 
   const int row0 = j + 1 + w * R;
   const int rows_here = max(0, min(R, n - row0));
-  const bool my_row = rloc < rows_here;
+  const bool my_row = rowwave && rloc < rows_here;
   const int pos = row0 + rloc;
   int lp = pos;
 
-  T L[KC], grA[NG], grB[NG];
+  T L[KC];
 #pragma unroll
   for (int c = 0; c < KC; ++c) L[c] = T(0);
-#pragma unroll
-  for (int k4 = 0; k4 < NG; ++k4) { grA[k4] = T(0); grB[k4] = T(0); }
   for (int s = lane; s < TOT; s += kWave) gcol[s] = T(0);
   if (tid == 0) s_abort = 0;
-  int nmoved = 0;                                  // entries in this wave's moved list
+  // Positions that received a displaced row, in registers: entry e (lane e,
+  // or lane e-64 of the second pair) = (position, block-start index).  The
+  // last entry with position x names the row at x; a position never listed
+  // holds the row of its own block-start index.  At most nt <= 128 entries.
+  int mpos0 = -1, midx0 = 0, mpos1 = -1, midx1 = 0, nmoved = 0;
+  auto lookup = [&](int x) -> int {
+    const unsigned long long b1 = __ballot(lane + kWave < nmoved && mpos1 == x);
+    const unsigned long long b0 = __ballot(lane < nmoved && mpos0 == x);
+    if (b1) return __builtin_amdgcn_readlane(midx1, 63 - __clzll(b1));
+    if (b0) return __builtin_amdgcn_readlane(midx0, 63 - __clzll(b0));
+    return x;
+  };
   int qk = j;                                      // block-start index of the row at position k
+  T l_prev = T(0), w_prev = T(0);                  // this row's slots 2t-2, 2t-1
+  T gc0 = T(0), gc1 = T(0);                        // g of column k at slots 2t-2, 2t-1
   // column j: S(pos, j) = A(pos, j), every held row is below j
   T cv = T(0);
   {
@@ -124,10 +172,11 @@ __global__ void __launch_bounds__(kPanelThreads, 1) pair_panel_kernel(PanelArgs 
   for (int t = 0; t < nt; ++t) {
     const int k = j + 2 * t;
     const int ns = 2 * t;                          // slots filled so far
+    const int umax = ns > 0 ? ns - 1 : 0;
     const bool last = t + 1 == nt;
     const bool active = my_row && lp >= k + 1;
 
-    // ---- pivot of column k ----
+    // ---- pivot candidate of column k ----
     {
       double av = -1.0;
       if (active) {
@@ -147,69 +196,107 @@ __global__ void __launch_bounds__(kPanelThreads, 1) pair_panel_kernel(PanelArgs 
         red_k[wave] = ((uint64_t)(uint32_t)bi << 32) | ((uint64_t)wpos << 1) | (uint64_t)wsg;
       }
     }
-    exchange_pivot<T>(a, k / 2 + 1, k, wave, lane, w, red_v, red_k, s_p, s_posw, s_alpha, s_abort);
+    const int stamp = k / 2 + 1;
+    exchange_publish(a, stamp, wave, lane, w, red_v, red_k);
+
+    // ---- column k+2 for the row qq at position k+2 (independent of the
+    //      pivot unless it comes from k+2): its slots, S(pos, qq), cA = column
+    //      k at row qq, and asum = S(pos, qq) + the old slots' part of the
+    //      refresh, for every row now at a position >= k+1 ----
+    const int no = ns >= 2 ? ns - 2 : 0;           // slots visible before the agreement
+    const int uo = no > 0 ? no - 1 : 0;
+    T apart = T(0), cA = T(0);
+    auto spec = [&](int qq) {
+      T lvA = T(0), lsgA = T(1);
+      if (my_row && part == 0 && lp >= k + 1 && pos != qq) {
+        lvA = A[(int64_t)max(pos, qq) + (int64_t)min(pos, qq) * lda];
+        lsgA = pos > qq ? T(1) : T(-1);
+      }
+      T lrQ[NLQ];
+      const T* growQ = G + (int64_t)(qq - (j + 1));
+#pragma unroll
+      for (int u = 0; u < NLQ; ++u) lrQ[u] = ld_coh_t(&growQ[(int64_t)min(u * kWave + lane, uo) * ldw]);
+      T sA = A[(int64_t)max(qq, qk) + (int64_t)min(qq, qk) * lda];
+      if (qq < qk) sA = -sA;
+#pragma unroll
+      for (int u = 0; u < NLQ; ++u) {
+        const int s = u * kWave + lane;
+        if (s < no) bufQ[s] = lrQ[u];
+      }
+      wave_lds_sync();
+      T dA = T(0);
+#pragma unroll
+      for (int u = 0; u < NLQ; ++u) {
+        const int s = u * kWave + lane;
+        if (s < no) dA = fma(bufQ[s], gcol[s], dA);
+      }
+      cA = sA + wave_sum(dA);
+      T grA[NG];
+      const int c16 = lane & 15;
+#pragma unroll
+      for (int kk = 0; kk < NG; ++kk) grA[kk] = g_of(bufQ, (16 * kk + c16) * S + part, no);
+      T accA[4] = {T(0), T(0), T(0), T(0)};
+      if (0 * 16 * S < no) refresh16<0>(accA, grA[0], L);
+      if (1 * 16 * S < no) refresh16<1>(accA, grA[1], L);
+      if (2 * 16 * S < no) refresh16<2>(accA, grA[2], L);
+      if (3 * 16 * S < no) refresh16<3>(accA, grA[3], L);
+      apart = fma(lsgA, lvA, (accA[0] + accA[1]) + (accA[2] + accA[3]));
+    };
+    const int qs = last ? 0 : lookup(k + 2);       // row at position k+2 before the exchange
+    const int displaced = lookup(k + 1);           // row at position k+1 before the exchange
+    if (!last && rowwave) spec(qs);
+
+    exchange_collect<T>(a, stamp, k, wave, lane, s_p, s_posw, s_alpha, s_abort);
     if (s_abort) return;
     const int p = s_p;
     const int posw = s_posw;
     const T alph = s_alpha;
+    // the row at position k+2 after the exchange: the displaced row when the
+    // pivot came from k+2, else the same as before
+    const int q = last ? 0 : (p == k + 2 ? displaced : qs);
 
-    // ---- exchange positions k+1 and p; track the displaced row ----
-    // moved list: the last entry with position x names the row at x; a
-    // position never listed holds the row of its own block-start index.
-    auto lookup = [&](int x) -> int {
-      int found = x;
-      for (int e0 = 0; e0 < nmoved; e0 += kWave) {
-        const int e = e0 + lane;
-        const bool hit = e < nmoved && moved_pos[e] == x;
-        const unsigned long long b = __ballot(hit);
-        if (b) found = __builtin_amdgcn_readlane(moved_idx[e0 + lane], 63 - __clzll(b));
+    // ---- the pivot row's part, issued first: S(pos, posw) for every row at
+    //      a position >= k+1 but the pivot (a superset of the rows that get a
+    //      w), its slots, S(q, posw) and row q's slots 2t-2, 2t-1 ----
+    T lvB = T(0), lsgB = T(1);
+    T lrB[NLQ];
+    T sB = T(0), qn0 = T(0), qn1 = T(0);
+    if (rowwave) {
+      if (my_row && part == 0 && lp >= k + 1 && pos != posw) {
+        lvB = A[(int64_t)max(pos, posw) + (int64_t)min(pos, posw) * lda];
+        lsgB = pos > posw ? T(1) : T(-1);
       }
-      return found;
-    };
+      const T* growB = G + (int64_t)(posw - (j + 1));
+#pragma unroll
+      for (int u = 0; u < NLQ; ++u) lrB[u] = ld_coh_t(&growB[(int64_t)min(u * kWave + lane, umax) * ldw]);
+      if (!last) {
+        sB = A[(int64_t)max(q, posw) + (int64_t)min(q, posw) * lda];
+        if (q < posw) sB = -sB;
+        if (ns >= 2) {
+          const T* growQ = G + (int64_t)(q - (j + 1));
+          qn0 = ld_coh_t(&growQ[(int64_t)(ns - 2) * ldw]);
+          qn1 = ld_coh_t(&growQ[(int64_t)(ns - 1) * ldw]);
+        }
+      }
+    }
+
+    // ---- exchange positions k+1 and p ----
     if (p != k + 1) {
-      const int displaced = lookup(k + 1);         // row that was at position k+1
-      if (lane == 0) { moved_pos[nmoved] = p; moved_idx[nmoved] = displaced; }
+      if (lane == nmoved) { mpos0 = p; midx0 = displaced; }
+      if (lane + kWave == nmoved) { mpos1 = p; midx1 = displaced; }
       ++nmoved;
-      wave_lds_sync();
       if (my_row) {
         if (lp == p) lp = k + 1;
         else if (lp == k + 1) lp = p;
       }
     }
-    const int q = last ? 0 : lookup(k + 2);        // block-start index of the row at position k+2
+    if (!last && q != qs && rowwave) spec(q);      // the pivot came from position k+2
     const bool next2 = my_row && lp >= k + 2;      // rows that get l and w
     const bool next3 = !last && my_row && lp >= k + 3;   // rows of the next column
 
-    // ---- one round of loads ----
-    T lvB = T(0), lsgB = T(1), lvA = T(0), lsgA = T(1);
-    if (next2 && part == 0) {
-      lvB = A[(int64_t)max(pos, posw) + (int64_t)min(pos, posw) * lda];
-      lsgB = pos > posw ? T(1) : T(-1);
-    }
-    if (next3 && part == 0) {
-      lvA = A[(int64_t)max(pos, q) + (int64_t)min(pos, q) * lda];
-      lsgA = pos > q ? T(1) : T(-1);
-    }
-    T lrB[NLQ], lrQ[NLQ];
-    {
-      const int umax = ns > 0 ? ns - 1 : 0;
-      const T* growB = G + (int64_t)(posw - (j + 1));
-#pragma unroll
-      for (int qq = 0; qq < NLQ; ++qq) lrB[qq] = ld_coh_t(&growB[(int64_t)min(qq * kWave + lane, umax) * ldw]);
-      const T* growQ = G + (int64_t)((last ? posw : q) - (j + 1));
-#pragma unroll
-      for (int qq = 0; qq < NLQ; ++qq) lrQ[qq] = ld_coh_t(&growQ[(int64_t)min(qq * kWave + lane, umax) * ldw]);
-    }
-    T sA = T(0), sB = T(0);                        // S(q, q_k), S(q, posw)
-    if (!last) {
-      sA = A[(int64_t)max(q, qk) + (int64_t)min(q, qk) * lda];
-      if (q < qk) sA = -sA;
-      sB = A[(int64_t)max(q, posw) + (int64_t)min(q, posw) * lda];
-      if (q < posw) sB = -sB;
-    }
-
+    T l = T(0), wv_keep = T(0), gq0 = T(0), gq1 = T(0);
+    if (rowwave) {
     // ---- multiplier of column k into slot 2t ----
-    T l = T(0);
     if (next2) l = (alph != T(0)) ? cv / alph : T(0);
     {
       const int c = ns / S;
@@ -217,84 +304,77 @@ __global__ void __launch_bounds__(kPanelThreads, 1) pair_panel_kernel(PanelArgs 
       const T v = l;
       LTLT_SET_GROUP(0) LTLT_SET_GROUP(16) LTLT_SET_GROUP(32) LTLT_SET_GROUP(48)
     }
-
-    // ---- slots of the pivot row and of row q into LDS ----
 #pragma unroll
-    for (int qq = 0; qq < NLQ; ++qq) {
-      const int s = qq * kWave + lane;
-      if (s < ns) { bufB[s] = lrB[qq]; bufQ[s] = lrQ[qq]; }
+    for (int u = 0; u < NLQ; ++u) {
+      const int s = u * kWave + lane;
+      if (s < ns) bufB[s] = lrB[u];
     }
+    if (!last && ns >= 2 && lane == 0) { bufQ[ns - 2] = qn0; bufQ[ns - 1] = qn1; }
     wave_lds_sync();
-
-    // ---- the two newest slots of row q, and the g of column k+2 ----
-    T gq0 = T(0), gq1 = T(0);                      // g_{2t} = w_t(q), g_{2t+1} = -l_t(q)
+    // the previous step's terms: column k at row q (cA) and column k+2 (asum)
+    T asum = T(0);
     if (!last) {
-      T dA = T(0), dB = T(0);
-#pragma unroll
-      for (int qq = 0; qq < NLQ; ++qq) {
-        const int s = qq * kWave + lane;
-        if (s < ns) {
-          dA = fma(bufQ[s], gcol[s], dA);
-          dB = fma(bufQ[s], g_of(bufB, s, ns), dB);
-        }
-      }
-      const T cA = sA + wave_sum(dA);              // column k at row q
-      const T cB = sB + wave_sum(dB);              // column k+1 at row q
-      const T lq = (alph != T(0)) ? cA / alph : T(0);
-      gq0 = cB;
-      gq1 = -lq;
+      cA = fma(qn1, gc1, fma(qn0, gc0, cA));
+      asum = fma(w_prev, -qn0, fma(l_prev, qn1, part_sum<S>(apart)));
     }
-    // g registers (row broadcast layout): grB from the pivot row, grA from
-    // row q, both over the slots filled before this step
+
+    // ---- g of column k+1 (registers), the newest slots of row q ----
+    T grB[NG];
     {
       const int c16 = lane & 15;
 #pragma unroll
-      for (int kk = 0; kk < NG; ++kk) {
-        const int s = (16 * kk + c16) * S + part;
-        grB[kk] = g_of(bufB, s, ns);
-        grA[kk] = last ? T(0) : g_of(bufQ, s, ns);
-      }
+      for (int kk = 0; kk < NG; ++kk) grB[kk] = g_of(bufB, (16 * kk + c16) * S + part, ns);
     }
-    // g of column k+2 by slot, for the next step's dot products
     if (!last) {
-      wave_lds_sync();                             // gcol reads above are done
+      T dB = T(0);
 #pragma unroll
-      for (int qq = 0; qq < NLQ; ++qq) {
-        const int s = qq * kWave + lane;
-        const T gv = s < ns ? g_of(bufQ, s, ns) : (s == ns ? gq0 : (s == ns + 1 ? gq1 : T(0)));
-        gcol[s] = gv;
+      for (int u = 0; u < NLQ; ++u) {
+        const int s = u * kWave + lane;
+        if (s < ns) dB = fma(bufQ[s], g_of(bufB, s, ns), dB);
       }
+      gq0 = sB + wave_sum(dB);                     // column k+1 at row q
+      gq1 = -((alph != T(0)) ? cA / alph : T(0));  // -(column k at row q) / alpha_k
     }
 
-    // ---- one pass over the slots: column k+1 (w) and column k+2 ----
+    // ---- column k+1 (w, slot 2t+1) and column k+2 ----
     {
       T accB[4] = {T(0), T(0), T(0), T(0)};
-      T accA[4] = {T(0), T(0), T(0), T(0)};
-      if (0 * 16 * S < ns) { refresh16<0>(accB, grB[0], L); refresh16<0>(accA, grA[0], L); }
-      if (1 * 16 * S < ns) { refresh16<1>(accB, grB[1], L); refresh16<1>(accA, grA[1], L); }
-      if (2 * 16 * S < ns) { refresh16<2>(accB, grB[2], L); refresh16<2>(accA, grA[2], L); }
-      if (3 * 16 * S < ns) { refresh16<3>(accB, grB[3], L); refresh16<3>(accA, grA[3], L); }
+      if (0 * 16 * S < ns) refresh16<0>(accB, grB[0], L);
+      if (1 * 16 * S < ns) refresh16<1>(accB, grB[1], L);
+      if (2 * 16 * S < ns) refresh16<2>(accB, grB[2], L);
+      if (3 * 16 * S < ns) refresh16<3>(accB, grB[3], L);
       const T wsum = part_sum<S>(fma(lsgB, lvB, (accB[0] + accB[1]) + (accB[2] + accB[3])));
       const T wv = next2 ? wsum : T(0);
-      const T asum = part_sum<S>(fma(lsgA, lvA, (accA[0] + accA[1]) + (accA[2] + accA[3])));
+      wv_keep = wv;
       cv = next3 ? fma(wv, gq1, fma(l, gq0, asum)) : T(0);
-      // w into slot 2t+1
       {
         const int c = (ns + 1) / S;
         const bool on = next2 && part == (ns + 1) % S;
         const T v = wv;
         LTLT_SET_GROUP(0) LTLT_SET_GROUP(16) LTLT_SET_GROUP(32) LTLT_SET_GROUP(48)
       }
-      // both new slots to G (read by other waves as a pivot row or row q)
       int ro = pos - (j + 1);
       asm volatile("" : "+v"(ro));
       if (next2 && part == ns % S) st_coh_t(&G[(int64_t)ro + (int64_t)ns * ldw], l);
       if (next2 && part == (ns + 1) % S) st_coh_t(&G[(int64_t)ro + (int64_t)(ns + 1) * ldw], wv);
     }
+    // g of column k+2 by slot, for the next step's cA
+    if (!last) {
+#pragma unroll
+      for (int u = 0; u < NLQ; ++u) {
+        const int s = u * kWave + lane;
+        gcol[s] = s < ns ? g_of(bufQ, s, ns) : (s == ns ? gq0 : (s == ns + 1 ? gq1 : T(0)));
+      }
+    }
+    }
     if (tid == 0 && w == 0) {
       a.ipiv[k + 1] = p;
       static_cast<T*>(a.alpha)[t] = alph;
     }
+    l_prev = l;
+    w_prev = next2 ? wv_keep : T(0);
+    gc0 = gq0;
+    gc1 = gq1;
     qk = q;
     wave_lds_sync();
   }
@@ -332,7 +412,7 @@ hipError_t launch_pair_panel_s(const PanelArgs& a, size_t lds, hipStream_t st) {
 
 template <typename T>
 hipError_t launch_pair_panel(const PanelArgs& a, size_t lds, hipStream_t st) {
-  if (a.P > kMaxPanelRecords || a.P > a.nrec || a.R != kPanelThreads / panel_split(a.bw) || (a.bw & 1))
+  if (a.P > kMaxPanelRecords || a.P > a.nrec || a.R != pair_panel_rows(a.bw) || (a.bw & 1))
     return hipErrorInvalidValue;
   switch (panel_split(a.bw)) {
     case 1: return launch_pair_panel_s<T, 1>(a, lds, st);
