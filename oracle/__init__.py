@@ -77,7 +77,7 @@ def _load():
                 getattr(lib, name).argtypes = [i64, p, i64, p, p, p]
                 getattr(lib, name).restype = None
             for name in ("oracle_pfaffian_direct_f64", "oracle_pfaffian_direct_f32"):
-                getattr(lib, name).argtypes = [i64, p, i64, p]
+                getattr(lib, name).argtypes = [i64, p, i64, p, i64]
                 getattr(lib, name).restype = None
             for name in ("oracle_ltlt_batched_f64", "oracle_ltlt_batched_f32"):
                 getattr(lib, name).argtypes = [i64, i64, p, i64, i64, p, i64, p, p]
@@ -151,16 +151,26 @@ def pfaffian_direct(X: np.ndarray):
     Returns ``(logabs, sign, alpha, ipiv)``: alpha[i] = alpha_{2i} of the even
     steps (n/2 values), ipiv the 0-based pivots with ipiv[k+1] = p_k for even
     k and ipiv[i] = i elsewhere.  Odd n gives (-inf, 0, [], identity)."""
-    lib = _load()
     n = X.shape[0]
     buf = np.ascontiguousarray(X.T)          # column-major image of X
-    ipiv = np.zeros(max(n, 1), dtype=np.int32)
-    getattr(lib, "oracle_pfaffian_direct_" + _sfx(buf.dtype))(n, buf.ctypes.data, n, ipiv.ctypes.data)
-    ipiv = ipiv[:n]
+    ipiv = pfaffian_direct_colmajor(buf, n)
     out = np.tril(buf.T, -1)
     alpha = np.array([out[k + 1, k] for k in range(0, n - 1, 2)] if n % 2 == 0 else [], dtype=buf.dtype)
     logabs, sign = pfaffian_packed(np.ascontiguousarray(out), ipiv)
     return logabs, sign, alpha, ipiv
+
+
+def pfaffian_direct_colmajor(buf: np.ndarray, n: int, nsteps: int = -1):
+    """The even column steps in place on a C-ordered (n, lda) array holding
+    the column-major matrix (as ``ltlt_colmajor``); ``nsteps >= 0`` stops
+    after that many even steps.  Returns the int32 pivot vector."""
+    lib = _load()
+    if not (buf.flags.c_contiguous and buf.ndim == 2 and buf.shape[0] >= n):
+        raise ValueError("buf must be a C-contiguous (n, lda) array")
+    ipiv = np.zeros(max(n, 1), dtype=np.int32)
+    getattr(lib, "oracle_pfaffian_direct_" + _sfx(buf.dtype))(n, buf.ctypes.data, buf.shape[1], ipiv.ctypes.data,
+                                                               int(nsteps))
+    return ipiv[:n]
 
 
 def ltlt_batched(Xs: np.ndarray):

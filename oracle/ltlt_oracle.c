@@ -53,11 +53,11 @@ void oracle_pfaffian_f32(int64_t n, const float* A, int64_t lda, const int32_t* 
                          double* logabs, int32_t* sign)
 { pfaffian_f32(n, A, lda, ipiv, logabs, sign); }
 
-void oracle_pfaffian_direct_f64(int64_t n, double* A, int64_t lda, int32_t* ipiv)
-{ pfaffian_direct_f64(n, A, lda, ipiv); }
+void oracle_pfaffian_direct_f64(int64_t n, double* A, int64_t lda, int32_t* ipiv, int64_t nsteps)
+{ pfaffian_direct_f64(n, A, lda, ipiv, nsteps); }
 
-void oracle_pfaffian_direct_f32(int64_t n, float* A, int64_t lda, int32_t* ipiv)
-{ pfaffian_direct_f32(n, A, lda, ipiv); }
+void oracle_pfaffian_direct_f32(int64_t n, float* A, int64_t lda, int32_t* ipiv, int64_t nsteps)
+{ pfaffian_direct_f32(n, A, lda, ipiv, nsteps); }
 
 /* Batched: `batch` matrices, matrix b at A + b*strideA, pivots at
  * ipiv + b*strideIpiv, one after the other. */

@@ -133,9 +133,9 @@ static void CAT(pfaffian, SFX)(int64_t n, const REAL* A, int64_t lda, const int3
  * values), ipiv[k+1] = p_k for even k and ipiv[i] = i otherwise; the
  * Pfaffian of the result is read by `pfaffian` above.  Odd n: no steps
  * (Pf = 0). */
-static void CAT(pfaffian_direct, SFX)(int64_t n, REAL* A, int64_t lda, int32_t* ipiv)
+static void CAT(pfaffian_direct, SFX)(int64_t n, REAL* A, int64_t lda, int32_t* ipiv, int64_t nsteps)
 {
-    int64_t i, j, k, r, p;
+    int64_t i, j, k, r, p, done;
     REAL best, alpha;
     REAL* v;
 
@@ -143,7 +143,8 @@ static void CAT(pfaffian_direct, SFX)(int64_t n, REAL* A, int64_t lda, int32_t* 
     if (n % 2 != 0 || n < 2) return;
     v = (REAL*)malloc((size_t)n * sizeof(REAL));
     if (!v) return;
-    for (k = 0; k + 1 < n; k += 2) {
+    /* nsteps >= 0 stops after that many even steps (a timing sample) */
+    for (k = 0, done = 0; k + 1 < n && (nsteps < 0 || done < nsteps); k += 2, ++done) {
         p = k + 1;
         best = FABS(AT(k + 1, k));
         for (r = k + 2; r < n; ++r) {
