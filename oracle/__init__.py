@@ -23,6 +23,10 @@ What it computes (textbook definitions, written out plainly):
   matrix product.
 * ``unpack`` -- reads L, the tridiagonal T and P back out of the packed
   output, for the residual P X P^T - L T L^T.
+* ``solve`` / ``tridiag_skew_solve`` -- X^{-1} B from the factors:
+  permutation, forward substitution with L, the two recurrences of the skew
+  tridiagonal T, backward substitution with L^T, inverse permutation
+  (triangular solves by scipy, the recurrences written out).
 
 Every floating-point routine runs in the precision of its input (fp64, or fp32
 for fp32 parity); the Pfaffian accumulates in fp64.
@@ -223,6 +227,50 @@ def unpack(packed: np.ndarray, ipiv: np.ndarray):
         j = int(ipiv[i])
         perm[i], perm[j] = perm[j], perm[i]
     return L, T, perm
+
+
+def tridiag_skew_solve(alpha: np.ndarray, R: np.ndarray) -> np.ndarray:
+    """Solve T W = R for the skew tridiagonal T with T[k+1, k] = alpha[k],
+    T[k, k+1] = -alpha[k] (n = len(alpha) + 1, n even), by its two
+    recurrences: row 0 gives W[1] = -R[0] / alpha[0] and the even rows i give
+    the odd unknowns forward, W[i+1] = (alpha[i-1] W[i-1] - R[i]) / alpha[i];
+    row n-1 gives W[n-2] = R[n-1] / alpha[n-2] and the odd rows i give the
+    even unknowns backward, W[i-1] = (R[i] + alpha[i] W[i+1]) / alpha[i-1].
+    R is (n,) or (n, nrhs); fp64."""
+    a = np.asarray(alpha, dtype=np.float64)
+    R = np.asarray(R, dtype=np.float64)
+    n = a.shape[0] + 1
+    if n % 2:
+        raise ValueError("a skew tridiagonal matrix of odd order is singular")
+    W = np.zeros_like(R)
+    W[1] = -R[0] / a[0]
+    for i in range(2, n - 1, 2):
+        W[i + 1] = (a[i - 1] * W[i - 1] - R[i]) / a[i]
+    W[n - 2] = R[n - 1] / a[n - 2]
+    for i in range(n - 3, 0, -2):
+        W[i - 1] = (R[i] + a[i] * W[i + 1]) / a[i - 1]
+    return W
+
+
+def solve(packed: np.ndarray, ipiv: np.ndarray, B: np.ndarray) -> np.ndarray:
+    """X^{-1} B from the factors (fp64).  With P X P^T = L T L^T (``unpack``),
+    X x = b is L T L^T (P x) = P b, so: y = P b (y[i] = b[perm[i]]),
+    z = L^{-1} y (unit lower, forward substitution), w = T^{-1} z (the two
+    recurrences of ``tridiag_skew_solve``), u = L^{-T} w (backward
+    substitution) and x = P^T u (x[perm[i]] = u[i]).  B is (n,) or
+    (n, nrhs); n must be even (odd order: X is singular)."""
+    from scipy.linalg import solve_triangular
+    n = packed.shape[0]
+    L, _, perm = unpack(np.asarray(packed, dtype=np.float64), ipiv)
+    alpha = np.array([packed[k + 1, k] for k in range(n - 1)], dtype=np.float64)
+    Bd = np.asarray(B, dtype=np.float64)
+    y = Bd[perm]
+    z = solve_triangular(L, y, lower=True, unit_diagonal=True)
+    w = tridiag_skew_solve(alpha, z)
+    u = solve_triangular(L.T, w, lower=False, unit_diagonal=True)
+    x = np.empty_like(u)
+    x[perm] = u
+    return x
 
 
 def residual(X: np.ndarray, packed: np.ndarray, ipiv: np.ndarray) -> float:
