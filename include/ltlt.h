@@ -53,6 +53,7 @@ extern "C" {
 #define LTLT_ERR_HIP_BASE (-1000)      /* returned as LTLT_ERR_HIP_BASE - (int)hipError_t */
 #define LTLT_ERR_UNSUPPORTED (-2000)
 #define LTLT_ERR_DEVICE_TIMEOUT (-3000) /* a device-side wait exceeded its bound (see ltlt_device_status) */
+#define LTLT_ERR_SINGULAR (-4000)       /* ltlt_solve: odd order, X is singular */
 
 /* Largest n accepted by ltlt_factor_batched. */
 #define LTLT_BATCHED_MAX_N 64
@@ -125,6 +126,28 @@ int ltlt_pfaffian(int64_t n, const void* A, int64_t lda, int dtype, const int32_
  */
 int ltlt_pfaffian_direct(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, int64_t nb,
                          double* logabs, int32_t* sign, hipStream_t stream);
+
+/*
+ * ltlt_solve -- X x = b for each column b of B, from the output of
+ * ltlt_factor (packed A and ipiv).  With P X P^T = L T L^T:
+ *   x = P^T L^{-T} T^{-1} L^{-1} P b,
+ * a permutation, a forward substitution with the unit lower L (read from the
+ * packed columns: L(r, c) = A(r, c-1), r >= c+1; L(:,0) = e_0), the two
+ * recurrences of the skew tridiagonal T (T(k+1,k) = A(k+1,k)), a backward
+ * substitution with L^T and the inverse permutation (the paper does not
+ * treat solves; this is the factorization's defining identity).
+ *   n, A, lda, dtype, ipiv: as left by ltlt_factor (A and ipiv are read only).
+ *   nrhs: number of right-hand sides (>= 0).
+ *   B (device, dtype): n x nrhs column-major, leading dimension ldb >= n;
+ *       overwritten with the solutions.
+ * Returns 0; -i when argument i is invalid; LTLT_ERR_SINGULAR for odd n
+ * (a skew-symmetric matrix of odd order is singular); a runtime or
+ * device-wait error as ltlt_factor.  When some alpha_{2j} is 0 (Pf(X) = 0)
+ * the solutions are not finite.  Stream-ordered; uses the library's cached
+ * workspace.
+ */
+int ltlt_solve(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* ipiv, int64_t nrhs, void* B,
+               int64_t ldb, hipStream_t stream);
 
 /*
  * ltlt_factor_batched -- independent factorizations and Pfaffians of `batch`

@@ -63,6 +63,8 @@ _SYMBOLS = {
     "ltlt_mfma_probe": ([ctypes.c_int, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "ltlt_pfaffian_direct": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
                               ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
+    "ltlt_solve": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_int64,
+                    ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p], ctypes.c_int),
 }
 
 
@@ -75,6 +77,8 @@ class LtltError(RuntimeError):
             what = "a device-side bounded wait gave up"
         elif code == -2000:
             what = "size not supported on this device"
+        elif code == -4000:
+            what = "X is singular (odd order)"
         elif code <= -1000:
             what = f"HIP runtime error {-1000 - code}"
         else:
@@ -197,6 +201,34 @@ def pfaffian_direct(A, nb: int = 0, ipiv=None):
                                        logabs.data_ptr(), sign.data_ptr(), _stream_ptr(A.device))
     _check("ltlt_pfaffian_direct", code)
     return ipiv[:n], logabs, sign
+
+
+def solve(A, ipiv, B):
+    """Overwrite B (column-major n or n x nrhs, same dtype and device as A)
+    with X^{-1} B from ``factor``'s output (see ``ltlt_solve``)."""
+    _require_gpu(A)
+    _require_gpu(B)
+    lda = _colmajor_lda(A)
+    n = A.shape[0]
+    if B.dtype != A.dtype:
+        raise ValueError("B must have A's dtype")
+    if B.dim() == 1:
+        nrhs, ldb = 1, max(B.shape[0], 1)
+        if B.stride(0) != 1:
+            raise ValueError("B must be contiguous")
+    elif B.dim() == 2:
+        nrhs = B.shape[1]
+        if B.shape[0] > 1 and B.stride(0) != 1:
+            raise ValueError("B must be column-major")
+        ldb = B.stride(1) if nrhs > 1 else max(B.shape[0], 1)
+    else:
+        raise ValueError("B must be 1-D or 2-D")
+    if B.shape[0] != n:
+        raise ValueError("B must have n rows")
+    code = load().ltlt_solve(n, A.data_ptr(), lda, _dtype_code(A), ipiv.data_ptr(), nrhs, B.data_ptr(), ldb,
+                             _stream_ptr(A.device))
+    _check("ltlt_solve", code)
+    return B
 
 
 def factor_batched(A, ipiv=None):

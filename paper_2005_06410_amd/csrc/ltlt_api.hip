@@ -381,6 +381,56 @@ int ltlt_pfaffian_direct(int64_t n, void* A, int64_t lda, int dtype, int32_t* ip
   return pfaffian_direct_impl<float>(n, static_cast<float*>(A), lda, ipiv, (int)nb, logabs, sign, stream);
 }
 
+int ltlt_solve(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* ipiv, int64_t nrhs, void* B,
+               int64_t ldb, hipStream_t stream) {
+  if (n < 0 || n > (int64_t)INT32_MAX / 2) return -1;
+  if (A == nullptr && n > 0) return -2;
+  if (lda < std::max<int64_t>(1, n)) return -3;
+  if (bad_dtype(dtype)) return -4;
+  if (ipiv == nullptr && n > 0) return -5;
+  if (nrhs < 0 || nrhs > (int64_t)INT32_MAX / 2) return -6;
+  if (B == nullptr && n > 0 && nrhs > 0) return -7;
+  if (ldb < std::max<int64_t>(1, n)) return -8;
+  if (n & 1) return LTLT_ERR_SINGULAR;           // a skew matrix of odd order is singular
+  if (n == 0 || nrhs == 0) return 0;
+  const size_t esz = dtype == LTLT_F64 ? sizeof(double) : sizeof(float);
+  const int64_t ldy = (n + 63) / 64 * 64;
+  const int nblk = (int)((n + 63) / 64);
+  Carve cv;
+  const size_t o_perm = cv.take<int>((size_t)n);
+  const size_t o_scr = cv.take<int>((size_t)n);
+  const size_t o_al = cv.take<char>((size_t)n * esz);
+  const size_t o_ral = cv.take<char>((size_t)n * esz);
+  const size_t o_Y = cv.take<char>((size_t)ldy * kSolveRhs * esz);
+  const size_t o_W = cv.take<char>((size_t)ldy * kSolveRhs * esz);
+  const size_t o_fl = cv.take<int>((size_t)2 * nblk);
+  void* ws = nullptr;
+  int* status = nullptr;
+  hipError_t e = workspace(cv.off, &ws, &status);
+  if (e != hipSuccess) return hip_err(e);
+  char* base = static_cast<char*>(ws);
+  SolveWork w{};
+  w.perm = reinterpret_cast<int*>(base + o_perm);
+  w.scratch = reinterpret_cast<int*>(base + o_scr);
+  w.alpha = base + o_al;
+  w.ralpha = base + o_ral;
+  w.Y = base + o_Y;
+  w.W = base + o_W;
+  w.ldy = ldy;
+  w.flags = reinterpret_cast<int*>(base + o_fl);
+  w.status = status;
+  e = launch_init(nullptr, 0, status, stream);    // clear the bounded-wait flag
+  if (e == hipSuccess) {
+    if (dtype == LTLT_F64)
+      e = launch_solve<double>((int)n, static_cast<const double*>(A), lda, ipiv, (int)nrhs, static_cast<double*>(B),
+                               ldb, w, stream);
+    else
+      e = launch_solve<float>((int)n, static_cast<const float*>(A), lda, ipiv, (int)nrhs, static_cast<float*>(B),
+                              ldb, w, stream);
+  }
+  return e == hipSuccess ? 0 : hip_err(e);
+}
+
 int ltlt_factor_batched(int64_t n, int64_t batch, void* A, int64_t lda, int64_t strideA, int dtype,
                         int32_t* ipiv, int64_t strideIpiv, double* logabs, int32_t* sign, hipStream_t stream) {
   if (n < 0 || n > LTLT_BATCHED_MAX_N) return -1;

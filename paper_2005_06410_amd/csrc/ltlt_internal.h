@@ -72,6 +72,23 @@ int panel_rows(int bw);
 
 // Pfaffian-only path (even column steps): the pair panel and the commit of
 // its alphas.
+// Solve with the factors.
+constexpr int kSolveRhs = 8;                    // right-hand sides per pass
+constexpr size_t kSolvePermLds = 144 * 1024;    // LDS the permutation kernel may use (8 n bytes)
+struct SolveWork {
+  int* perm;          // [n]
+  int* scratch;       // [n] index array when it does not fit in LDS
+  void* alpha;        // [n] alpha_k
+  void* ralpha;       // [n] 1 / alpha_k
+  void* Y;            // [ldy][kSolveRhs]
+  void* W;            // [ldy][kSolveRhs]
+  int64_t ldy;
+  int* flags;         // [2 * blocks]
+  int* status;
+};
+template <typename T> hipError_t launch_solve(int n, const T* A, int64_t lda, const int* ipiv, int nrhs, T* B,
+                                              int64_t ldb, const SolveWork& w, hipStream_t s);
+
 int pair_panel_rows(int bw);                     // rows per pair-panel workgroup
 template <typename T> size_t pair_lds_bytes(int bw, int R);
 template <typename T> int pair_max_blocks(int bw, size_t lds);

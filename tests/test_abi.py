@@ -32,7 +32,7 @@ def test_header_declares_the_entry_points():
     for must in ["ltlt_factor", "ltlt_factor_nb", "ltlt_pfaffian", "ltlt_factor_batched",
                  "ltlt_skew_update", "ltlt_device_status", "ltlt_profile_enable",
                  "ltlt_profile_read", "ltlt_release_workspace", "ltlt_mfma_probe",
-                 "ltlt_pfaffian_direct"]:
+                 "ltlt_pfaffian_direct", "ltlt_solve"]:
         assert must in names
 
 
@@ -143,6 +143,23 @@ def test_mfma_probe_argument_checks(lib, args, code):
 ])
 def test_pfaffian_direct_argument_checks(lib, args, code):
     assert lib.ltlt_pfaffian_direct(*args) == code
+
+
+@pytest.mark.parametrize("args,code", [
+    ((-1, 1, 1, 0, 1, 1, 1, 1, NULL), -1),
+    ((4, NULL, 4, 0, 1, 1, 1, 4, NULL), -2),
+    ((4, 1, 3, 0, 1, 1, 1, 4, NULL), -3),
+    ((4, 1, 4, 9, 1, 1, 1, 4, NULL), -4),
+    ((4, 1, 4, 0, NULL, 1, 1, 4, NULL), -5),
+    ((4, 1, 4, 0, 1, -1, 1, 4, NULL), -6),
+    ((4, 1, 4, 0, 1, 1, NULL, 4, NULL), -7),
+    ((4, 1, 4, 0, 1, 1, 1, 3, NULL), -8),
+    ((5, 1, 5, 0, 1, 1, 1, 5, NULL), -4000),     # odd order: singular
+    ((0, NULL, 1, 0, NULL, 1, NULL, 1, NULL), 0),  # nothing to solve
+    ((4, 1, 4, 0, 1, 0, NULL, 4, NULL), 0),        # no right-hand side
+])
+def test_solve_argument_checks(lib, args, code):
+    assert lib.ltlt_solve(*args) == code
 
 
 def test_error_messages():
