@@ -398,7 +398,9 @@ int ltlt_solve(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* 
   const int nblk = (int)((n + 63) / 64);
   Carve cv;
   const size_t o_perm = cv.take<int>((size_t)n);
-  const size_t o_scr = cv.take<int>((size_t)n);
+  const size_t o_cnt = cv.take<int>((size_t)2 * n);
+  const size_t o_off = cv.take<int>((size_t)n + 1);
+  const size_t o_list = cv.take<int>((size_t)n);
   const size_t o_al = cv.take<char>((size_t)n * esz);
   const size_t o_ral = cv.take<char>((size_t)n * esz);
   const size_t o_Y = cv.take<char>((size_t)ldy * kSolveRhs * esz);
@@ -411,7 +413,9 @@ int ltlt_solve(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* 
   char* base = static_cast<char*>(ws);
   SolveWork w{};
   w.perm = reinterpret_cast<int*>(base + o_perm);
-  w.scratch = reinterpret_cast<int*>(base + o_scr);
+  w.cnt = reinterpret_cast<int*>(base + o_cnt);
+  w.off = reinterpret_cast<int*>(base + o_off);
+  w.list = reinterpret_cast<int*>(base + o_list);
   w.alpha = base + o_al;
   w.ralpha = base + o_ral;
   w.Y = base + o_Y;

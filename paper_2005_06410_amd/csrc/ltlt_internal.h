@@ -74,10 +74,11 @@ int panel_rows(int bw);
 // its alphas.
 // Solve with the factors.
 constexpr int kSolveRhs = 8;                    // right-hand sides per pass
-constexpr size_t kSolvePermLds = 144 * 1024;    // LDS the permutation kernel may use (8 n bytes)
 struct SolveWork {
   int* perm;          // [n]
-  int* scratch;       // [n] index array when it does not fit in LDS
+  int* cnt;           // [2n] counters (steps per target position, fill)
+  int* off;           // [n+1] bucket offsets
+  int* list;          // [n] steps by target position
   void* alpha;        // [n] alpha_k
   void* ralpha;       // [n] 1 / alpha_k
   void* Y;            // [ldy][kSolveRhs]

@@ -11,8 +11,8 @@
 //   x = P^T u          x[perm[i]] = u[i].
 //
 // gfx950 mapping:
-//  * perm: one thread applies the n exchanges to an index array in LDS
-//    (ipiv[i] >= i, so position i is final once step i is done);
+//  * perm: every row follows its own moves through the exchanges, in
+//    parallel (the steps bucketed by the position they target);
 //  * the triangular solves are persistent cooperative kernels over 64-row
 //    blocks, left-looking: the workgroup of block b streams the 64x64 tiles
 //    of L to the left of its diagonal block (forward) or below it (backward)
@@ -40,32 +40,67 @@ constexpr int kSGroups = kSThreads / kSB;   // column (or row) groups of a tile
 constexpr int kSCols = kSB / kSGroups;      // 16 columns per group
 
 // ---- permutation ----------------------------------------------------------
-// at[i] = index of the row at position i after the exchanges (i, ipiv[i]),
-// i = 0 .. n-1, in order.  With use_lds the index array and a copy of ipiv
-// sit in LDS (8 n bytes); otherwise the index array is in global scratch and
-// ipiv is read from global memory (slow: one dependent access per step).
-__global__ void __launch_bounds__(256) solve_perm_kernel(int n, const int* ipiv, int* perm, int* gscratch,
-                                                         int use_lds) {
-  extern __shared__ int slds[];
-  int* at = use_lds ? slds : gscratch;
-  const int* piv = ipiv;
-  if (use_lds) {
-    int* sp = slds + n;
-    for (int i = threadIdx.x; i < n; i += blockDim.x) sp[i] = ipiv[i];
-    piv = sp;
+// perm[i] = index of the row at position i after the exchanges (i, ipiv[i]),
+// i = 0 .. n-1 in order, with ipiv[i] >= i, so position i is final once step
+// i is done.  Computed per row, in parallel: a row at position x at step t
+// is moved next either by the first step s in [t, x) with ipiv[s] = x (it
+// then lands at s, final), or, failing that, by step x itself (to ipiv[x],
+// or it stays at x when ipiv[x] = x).  The steps are bucketed by the position
+// they target (count, scan, scatter), then every row walks its positions.
+__global__ void perm_count_kernel(int n, const int* ipiv, int* cnt) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s < n) {
+    const int x = ipiv[s];
+    if (x > s && x < n) atomicAdd(&cnt[x], 1);
   }
-  for (int i = threadIdx.x; i < n; i += blockDim.x) at[i] = i;
+}
+
+// exclusive prefix sum of cnt[0..n) into off[0..n] (one workgroup)
+__global__ void __launch_bounds__(1024) perm_scan_kernel(int n, const int* cnt, int* off) {
+  __shared__ int part[1024];
+  const int t = threadIdx.x;
+  const int per = (n + 1023) / 1024;
+  const int lo = min(n, t * per), hi = min(n, lo + per);
+  int sum = 0;
+  for (int i = lo; i < hi; ++i) sum += cnt[i];
+  part[t] = sum;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int i = 0; i < n; ++i) {
-      const int p = piv[i];
-      const int x = at[i], y = at[p];
-      at[i] = y;
-      at[p] = x;
+  for (int d = 1; d < 1024; d <<= 1) {            // inclusive scan of the per-thread sums
+    const int v = t >= d ? part[t - d] : 0;
+    __syncthreads();
+    part[t] += v;
+    __syncthreads();
+  }
+  int run = part[t] - sum;
+  for (int i = lo; i < hi; ++i) { off[i] = run; run += cnt[i]; }
+  if (t == 1023) off[n] = part[1023];
+}
+
+__global__ void perm_scatter_kernel(int n, const int* ipiv, const int* off, int* fill, int* list) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s < n) {
+    const int x = ipiv[s];
+    if (x > s && x < n) list[off[x] + atomicAdd(&fill[x], 1)] = s;
+  }
+}
+
+__global__ void perm_walk_kernel(int n, const int* ipiv, const int* off, const int* list, int* perm) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= n) return;
+  int x = r, t = 0;
+  for (;;) {
+    int first = INT32_MAX;                         // first step s in [t, x) targeting x
+    for (int e = off[x]; e < off[x + 1]; ++e) {
+      const int s = list[e];
+      if (s >= t && s < first) first = s;
     }
+    if (first != INT32_MAX) { x = first; break; }
+    const int p = ipiv[x];
+    if (p <= x || p >= n) break;                   // no move (ipiv[x] = x)
+    t = x + 1;
+    x = p;
   }
-  __syncthreads();
-  for (int i = threadIdx.x; i < n; i += blockDim.x) perm[i] = at[i];
+  perm[x] = r;
 }
 
 template <typename T>
@@ -99,34 +134,70 @@ __global__ void solve_flags_kernel(int* flags, int count) {
 }
 
 // ---- skew tridiagonal recurrences -----------------------------------------
-// lane l < nr: odd unknowns of right-hand side l, forward; lane 32 + l: even
-// unknowns, backward.  Each chain reads the inputs of the other chain's
-// parity, so the result goes to a separate buffer W.
+// Wave 0 runs the odd unknowns forward, wave 1 the even unknowns backward;
+// lane q < nr takes right-hand side q.  Each chain reads the inputs of the
+// other chain's parity, so the result goes to a separate buffer W.  The
+// inputs of kTriChunk steps at a time are staged in LDS by the whole wave, so
+// that the chain itself waits only on its own arithmetic.
+constexpr int kTriChunk = 512;
 template <typename T>
-__global__ void __launch_bounds__(64) solve_tridiag_kernel(int n, int nr, const T* alpha, const T* ralpha,
-                                                           const T* Y, T* W, int64_t ldy) {
-  const int lane = threadIdx.x;
-  const int q = lane & 31;
-  if (q >= nr) return;
-  const T* y = Y + (int64_t)q * ldy;
-  T* wv = W + (int64_t)q * ldy;
-  if (lane < 32) {
-    // W[1] = -R[0] / alpha_0;  W[i+1] = (alpha_{i-1} W[i-1] - R[i]) / alpha_i, i even
-    T wprev = -y[0] * ralpha[0];
-    wv[1] = wprev;
-    for (int i = 2; i + 1 < n; i += 2) {
-      const T w = (alpha[i - 1] * wprev - y[i]) * ralpha[i];
-      wv[i + 1] = w;
-      wprev = w;
+__global__ void __launch_bounds__(128) solve_tridiag_kernel(int n, int nr, const T* alpha, const T* ralpha,
+                                                            const T* Y, T* W, int64_t ldy) {
+  __shared__ T sbuf[2][kTriChunk * (2 + kSolveRhs)];
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x & (kWave - 1);
+  T* sa = sbuf[wave];                              // multiplier alpha of each step
+  T* sr = sa + kTriChunk;                          // reciprocal alpha of each step
+  T* sy = sr + kTriChunk;                          // [step][rhs] right-hand side entry
+  const int half = n / 2;                          // unknowns per chain
+  if (wave == 0) {
+    // W[1] = -R[0] / alpha_0;  step s >= 1, i = 2s:  W[i+1] = (alpha_{i-1} W[i-1] - R[i]) / alpha_i
+    T wprev = T(0);
+    if (lane < nr) {
+      wprev = -Y[(int64_t)lane * ldy] * ralpha[0];
+      W[1 + (int64_t)lane * ldy] = wprev;
+    }
+    for (int s0 = 1; s0 < half; s0 += kTriChunk) {
+      const int cnt = min(kTriChunk, half - s0);
+      for (int e = lane; e < cnt; e += kWave) {
+        const int i = 2 * (s0 + e);
+        sa[e] = alpha[i - 1];
+        sr[e] = ralpha[i];
+        for (int q = 0; q < nr; ++q) sy[e * kSolveRhs + q] = Y[(int64_t)i + (int64_t)q * ldy];
+      }
+      wave_lds_sync();
+      if (lane < nr) {
+        for (int e = 0; e < cnt; ++e) {
+          const T w = (sa[e] * wprev - sy[e * kSolveRhs + lane]) * sr[e];
+          W[(int64_t)(2 * (s0 + e) + 1) + (int64_t)lane * ldy] = w;
+          wprev = w;
+        }
+      }
+      wave_lds_sync();
     }
   } else {
-    // W[n-2] = R[n-1] / alpha_{n-2};  W[i-1] = (R[i] + alpha_i W[i+1]) / alpha_{i-1}, i odd
-    T wnext = y[n - 1] * ralpha[n - 2];
-    wv[n - 2] = wnext;
-    for (int i = n - 3; i >= 1; i -= 2) {
-      const T w = (y[i] + alpha[i] * wnext) * ralpha[i - 1];
-      wv[i - 1] = w;
-      wnext = w;
+    // W[n-2] = R[n-1] / alpha_{n-2};  step s >= 1, i = n-1-2s:  W[i-1] = (R[i] + alpha_i W[i+1]) / alpha_{i-1}
+    T wnext = T(0);
+    if (lane < nr) {
+      wnext = Y[(int64_t)(n - 1) + (int64_t)lane * ldy] * ralpha[n - 2];
+      W[(int64_t)(n - 2) + (int64_t)lane * ldy] = wnext;
+    }
+    for (int s0 = 1; s0 < half; s0 += kTriChunk) {
+      const int cnt = min(kTriChunk, half - s0);
+      for (int e = lane; e < cnt; e += kWave) {
+        const int i = n - 1 - 2 * (s0 + e);
+        sa[e] = alpha[i];
+        sr[e] = ralpha[i - 1];
+        for (int q = 0; q < nr; ++q) sy[e * kSolveRhs + q] = Y[(int64_t)i + (int64_t)q * ldy];
+      }
+      wave_lds_sync();
+      if (lane < nr) {
+        for (int e = 0; e < cnt; ++e) {
+          const T w = (sy[e * kSolveRhs + lane] + sa[e] * wnext) * sr[e];
+          W[(int64_t)(n - 2 - 2 * (s0 + e)) + (int64_t)lane * ldy] = w;
+          wnext = w;
+        }
+      }
+      wave_lds_sync();
     }
   }
 }
@@ -183,132 +254,107 @@ __device__ __forceinline__ bool wait_flag(int* flag, int* status, int& s_abort) 
   return s_abort == 0;
 }
 
-// Forward: z_b = y_b - sum_{c<b} L_bc z_c, then z_b = L_bb^{-1} z_b.
+// Broadcast lane l's value (l wave-uniform) through scalar registers.
 template <typename T>
-__global__ void __launch_bounds__(kSThreads, 1) solve_lower_kernel(SolveTriArgs a) {
+__device__ __forceinline__ T lane_bcast(T x, int l) {
+  if constexpr (sizeof(T) == 8) {
+    const int lo = __builtin_amdgcn_readlane(__double2loint(x), l);
+    const int hi = __builtin_amdgcn_readlane(__double2hiint(x), l);
+    return __hiloint2double(hi, lo);
+  } else {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
+  }
+}
+
+// Forward (UPPER = false): z_b = L_bb^{-1} (y_b - sum_{c<b} L_bc z_c).
+// Backward (UPPER = true), blocks from the last one down:
+//   u_b = L_bb^{-T} (w_b - sum_{b'>b} L_{b'b}^T u_{b'}).
+// The off-diagonal tiles of a block are streamed through LDS with the next
+// tile's values already in registers (they do not depend on any flag); the
+// diagonal tile has its own buffer, loaded at the start of the block.
+template <typename T, bool UPPER>
+__global__ void __launch_bounds__(kSThreads, 1) solve_tri_kernel(SolveTriArgs a) {
   __shared__ T tile[kSB * kSLd];
-  __shared__ T yc[kSB * kSolveRhs];                // z of the block a tile multiplies
-  __shared__ T part[kSGroups * kSB * kSolveRhs];   // partial sums of the four column groups
+  __shared__ T dtile[kSB * kSLd];
+  __shared__ T yc[kSB * kSolveRhs];                // solution of the block a tile multiplies
+  __shared__ T part[kSGroups * kSB * kSolveRhs];   // partial sums of the four groups
   __shared__ int s_abort;
   const T* A = static_cast<const T*>(a.A);
   T* Y = static_cast<T*>(a.Y);
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int r = tid & (kSB - 1), g = tid / kSB;
-  const int n = a.n, nr = a.nr;
+  const int n = a.n, nr = a.nr, nblk = a.nblk;
+  const int64_t lda = a.lda, ldy = a.ldy;
   if (tid == 0) s_abort = 0;
   __syncthreads();
-  for (int b = blockIdx.x; b < a.nblk; b += gridDim.x) {
-    const int r0 = b * kSB;
+  for (int i = blockIdx.x; i < nblk; i += gridDim.x) {
+    const int b = UPPER ? nblk - 1 - i : i;
+    const int d0 = b * kSB;
+    const int ntile = UPPER ? nblk - 1 - b : b;
+    // tile t multiplies the solution of block src(t): forward t, backward nblk-1-t
+    auto src = [&](int t) { return UPPER ? nblk - 1 - t : t; };
+    T regs[kSCols];
+    auto fetch = [&](int t) {
+      const int s0 = src(t) * kSB;
+      const int rr0 = UPPER ? s0 : d0, cc0 = UPPER ? d0 : s0;
+#pragma unroll
+      for (int jj = 0; jj < kSCols; ++jj) regs[jj] = l_entry(A, lda, n, rr0 + r, cc0 + g + kSGroups * jj);
+    };
+    load_l_tile(A, lda, n, d0, d0, dtile, tid);
     T acc[kSolveRhs];
 #pragma unroll
     for (int q = 0; q < kSolveRhs; ++q) acc[q] = T(0);
-    for (int c = 0; c < b; ++c) {
-      const int c0 = c * kSB;
-      load_l_tile(A, a.lda, n, r0, c0, tile, tid);
-      if (!wait_flag<T>(&a.flag[c], a.status, s_abort)) return;
+    if (ntile > 0) fetch(0);
+    for (int t = 0; t < ntile; ++t) {
+#pragma unroll
+      for (int jj = 0; jj < kSCols; ++jj) tile[(g + kSGroups * jj) * kSLd + r] = regs[jj];
+      if (t + 1 < ntile) fetch(t + 1);
+      const int sb = src(t), s0 = sb * kSB;
+      if (!wait_flag<T>(&a.flag[sb], a.status, s_abort)) return;
       for (int e = tid; e < kSB * nr; e += kSThreads) {
         const int rr = e % kSB, q = e / kSB;
-        yc[rr * kSolveRhs + q] = (c0 + rr < n) ? ld_coh_t(&Y[(int64_t)(c0 + rr) + (int64_t)q * a.ldy]) : T(0);
+        yc[rr * kSolveRhs + q] = (s0 + rr < n) ? ld_coh_t(&Y[(int64_t)(s0 + rr) + (int64_t)q * ldy]) : T(0);
       }
       __syncthreads();
+      // forward: thread (row r, column group g); backward: (column r, row group g)
 #pragma unroll 4
       for (int jj = 0; jj < kSCols; ++jj) {
-        const int cc = g * kSCols + jj;
-        const T lv = tile[cc * kSLd + r];
+        const int k = g * kSCols + jj;
+        const T lv = UPPER ? tile[r * kSLd + k] : tile[k * kSLd + r];
 #pragma unroll
         for (int q = 0; q < kSolveRhs; ++q)
-          if (q < nr) acc[q] = fma(lv, yc[cc * kSolveRhs + q], acc[q]);
+          if (q < nr) acc[q] = fma(lv, yc[k * kSolveRhs + q], acc[q]);
       }
       __syncthreads();
     }
-    // sum the four groups, subtract from y_b
 #pragma unroll
     for (int q = 0; q < kSolveRhs; ++q) part[(g * kSB + r) * kSolveRhs + q] = acc[q];
-    load_l_tile(A, a.lda, n, r0, r0, tile, tid);
     __syncthreads();
     // diagonal block: wave w solves right-hand sides w, w+4; lane = row
+    // (forward) or column (backward) of the block
     for (int q = wave; q < nr; q += kSThreads / kWave) {
       T x = T(0);
-      if (r0 + lane < n) {
-        x = ld_coh_t(&Y[(int64_t)(r0 + lane) + (int64_t)q * a.ldy]);
-        T s = T(0);
+      if (d0 + lane < n) {
+        x = ld_coh_t(&Y[(int64_t)(d0 + lane) + (int64_t)q * ldy]);
+        T sum = T(0);
 #pragma unroll
-        for (int gg = 0; gg < kSGroups; ++gg) s += part[(gg * kSB + lane) * kSolveRhs + q];
-        x -= s;
+        for (int gg = 0; gg < kSGroups; ++gg) sum += part[(gg * kSB + lane) * kSolveRhs + q];
+        x -= sum;
       }
-#pragma unroll 8
-      for (int cc = 0; cc < kSB; ++cc) {
-        const T xc = __shfl(x, cc, kWave);
-        if (lane > cc) x = fma(-tile[cc * kSLd + lane], xc, x);
-      }
-      if (r0 + lane < n) st_coh_t(&Y[(int64_t)(r0 + lane) + (int64_t)q * a.ldy], x);
-    }
-    wait_stores();
-    __syncthreads();
-    if (tid == 0) st_coh(&a.flag[b], 1);
-  }
-}
-
-// Backward: u_b = w_b - sum_{b'>b} L_{b'b}^T u_{b'}, then u_b = L_bb^{-T} u_b.
-// Blocks are taken from the last one down.
-template <typename T>
-__global__ void __launch_bounds__(kSThreads, 1) solve_upper_kernel(SolveTriArgs a) {
-  __shared__ T tile[kSB * kSLd];
-  __shared__ T yc[kSB * kSolveRhs];
-  __shared__ T part[kSGroups * kSB * kSolveRhs];
-  __shared__ int s_abort;
-  const T* A = static_cast<const T*>(a.A);
-  T* Y = static_cast<T*>(a.Y);
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-  const int cl = tid & (kSB - 1), g = tid / kSB;   // this thread's column of the block, row group
-  const int n = a.n, nr = a.nr;
-  if (tid == 0) s_abort = 0;
-  __syncthreads();
-  for (int i = blockIdx.x; i < a.nblk; i += gridDim.x) {
-    const int b = a.nblk - 1 - i;
-    const int c0 = b * kSB;
-    T acc[kSolveRhs];
+      if constexpr (!UPPER) {
 #pragma unroll
-    for (int q = 0; q < kSolveRhs; ++q) acc[q] = T(0);
-    for (int bp = a.nblk - 1; bp > b; --bp) {
-      const int r0 = bp * kSB;
-      load_l_tile(A, a.lda, n, r0, c0, tile, tid);   // tile[cc][rr] = L(r0 + rr, c0 + cc)
-      if (!wait_flag<T>(&a.flag[bp], a.status, s_abort)) return;
-      for (int e = tid; e < kSB * nr; e += kSThreads) {
-        const int rr = e % kSB, q = e / kSB;
-        yc[rr * kSolveRhs + q] = (r0 + rr < n) ? ld_coh_t(&Y[(int64_t)(r0 + rr) + (int64_t)q * a.ldy]) : T(0);
-      }
-      __syncthreads();
-#pragma unroll 4
-      for (int jj = 0; jj < kSCols; ++jj) {
-        const int rr = g * kSCols + jj;
-        const T lv = tile[cl * kSLd + rr];
+        for (int cc = 0; cc < kSB; ++cc) {
+          const T xc = lane_bcast(x, cc);
+          if (lane > cc) x = fma(-dtile[cc * kSLd + lane], xc, x);   // L(d0+lane, d0+cc)
+        }
+      } else {
 #pragma unroll
-        for (int q = 0; q < kSolveRhs; ++q)
-          if (q < nr) acc[q] = fma(lv, yc[rr * kSolveRhs + q], acc[q]);
+        for (int rr = kSB - 1; rr >= 0; --rr) {
+          const T xr = lane_bcast(x, rr);
+          if (lane < rr) x = fma(-dtile[lane * kSLd + rr], xr, x);   // L(d0+rr, d0+lane)
+        }
       }
-      __syncthreads();
-    }
-#pragma unroll
-    for (int q = 0; q < kSolveRhs; ++q) part[(g * kSB + cl) * kSolveRhs + q] = acc[q];
-    load_l_tile(A, a.lda, n, c0, c0, tile, tid);
-    __syncthreads();
-    // diagonal block, backward: lane = column c of the block
-    for (int q = wave; q < nr; q += kSThreads / kWave) {
-      T x = T(0);
-      if (c0 + lane < n) {
-        x = ld_coh_t(&Y[(int64_t)(c0 + lane) + (int64_t)q * a.ldy]);
-        T s = T(0);
-#pragma unroll
-        for (int gg = 0; gg < kSGroups; ++gg) s += part[(gg * kSB + lane) * kSolveRhs + q];
-        x -= s;
-      }
-#pragma unroll 8
-      for (int rr = kSB - 1; rr >= 0; --rr) {
-        const T xr = __shfl(x, rr, kWave);
-        if (lane < rr) x = fma(-tile[lane * kSLd + rr], xr, x);   // L(c0+rr, c0+lane)
-      }
-      if (c0 + lane < n) st_coh_t(&Y[(int64_t)(c0 + lane) + (int64_t)q * a.ldy], x);
+      if (d0 + lane < n) st_coh_t(&Y[(int64_t)(d0 + lane) + (int64_t)q * ldy], x);
     }
     wait_stores();
     __syncthreads();
@@ -321,9 +367,7 @@ int solve_tri_max_blocks() {
   int dev = 0, per_cu = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-  const void* k;
-  if constexpr (UPPER) k = (const void*)solve_upper_kernel<T>;
-  else k = (const void*)solve_lower_kernel<T>;
+  const void* k = (const void*)solve_tri_kernel<T, UPPER>;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, kSThreads, 0) != hipSuccess) return 0;
   return per_cu * cus;
 }
@@ -335,32 +379,21 @@ hipError_t launch_solve_tri(const SolveTriArgs& a, hipStream_t s) {
   const int grid = a.nblk < cap ? a.nblk : cap;
   SolveTriArgs copy = a;
   void* args[] = {&copy};
-  const void* k;
-  if constexpr (UPPER) k = (const void*)solve_upper_kernel<T>;
-  else k = (const void*)solve_lower_kernel<T>;
+  const void* k = (const void*)solve_tri_kernel<T, UPPER>;
   return hipLaunchCooperativeKernel(k, dim3(grid), dim3(kSThreads), args, 0, s);
 }
-
-size_t solve_perm_lds_bytes(int n) { return 2 * (size_t)n * sizeof(int); }
 
 template <typename T>
 hipError_t launch_solve(int n, const T* A, int64_t lda, const int* ipiv, int nrhs, T* B, int64_t ldb,
                         const SolveWork& w, hipStream_t s) {
   hipError_t e;
   {
-    const size_t lds = solve_perm_lds_bytes(n);
-    const int use_lds = lds <= kSolvePermLds ? 1 : 0;
-    if (use_lds) {
-      static bool attr_set = false;
-      if (!attr_set) {
-        e = hipFuncSetAttribute((const void*)solve_perm_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                (int)kSolvePermLds);
-        if (e != hipSuccess) return e;
-        attr_set = true;
-      }
-    }
-    hipLaunchKernelGGL(solve_perm_kernel, dim3(1), dim3(256), use_lds ? lds : 0, s, n, ipiv, w.perm, w.scratch,
-                       use_lds);
+    const int gb = (n + 255) / 256;
+    hipLaunchKernelGGL(solve_flags_kernel, dim3((2 * n + 255) / 256), dim3(256), 0, s, w.cnt, 2 * n);
+    hipLaunchKernelGGL(perm_count_kernel, dim3(gb), dim3(256), 0, s, n, ipiv, w.cnt);
+    hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(1024), 0, s, n, w.cnt, w.off);
+    hipLaunchKernelGGL(perm_scatter_kernel, dim3(gb), dim3(256), 0, s, n, ipiv, w.off, w.cnt + n, w.list);
+    hipLaunchKernelGGL(perm_walk_kernel, dim3(gb), dim3(256), 0, s, n, ipiv, w.off, w.list, w.perm);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   T* alpha = static_cast<T*>(w.alpha);
@@ -381,7 +414,7 @@ hipError_t launch_solve(int n, const T* A, int64_t lda, const int* ipiv, int nrh
     ta.A = A; ta.lda = lda; ta.n = n; ta.nblk = nblk; ta.Y = Y; ta.ldy = w.ldy; ta.nr = nr;
     ta.flag = w.flags; ta.status = w.status;
     if ((e = launch_solve_tri<T, false>(ta, s)) != hipSuccess) return e;
-    hipLaunchKernelGGL(solve_tridiag_kernel<T>, dim3(1), dim3(64), 0, s, n, nr, alpha, ralpha, Y, W, w.ldy);
+    hipLaunchKernelGGL(solve_tridiag_kernel<T>, dim3(1), dim3(128), 0, s, n, nr, alpha, ralpha, Y, W, w.ldy);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     ta.Y = W;
     ta.flag = w.flags + nblk;
