@@ -405,7 +405,7 @@ int ltlt_solve(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* 
   const size_t o_ral = cv.take<char>((size_t)n * esz);
   const size_t o_Y = cv.take<char>((size_t)ldy * kSolveRhs * esz);
   const size_t o_W = cv.take<char>((size_t)ldy * kSolveRhs * esz);
-  const size_t o_fl = cv.take<int>((size_t)2 * nblk);
+  const size_t o_box = cv.take<uint64_t>((size_t)nblk * kSolveRhs * 64 * 2);
   void* ws = nullptr;
   int* status = nullptr;
   hipError_t e = workspace(cv.off, &ws, &status);
@@ -421,7 +421,7 @@ int ltlt_solve(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* 
   w.Y = base + o_Y;
   w.W = base + o_W;
   w.ldy = ldy;
-  w.flags = reinterpret_cast<int*>(base + o_fl);
+  w.box = reinterpret_cast<uint64_t*>(base + o_box);
   w.status = status;
   e = launch_init(nullptr, 0, status, stream);    // clear the bounded-wait flag
   if (e == hipSuccess) {

@@ -84,7 +84,7 @@ struct SolveWork {
   void* Y;            // [ldy][kSolveRhs]
   void* W;            // [ldy][kSolveRhs]
   int64_t ldy;
-  int* flags;         // [2 * blocks]
+  uint64_t* box;      // [blocks][kSolveRhs][64][2] stamped solution words
   int* status;
 };
 template <typename T> hipError_t launch_solve(int n, const T* A, int64_t lda, const int* ipiv, int nrhs, T* B,

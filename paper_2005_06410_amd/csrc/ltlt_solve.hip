@@ -16,9 +16,10 @@
 //  * the triangular solves are persistent cooperative kernels over 64-row
 //    blocks, left-looking: the workgroup of block b streams the 64x64 tiles
 //    of L to the left of its diagonal block (forward) or below it (backward)
-//    through LDS, waiting for the flag of the block each tile multiplies,
-//    then solves its diagonal block (one wave per right-hand side, the
-//    unknown broadcast by readlane) and raises its own flag.  A workgroup
+//    through LDS, waiting for the stamped solution words of the block each
+//    tile multiplies, then solves its diagonal block (one wave per
+//    right-hand side, the unknown broadcast by readlane) and publishes its
+//    own solution as stamped words.  A workgroup
 //    takes its blocks in dependency order, so the earliest unfinished block
 //    always has its inputs and the grid cannot deadlock; every wait is
 //    bounded.  Each solve reads the lower triangle of L once: HBM-bound for
@@ -30,6 +31,8 @@
 #include "ltlt_device.h"
 #include "ltlt_exchange.h"
 #include "ltlt_internal.h"
+
+#include <atomic>
 
 namespace ltlt {
 
@@ -128,9 +131,9 @@ __global__ void solve_alpha_kernel(int n, const T* A, int64_t lda, T* alpha, T* 
   }
 }
 
-__global__ void solve_flags_kernel(int* flags, int count) {
+__global__ void zero_ints_kernel(int* v, int count) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < count) flags[i] = 0;
+  if (i < count) v[i] = 0;
 }
 
 // ---- skew tridiagonal recurrences -----------------------------------------
@@ -211,9 +214,38 @@ struct SolveTriArgs {
   void* Y;
   int64_t ldy;
   int nr;             // right-hand sides of this pass (<= kSolveRhs)
-  int* flag;          // [nblk], 0 = not yet solved
+  uint64_t* box;      // [nblk][kSolveRhs][kSB][2] stamped solution words
+  unsigned stamp;     // stamp of this launch (never 0)
   int* status;
 };
+
+// A solution value crosses workgroups as two 64-bit words, each holding one
+// 32-bit half of the value above the 32-bit stamp of the launch: naturally
+// aligned 64-bit stores are single-copy atomic, so a reader that sees the
+// stamp in both words has the value, without a separate flag (and the writer
+// does not wait for its stores before signalling).  Words of an earlier
+// launch carry an older stamp and never validate.
+template <typename T>
+__device__ __forceinline__ void box_put(uint64_t* w, T x, unsigned stamp) {
+  unsigned hi, lo;
+  if constexpr (sizeof(T) == 8) {
+    hi = (unsigned)__double2hiint(x);
+    lo = (unsigned)__double2loint(x);
+  } else {
+    hi = __float_as_uint(x);
+    lo = 0u;
+  }
+  st_coh64(&w[0], ((uint64_t)hi << 32) | stamp);
+  st_coh64(&w[1], ((uint64_t)lo << 32) | stamp);
+}
+template <typename T>
+__device__ __forceinline__ bool box_get(const uint64_t* w, unsigned stamp, T& x) {
+  const uint64_t w0 = ld_coh64(&w[0]), w1 = ld_coh64(&w[1]);
+  if ((unsigned)w0 != stamp || (unsigned)w1 != stamp) return false;
+  if constexpr (sizeof(T) == 8) x = __hiloint2double((int)(w0 >> 32), (int)(w1 >> 32));
+  else x = __uint_as_float((unsigned)(w0 >> 32));
+  return true;
+}
 
 // L(r, c) for global row r and column c: unit lower, L(:,0) = e_0,
 // L(r, c) = A(r, c-1) below the diagonal.
@@ -237,21 +269,28 @@ __device__ __forceinline__ void load_l_tile(const T* A, int64_t lda, int n, int 
   }
 }
 
+// Poll the solution of block sb until every (row, right-hand side) entry
+// carries this launch's stamp; the values land in yc[row][rhs].  Bounded.
 template <typename T>
-__device__ __forceinline__ bool wait_flag(int* flag, int* status, int& s_abort) {
-  if (threadIdx.x == 0) {
-    const uint64_t t0 = wall_ticks();
-    while (ld_coh(flag) == 0) {
-      if (ld_coh(status) != 0 || wall_ticks() - t0 > kWaitLimitTicks) {
-        atomicOr(status, 1);
-        s_abort = 1;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
+__device__ __forceinline__ bool wait_box(const SolveTriArgs& a, int sb, T* yc, int tid) {
+  const uint64_t* bx = a.box + (size_t)sb * kSolveRhs * kSB * 2;
+  const uint64_t t0 = wall_ticks();
+  for (;;) {
+    bool ok = true;
+    for (int e = tid; e < kSB * a.nr; e += kSThreads) {
+      const int rr = e % kSB, q = e / kSB;
+      T v;
+      if (box_get(&bx[((size_t)q * kSB + rr) * 2], a.stamp, v)) yc[rr * kSolveRhs + q] = v;
+      else ok = false;
     }
+    if (__syncthreads_and(ok)) return true;
+    const bool late = tid == 0 && (ld_coh(a.status) != 0 || wall_ticks() - t0 > kWaitLimitTicks);
+    if (__syncthreads_or(late)) {
+      if (tid == 0) atomicOr(a.status, 1);
+      return false;
+    }
+    __builtin_amdgcn_s_sleep(1);
   }
-  __syncthreads();
-  return s_abort == 0;
 }
 
 // Broadcast lane l's value (l wave-uniform) through scalar registers.
@@ -278,15 +317,12 @@ __global__ void __launch_bounds__(kSThreads, 1) solve_tri_kernel(SolveTriArgs a)
   __shared__ T dtile[kSB * kSLd];
   __shared__ T yc[kSB * kSolveRhs];                // solution of the block a tile multiplies
   __shared__ T part[kSGroups * kSB * kSolveRhs];   // partial sums of the four groups
-  __shared__ int s_abort;
   const T* A = static_cast<const T*>(a.A);
   T* Y = static_cast<T*>(a.Y);
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int r = tid & (kSB - 1), g = tid / kSB;
   const int n = a.n, nr = a.nr, nblk = a.nblk;
   const int64_t lda = a.lda, ldy = a.ldy;
-  if (tid == 0) s_abort = 0;
-  __syncthreads();
   for (int i = blockIdx.x; i < nblk; i += gridDim.x) {
     const int b = UPPER ? nblk - 1 - i : i;
     const int d0 = b * kSB;
@@ -301,6 +337,16 @@ __global__ void __launch_bounds__(kSThreads, 1) solve_tri_kernel(SolveTriArgs a)
       for (int jj = 0; jj < kSCols; ++jj) regs[jj] = l_entry(A, lda, n, rr0 + r, cc0 + g + kSGroups * jj);
     };
     load_l_tile(A, lda, n, d0, d0, dtile, tid);
+    // this wave's right-hand side entries of the block (rhs wave, wave + 4),
+    // read now: they are needed only at the diagonal step, which is on the
+    // chain from block to block
+    constexpr int kQW = kSolveRhs / (kSThreads / kWave);
+    T ypre[kQW];
+#pragma unroll
+    for (int k = 0; k < kQW; ++k) {
+      const int q = wave + (kSThreads / kWave) * k;
+      ypre[k] = (q < nr && d0 + lane < n) ? Y[(int64_t)(d0 + lane) + (int64_t)q * ldy] : T(0);
+    }
     T acc[kSolveRhs];
 #pragma unroll
     for (int q = 0; q < kSolveRhs; ++q) acc[q] = T(0);
@@ -309,13 +355,7 @@ __global__ void __launch_bounds__(kSThreads, 1) solve_tri_kernel(SolveTriArgs a)
 #pragma unroll
       for (int jj = 0; jj < kSCols; ++jj) tile[(g + kSGroups * jj) * kSLd + r] = regs[jj];
       if (t + 1 < ntile) fetch(t + 1);
-      const int sb = src(t), s0 = sb * kSB;
-      if (!wait_flag<T>(&a.flag[sb], a.status, s_abort)) return;
-      for (int e = tid; e < kSB * nr; e += kSThreads) {
-        const int rr = e % kSB, q = e / kSB;
-        yc[rr * kSolveRhs + q] = (s0 + rr < n) ? ld_coh_t(&Y[(int64_t)(s0 + rr) + (int64_t)q * ldy]) : T(0);
-      }
-      __syncthreads();
+      if (!wait_box<T>(a, src(t), yc, tid)) return;
       // forward: thread (row r, column group g); backward: (column r, row group g)
 #pragma unroll 4
       for (int jj = 0; jj < kSCols; ++jj) {
@@ -331,34 +371,40 @@ __global__ void __launch_bounds__(kSThreads, 1) solve_tri_kernel(SolveTriArgs a)
     for (int q = 0; q < kSolveRhs; ++q) part[(g * kSB + r) * kSolveRhs + q] = acc[q];
     __syncthreads();
     // diagonal block: wave w solves right-hand sides w, w+4; lane = row
-    // (forward) or column (backward) of the block
-    for (int q = wave; q < nr; q += kSThreads / kWave) {
+    // (forward) or column (backward) of the block.  The lane's entries of
+    // the diagonal tile go to registers first, so that the 64 dependent steps
+    // wait only on the scalar broadcast and the FMA.
+#pragma unroll
+    for (int k = 0; k < kQW; ++k) {
+      const int q = wave + (kSThreads / kWave) * k;
+      if (q >= nr) break;
+      T dl[kSB];
+#pragma unroll
+      for (int cc = 0; cc < kSB; ++cc) dl[cc] = UPPER ? dtile[lane * kSLd + cc] : dtile[cc * kSLd + lane];
       T x = T(0);
       if (d0 + lane < n) {
-        x = ld_coh_t(&Y[(int64_t)(d0 + lane) + (int64_t)q * ldy]);
         T sum = T(0);
 #pragma unroll
         for (int gg = 0; gg < kSGroups; ++gg) sum += part[(gg * kSB + lane) * kSolveRhs + q];
-        x -= sum;
+        x = ypre[k] - sum;
       }
       if constexpr (!UPPER) {
 #pragma unroll
         for (int cc = 0; cc < kSB; ++cc) {
           const T xc = lane_bcast(x, cc);
-          if (lane > cc) x = fma(-dtile[cc * kSLd + lane], xc, x);   // L(d0+lane, d0+cc)
+          if (lane > cc) x = fma(-dl[cc], xc, x);                    // L(d0+lane, d0+cc)
         }
       } else {
 #pragma unroll
         for (int rr = kSB - 1; rr >= 0; --rr) {
           const T xr = lane_bcast(x, rr);
-          if (lane < rr) x = fma(-dtile[lane * kSLd + rr], xr, x);   // L(d0+rr, d0+lane)
+          if (lane < rr) x = fma(-dl[rr], xr, x);                    // L(d0+rr, d0+lane)
         }
       }
-      if (d0 + lane < n) st_coh_t(&Y[(int64_t)(d0 + lane) + (int64_t)q * ldy], x);
+      if (d0 + lane < n) Y[(int64_t)(d0 + lane) + (int64_t)q * ldy] = x;
+      box_put(&a.box[(((size_t)b * kSolveRhs + q) * kSB + lane) * 2], d0 + lane < n ? x : T(0), a.stamp);
     }
-    wait_stores();
-    __syncthreads();
-    if (tid == 0) st_coh(&a.flag[b], 1);
+    __syncthreads();                               // part and dtile are reused by the next block
   }
 }
 
@@ -383,13 +429,22 @@ hipError_t launch_solve_tri(const SolveTriArgs& a, hipStream_t s) {
   return hipLaunchCooperativeKernel(k, dim3(grid), dim3(kSThreads), args, 0, s);
 }
 
+// Stamps of the mailbox words: a process-wide counter that skips 0 (zeroed
+// memory never validates).
+unsigned next_stamp() {
+  static std::atomic<unsigned> counter{0};
+  unsigned v;
+  do { v = counter.fetch_add(1) + 1; } while (v == 0);
+  return v;
+}
+
 template <typename T>
 hipError_t launch_solve(int n, const T* A, int64_t lda, const int* ipiv, int nrhs, T* B, int64_t ldb,
                         const SolveWork& w, hipStream_t s) {
   hipError_t e;
   {
     const int gb = (n + 255) / 256;
-    hipLaunchKernelGGL(solve_flags_kernel, dim3((2 * n + 255) / 256), dim3(256), 0, s, w.cnt, 2 * n);
+    hipLaunchKernelGGL(zero_ints_kernel, dim3((2 * n + 255) / 256), dim3(256), 0, s, w.cnt, 2 * n);
     hipLaunchKernelGGL(perm_count_kernel, dim3(gb), dim3(256), 0, s, n, ipiv, w.cnt);
     hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(1024), 0, s, n, w.cnt, w.off);
     hipLaunchKernelGGL(perm_scatter_kernel, dim3(gb), dim3(256), 0, s, n, ipiv, w.off, w.cnt + n, w.list);
@@ -408,16 +463,16 @@ hipError_t launch_solve(int n, const T* A, int64_t lda, const int* ipiv, int nrh
     T* Bq = B + (int64_t)q0 * ldb;
     hipLaunchKernelGGL(solve_gather_kernel<T>, dim3((n + 255) / 256, nr), dim3(256), 0, s, n, nr, w.perm, Bq, ldb,
                        Y, w.ldy);
-    hipLaunchKernelGGL(solve_flags_kernel, dim3((2 * nblk + 255) / 256), dim3(256), 0, s, w.flags, 2 * nblk);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     SolveTriArgs ta{};
     ta.A = A; ta.lda = lda; ta.n = n; ta.nblk = nblk; ta.Y = Y; ta.ldy = w.ldy; ta.nr = nr;
-    ta.flag = w.flags; ta.status = w.status;
+    ta.box = w.box; ta.status = w.status;
+    ta.stamp = next_stamp();
     if ((e = launch_solve_tri<T, false>(ta, s)) != hipSuccess) return e;
     hipLaunchKernelGGL(solve_tridiag_kernel<T>, dim3(1), dim3(128), 0, s, n, nr, alpha, ralpha, Y, W, w.ldy);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     ta.Y = W;
-    ta.flag = w.flags + nblk;
+    ta.stamp = next_stamp();
     if ((e = launch_solve_tri<T, true>(ta, s)) != hipSuccess) return e;
     hipLaunchKernelGGL(solve_scatter_kernel<T>, dim3((n + 255) / 256, nr), dim3(256), 0, s, n, nr, w.perm, W, w.ldy,
                        Bq, ldb);
