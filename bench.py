@@ -9,9 +9,12 @@ device copy (outside the timed events: the factorization works in place).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--nb 128]
                        [--n 16384] [--dtype f64|f32] [--no-cpu-baseline]
-                       [--workload factor|batched]
+                       [--workload factor|batched|pfaffian|solve] [--nrhs R]
 Prints one JSON line.  `--workload batched` instead times the batched path
-(8192 independent n=64 matrices, factors + Pfaffians) against HBM bandwidth.
+(8192 independent n=64 matrices, factors + Pfaffians) against HBM bandwidth;
+`--workload pfaffian` the Pfaffian by the even column steps alone;
+`--workload solve` the solve X x = b with the factors (R right-hand sides)
+against HBM bandwidth.
 """
 from __future__ import annotations
 
@@ -40,7 +43,8 @@ def parse():
     ap.add_argument("--seed", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--workload", choices=["factor", "batched", "pfaffian"], default="factor")
+    ap.add_argument("--workload", choices=["factor", "batched", "pfaffian", "solve"], default="factor")
+    ap.add_argument("--nrhs", type=int, default=1)
     ap.add_argument("--batch", type=int, default=8192)
     return ap.parse_args()
 
@@ -293,6 +297,102 @@ def run_pfaffian(args):
     print(json.dumps(out), flush=True)
 
 
+def run_solve(args):
+    """Solve X x = b with the factors of the headline matrix (ltlt_solve):
+    factor once (untimed), then time the solve of nrhs right-hand sides.
+    HBM-bound for few right-hand sides: the algorithmic bytes are two reads
+    of the strict lower triangle of L (forward and backward substitution)
+    plus one read and one write of B."""
+    import numpy as np
+    import torch
+
+    import paper_2005_06410_amd as lt
+    import synth
+
+    dev = torch.device("cuda:0")
+    n, nb, nrhs = args.n, args.nb, args.nrhs
+    np_dt = np.float64 if args.dtype == "f64" else np.float32
+    X = synth.skew_gauss(n, args.seed).astype(np_dt)
+    flat = torch.from_numpy(synth.to_colmajor(X).ravel()).to(dev)
+    A = flat.as_strided((n, n), (1, n))
+    ipiv = lt.factor(A, nb=nb)
+    rhs = synth.rng_for(args.seed + 1).standard_normal((n, nrhs)).astype(np_dt)
+    b0 = torch.from_numpy(np.asfortranarray(rhs)).to(dev).t().contiguous().t()
+    B = b0.clone().t().contiguous().t()
+    stream = torch.cuda.current_stream(dev)
+
+    def step():
+        B.copy_(b0)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        lt.solve(A, ipiv, B)
+        e1.record(stream)
+        return e0, e1
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    lt.device_status()
+    evs = [step() for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    lt.device_status()
+    ms_step = sum(a.elapsed_time(b) for a, b in evs) / len(evs)
+    esz = 8 if args.dtype == "f64" else 4
+    alg_bytes = 2 * esz * n * (n - 1) / 2 + 2 * esz * n * nrhs + 4 * n
+    gbs = alg_bytes / (ms_step * 1e-3) / 1e9
+    out = {
+        "metric": f"solve X x = b with the LTL^T factors, n={n} {args.dtype}, {nrhs} right-hand side(s): "
+                  "GB/s of algorithmic HBM bytes",
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": args.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": f"x = X^-1 b from the factors of one dense skew-symmetric n={n} {args.dtype} matrix "
+                        f"(strict upper iid N(0,1), seed {args.seed}), {nrhs} Gaussian right-hand side(s)",
+            "n": n,
+            "nrhs": nrhs,
+            "parallelism": "single GPU",
+        },
+        "roofline": {
+            "kernel": "solve_tri_kernel (forward + backward substitution)",
+            "bound": "hbm",
+            "achieved": round(gbs, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(gbs / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "algorithmic_bytes": alg_bytes,
+        },
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        from threadpoolctl import threadpool_limits
+        packed = np.tril(flat.cpu().numpy().reshape(n, n).T, -1)
+        piv = ipiv.cpu().numpy()
+        with threadpool_limits(limits=1):
+            t0 = time.perf_counter()
+            oracle.solve(packed, piv, rhs)
+            dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {
+            "value": round(alg_bytes / dt / 1e9, 4),
+            "unit": "GB/s",
+            "cores": 1,
+            "kind": "oracle",
+            "sample": f"one full solve of the same system ({dt:.1f} s, one BLAS thread; includes the oracle's "
+                      "unpacking of L and T)",
+        }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -315,6 +415,9 @@ def main():
         return
     if args.workload == "pfaffian":
         run_pfaffian(args)
+        return
+    if args.workload == "solve":
+        run_solve(args)
         return
     dev = torch.device("cuda:0")
     n, nb = args.n, args.nb

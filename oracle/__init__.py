@@ -32,7 +32,7 @@ Every floating-point routine runs in the precision of its input (fp64, or fp32
 for fp32 parity); the Pfaffian accumulates in fp64.
 
 Pins (tests that tie these functions to facts outside themselves) live in
-``tests/test_oracle_pins.py``; no function here is unpinned.
+``tests/test_oracle_pins*.py``; no function here is unpinned.
 """
 from __future__ import annotations
 
