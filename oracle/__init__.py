@@ -27,6 +27,10 @@ What it computes (textbook definitions, written out plainly):
   permutation, forward substitution with L, the two recurrences of the skew
   tridiagonal T, backward substitution with L^T, inverse permutation
   (triangular solves by scipy, the recurrences written out).
+* complex skew-symmetric X (X^T = -X, complex128 / complex64): ``ltlt`` and
+  ``pfaffian`` take the same steps in scalar C with the complex arithmetic
+  written out (``ltlt_oracle_complex.h``): pivot by |re| + |im|, Smith's
+  quotient; the Pfaffian comes back as (log|Pf|, phase Pf/|Pf|).
 
 Every floating-point routine runs in the precision of its input (fp64, or fp32
 for fp32 parity); the Pfaffian accumulates in fp64.
@@ -46,6 +50,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "ltlt_oracle.c")
 _HDR = os.path.join(_HERE, "ltlt_oracle_body.h")
+_HDR_C = os.path.join(_HERE, "ltlt_oracle_complex.h")
 _LIB = os.path.join(_HERE, "libltlt_oracle.so")
 _lock = threading.Lock()
 _lib = None
@@ -56,7 +61,8 @@ GCC_FLAGS = ["-O2", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared", "
 def build(force: bool = False) -> str:
     """Compile the C oracle with gcc (no FMA contraction, no reassociation)."""
     stale = (not os.path.exists(_LIB)
-             or os.path.getmtime(_LIB) < max(os.path.getmtime(_SRC), os.path.getmtime(_HDR)))
+             or os.path.getmtime(_LIB) < max(os.path.getmtime(_SRC), os.path.getmtime(_HDR),
+                                             os.path.getmtime(_HDR_C)))
     if force or stale:
         tmp = _LIB + ".tmp%d" % os.getpid()
         subprocess.check_call(["gcc", *GCC_FLAGS, _SRC, "-o", tmp, "-lm"])
@@ -72,12 +78,14 @@ def _load():
                 build()
             lib = ctypes.CDLL(_LIB)
             i64, p = ctypes.c_int64, ctypes.c_void_p
-            for name in ("oracle_ltlt_f64", "oracle_ltlt_f32"):
+            for name in ("oracle_ltlt_f64", "oracle_ltlt_f32", "oracle_ltlt_c128", "oracle_ltlt_c64"):
                 getattr(lib, name).argtypes = [i64, p, i64, p, i64]
                 getattr(lib, name).restype = None
-            lib.oracle_swap_f64.argtypes = [i64, p, i64, i64, i64]
-            lib.oracle_swap_f64.restype = None
-            for name in ("oracle_pfaffian_f64", "oracle_pfaffian_f32"):
+            for name in ("oracle_swap_f64", "oracle_swap_c128"):
+                getattr(lib, name).argtypes = [i64, p, i64, i64, i64]
+                getattr(lib, name).restype = None
+            for name in ("oracle_pfaffian_f64", "oracle_pfaffian_f32", "oracle_pfaffian_c128",
+                         "oracle_pfaffian_c64"):
                 getattr(lib, name).argtypes = [i64, p, i64, p, p, p]
                 getattr(lib, name).restype = None
             for name in ("oracle_pfaffian_direct_f64", "oracle_pfaffian_direct_f32"):
@@ -96,7 +104,11 @@ def _sfx(dtype) -> str:
         return "f64"
     if dt == np.float32:
         return "f32"
-    raise TypeError("oracle supports float64 and float32 only")
+    if dt == np.complex128:
+        return "c128"
+    if dt == np.complex64:
+        return "c64"
+    raise TypeError("oracle supports float64, float32, complex128 and complex64 only")
 
 
 def ltlt_colmajor(buf: np.ndarray, n: int, nsteps: int = -1):
@@ -129,13 +141,20 @@ def ltlt(X: np.ndarray, nsteps: int = -1):
 
 
 def pfaffian_packed(packed: np.ndarray, ipiv: np.ndarray):
-    """(log|Pf(X)|, sign) from the packed factors (row/col indexed n x n)."""
+    """(log|Pf(X)|, sign) from the packed factors (row/col indexed n x n).
+    Complex factors give (log|Pf(X)|, phase) with phase = Pf / |Pf| a Python
+    complex (0 when Pf = 0)."""
     lib = _load()
     n = packed.shape[0]
     buf = np.ascontiguousarray(packed.T)     # column-major image
     logabs = ctypes.c_double(0.0)
-    sign = ctypes.c_int32(0)
     ip = np.ascontiguousarray(ipiv, dtype=np.int32)
+    if np.iscomplexobj(packed):
+        ph = np.zeros(2, dtype=np.float64)
+        getattr(lib, "oracle_pfaffian_" + _sfx(packed.dtype))(n, buf.ctypes.data, n, ip.ctypes.data,
+                                                              ctypes.byref(logabs), ph.ctypes.data)
+        return float(logabs.value), complex(ph[0], ph[1])
+    sign = ctypes.c_int32(0)
     fn = getattr(lib, "oracle_pfaffian_" + _sfx(packed.dtype))
     fn(n, buf.ctypes.data, n, ip.ctypes.data, ctypes.byref(logabs), ctypes.byref(sign))
     return float(logabs.value), int(sign.value)
@@ -196,11 +215,13 @@ def ltlt_batched(Xs: np.ndarray):
 
 def swap_indices(X: np.ndarray, r: int, p: int) -> np.ndarray:
     """Q X Q^T for the transposition (r p), through the oracle's lower-storage
-    exchange; returns the full skew matrix rebuilt from the strict lower part."""
+    exchange; returns the full skew matrix rebuilt from the strict lower part
+    (fp64, or complex128 for complex X)."""
     lib = _load()
     n = X.shape[0]
-    buf = np.ascontiguousarray(X.T).astype(np.float64)
-    lib.oracle_swap_f64(n, buf.ctypes.data, n, r, p)
+    dt = np.complex128 if np.iscomplexobj(X) else np.float64
+    buf = np.ascontiguousarray(X.T).astype(dt)
+    getattr(lib, "oracle_swap_" + _sfx(dt))(n, buf.ctypes.data, n, r, p)
     low = np.tril(buf.T, -1)
     return low - low.T
 
@@ -214,7 +235,7 @@ def unpack(packed: np.ndarray, ipiv: np.ndarray):
     identity ordering, so (P X P^T)[i, j] = X[perm[i], perm[j]].
     """
     n = packed.shape[0]
-    dt = np.float64
+    dt = np.complex128 if np.iscomplexobj(packed) else np.float64
     L = np.eye(n, dtype=dt)
     T = np.zeros((n, n), dtype=dt)
     for k in range(n - 1):
@@ -278,8 +299,9 @@ def residual(X: np.ndarray, packed: np.ndarray, ipiv: np.ndarray) -> float:
     n = X.shape[0]
     if n == 0:
         return 0.0
-    L, T, perm = unpack(packed.astype(np.float64), ipiv)
-    Xd = X.astype(np.float64)
+    wide = np.complex128 if np.iscomplexobj(X) else np.float64
+    L, T, perm = unpack(packed.astype(wide), ipiv)
+    Xd = X.astype(wide)
     PXP = Xd[np.ix_(perm, perm)]
     R = PXP - L @ T @ L.T
     eps = np.finfo(X.dtype).eps

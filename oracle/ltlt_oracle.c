@@ -7,6 +7,9 @@
  * the GPU library; only the tests, the smoke check and the benchmark's CPU
  * baseline may load it.
  *
+ * Complex matrices (complex skew-symmetric, X^T = -X) use the same steps
+ * with written-out complex arithmetic (ltlt_oracle_complex.h).
+ *
  * Build: gcc -O2 -ffp-contract=off -fno-fast-math -shared -fPIC
  * (no contraction into FMA, no reassociation: every operation rounds once,
  * in the order written).
@@ -33,6 +36,22 @@
 #include "ltlt_oracle_body.h"
 #undef REAL
 #undef SFX
+#undef FABS
+
+#define REAL double
+#define CSFX _c128
+#define FABS fabs
+#include "ltlt_oracle_complex.h"
+#undef REAL
+#undef CSFX
+#undef FABS
+
+#define REAL float
+#define CSFX _c64
+#define FABS fabsf
+#include "ltlt_oracle_complex.h"
+#undef REAL
+#undef CSFX
 #undef FABS
 
 /* Exported entry points (ctypes). */
@@ -80,3 +99,21 @@ void oracle_ltlt_batched_f32(int64_t n, int64_t batch, float* A, int64_t lda, in
         pfaffian_f32(n, A + b * strideA, lda, ipiv + b * strideIpiv, logabs + b, sign + b);
     }
 }
+
+/* Complex: A holds (re, im) pairs, lda in complex elements. */
+void oracle_ltlt_c128(int64_t n, void* A, int64_t lda, int32_t* ipiv, int64_t nsteps)
+{ ltlt_c128(n, (cplx_c128*)A, lda, ipiv, nsteps); }
+
+void oracle_ltlt_c64(int64_t n, void* A, int64_t lda, int32_t* ipiv, int64_t nsteps)
+{ ltlt_c64(n, (cplx_c64*)A, lda, ipiv, nsteps); }
+
+void oracle_swap_c128(int64_t n, void* A, int64_t lda, int64_t r, int64_t p)
+{ cswap_indices_c128(n, (cplx_c128*)A, lda, r, p); }
+
+void oracle_pfaffian_c128(int64_t n, const void* A, int64_t lda, const int32_t* ipiv,
+                          double* logabs, double* phase)
+{ pfaffian_c128(n, (const cplx_c128*)A, lda, ipiv, logabs, phase); }
+
+void oracle_pfaffian_c64(int64_t n, const void* A, int64_t lda, const int32_t* ipiv,
+                         double* logabs, double* phase)
+{ pfaffian_c64(n, (const cplx_c64*)A, lda, ipiv, logabs, phase); }

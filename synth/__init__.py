@@ -55,6 +55,15 @@ def skew_gauss(n: int, seed: int, dtype=np.float64) -> np.ndarray:
     return X.astype(dtype, copy=False)
 
 
+def skew_gauss_complex(n: int, seed: int, dtype=np.complex128) -> np.ndarray:
+    """Complex skew-symmetric (X^T = -X, no conjugation): strict-upper real and
+    imaginary parts iid N(0,1); lower = -upper; zero diagonal."""
+    rng = rng_for(seed)
+    G = rng.standard_normal((2, n, n))
+    X = skew_from_upper(G[0] + 1j * G[1])
+    return X.astype(dtype, copy=False)
+
+
 def skew_graded(n: int, seed: int, dtype=np.float64, decades: float = 3.0) -> np.ndarray:
     """Strict-upper entries N(0,1) * 10**U(-decades, decades), elementwise.
 

@@ -27,8 +27,9 @@ def pf_closed4(X) -> float:
 
 
 def pf_matchings(X) -> float:
-    """Signed sum over perfect matchings (recursive first-row expansion)."""
-    X = np.asarray(X, dtype=np.float64)
+    """Signed sum over perfect matchings (recursive first-row expansion);
+    complex input gives a complex sum."""
+    X = np.asarray(X, dtype=np.complex128 if np.iscomplexobj(X) else np.float64)
 
     def rec(idx):
         if not idx:
@@ -87,13 +88,16 @@ def ltlt_dense(X):
     L = P (M_last ... M_0 P_0^T ... )^{-1}-style accumulation: here simply
     by carrying each multiplier column through the later exchanges.
     """
-    A = np.array(X, dtype=np.float64)
+    cplx = np.iscomplexobj(X)
+    dt = np.complex128 if cplx else np.float64
+    A = np.array(X, dtype=dt)
     n = A.shape[0]
     ipiv = np.arange(n)
     cols = []                      # multiplier vectors, full length n
     alpha = []
     for k in range(max(n - 2, 0)):
-        col = np.abs(A[k + 1:, k])
+        # complex: the magnitude of the BLAS complex i_amax, |re| + |im|
+        col = np.abs(A[k + 1:, k].real) + np.abs(A[k + 1:, k].imag) if cplx else np.abs(A[k + 1:, k])
         p = k + 1 + int(np.argmax(col))            # argmax returns the first maximum
         if col.max() == 0:
             p = k + 1
@@ -105,16 +109,16 @@ def ltlt_dense(X):
             c[[k + 1, p]] = c[[p, k + 1]]
         a = A[k + 1, k]
         alpha.append(a)
-        l = np.zeros(n)
+        l = np.zeros(n, dtype=dt)
         if a != 0:
             l[k + 2:] = A[k + 2:, k] / a
         cols.append(l)
-        M = np.eye(n)
+        M = np.eye(n, dtype=dt)
         M[k + 2:, k + 1] = -l[k + 2:]
         A = M @ A @ M.T
     if n >= 2:
         alpha.append(A[n - 1, n - 2])
-    L = np.eye(n)
+    L = np.eye(n, dtype=dt)
     for k, l in enumerate(cols):
         L[k + 2:, k + 1] = l[k + 2:]
     return np.array(alpha), ipiv, L, A
