@@ -45,9 +45,14 @@
 extern "C" {
 #endif
 
-/* Element types (argument `dtype`). */
+/* Element types (argument `dtype`).  The complex types hold (re, im) pairs
+ * (the layout of C99 / numpy / torch complex numbers); lda counts complex
+ * elements.  Only ltlt_factor, ltlt_factor_nb and ltlt_pfaffian_complex take
+ * them. */
 #define LTLT_F64 0
 #define LTLT_F32 1
+#define LTLT_C128 2
+#define LTLT_C64 3
 
 #define LTLT_OK 0
 #define LTLT_ERR_HIP_BASE (-1000)      /* returned as LTLT_ERR_HIP_BASE - (int)hipError_t */
@@ -70,20 +75,31 @@ extern "C" {
  *              final pivot order.  The strict upper triangle is never read or
  *              written.
  *   lda    (3) lda >= max(1, n).
- *   dtype  (4) LTLT_F64 or LTLT_F32 (element type of A; arithmetic in it).
+ *   dtype  (4) LTLT_F64 or LTLT_F32 (element type of A; arithmetic in it),
+ *              or LTLT_C128 / LTLT_C64 for a complex skew-symmetric X
+ *              (X^T = -X, a transpose without conjugation; the paper does
+ *              not treat this case): the same steps in complex
+ *              arithmetic, the pivot being the first index of the largest
+ *              |Re X(r,k)| + |Im X(r,k)| (the magnitude of the BLAS complex
+ *              i_amax) and the multipliers Smith quotients; same storage and
+ *              outputs with complex elements.  The library works on a split
+ *              copy (real and imaginary planes, 2 n^2 components of
+ *              workspace) and writes the strict lower triangle back at the end.
  *   ipiv   (5) device int32[n]: 0-based exchanges in LAPACK laswp order:
  *              ipiv[0] = 0, ipiv[k+1] = the index exchanged with k+1 at step
  *              k (>= k+1), ipiv[n-1] = n-1.  P applies (i, ipiv[i]) for
  *              i = 0..n-1 in increasing order.
  *   stream (6) HIP stream.
- * Uses the default panel width (128).
+ * Uses the default panel width (128 real, 64 complex).
  */
 int ltlt_factor(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, hipStream_t stream);
 
 /*
  * ltlt_factor_nb -- as ltlt_factor with an explicit panel width.
- *   nb (6) number of column steps per block, 1 <= nb <= 256; the trailing
- *          update of each block is one rank-(nb+1) lower-triangular product.
+ *   nb (6) number of column steps per block, 1 <= nb <= 256 (complex:
+ *          1 <= nb <= 128); the trailing update of each block is one
+ *          rank-(nb+1) lower-triangular product (complex: one real product of
+ *          depth 2(nb+1) per plane).
  *   stream is argument 7.
  */
 int ltlt_factor_nb(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, int64_t nb,
@@ -100,6 +116,22 @@ int ltlt_factor_nb(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, in
  */
 int ltlt_pfaffian(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* ipiv,
                   double* logabs, int32_t* sign, hipStream_t stream);
+
+/*
+ * ltlt_pfaffian_complex -- log|Pf(X)| and the phase Pf(X)/|Pf(X)| from the
+ * output of ltlt_factor for a complex X:
+ *        Pf(X) = det(P) * prod_j (-alpha_{2j}),  det(P) = (-1)^(#exchanges).
+ *   n, A, lda, dtype, ipiv (1-5) as returned by ltlt_factor with dtype
+ *              LTLT_C128 or LTLT_C64 (read only; other dtypes: -4).
+ *   logabs (6) device double[1]: sum_j log|alpha_{2j}| in fp64.
+ *   phase  (7) device double[2]: (re, im) of the unit complex number
+ *              det(P) prod_j (-alpha_{2j})/|alpha_{2j}|, in fp64.
+ *   stream (8).
+ * n = 0 gives logabs 0, phase 1.  Odd n, or any alpha_{2j} = 0, gives
+ * logabs = -inf and phase 0.
+ */
+int ltlt_pfaffian_complex(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* ipiv,
+                          double* logabs, double* phase, hipStream_t stream);
 
 /*
  * ltlt_pfaffian_direct -- Pf(X) without the factors: the pivoted reduction

@@ -38,7 +38,7 @@ __all__ = [
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libltlt.so")
-F64, F32 = 0, 1
+F64, F32, C128, C64 = 0, 1, 2, 3
 BATCHED_MAX_N = 64
 _lock = threading.Lock()
 _lib = None
@@ -50,6 +50,8 @@ _SYMBOLS = {
                         ctypes.c_int64, ctypes.c_void_p], ctypes.c_int),
     "ltlt_pfaffian": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
+    "ltlt_pfaffian_complex": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
+                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "ltlt_factor_batched": ([ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
                              ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
                              ctypes.c_void_p], ctypes.c_int),
@@ -120,7 +122,11 @@ def _dtype_code(t) -> int:
         return F64
     if t.dtype == torch.float32:
         return F32
-    raise TypeError("only float64 and float32 are supported")
+    if t.dtype == torch.complex128:
+        return C128
+    if t.dtype == torch.complex64:
+        return C64
+    raise TypeError("only float64, float32, complex128 and complex64 are supported")
 
 
 def _stream_ptr(device) -> int:
@@ -146,11 +152,13 @@ def _colmajor_lda(A) -> int:
 
 
 def factor(A, ipiv=None, nb: int | None = None):
-    """In-place P X P^T = L T L^T of the column-major skew matrix ``A``.
+    """In-place P X P^T = L T L^T of the column-major skew matrix ``A``
+    (float64, float32, or complex128 / complex64 for a complex X with
+    X^T = -X).
 
     Returns the int32 pivot tensor (0-based, LAPACK laswp order).  On return
     A's strict lower triangle holds alpha_k at (k+1, k) and L(r, k+1) at (r, k);
-    its strict upper triangle is scratch (unspecified)."""
+    its strict upper triangle is never touched."""
     torch = _torch()
     _require_gpu(A)
     lda = _colmajor_lda(A)
@@ -170,14 +178,21 @@ def factor(A, ipiv=None, nb: int | None = None):
 
 
 def pfaffian(A, ipiv):
-    """(logabs, sign) device tensors of Pf(X) from ``factor``'s output."""
+    """(logabs, sign) device tensors of Pf(X) from ``factor``'s output; for a
+    complex A, (logabs, phase) with phase = Pf/|Pf| a complex128 tensor."""
     torch = _torch()
     _require_gpu(A)
     lda = _colmajor_lda(A)
     n = A.shape[0]
     logabs = torch.empty(1, dtype=torch.float64, device=A.device)
-    sign = torch.empty(1, dtype=torch.int32, device=A.device)
     lib = load()
+    if A.is_complex():
+        phase = torch.empty((1, 2), dtype=torch.float64, device=A.device)
+        code = lib.ltlt_pfaffian_complex(n, A.data_ptr(), lda, _dtype_code(A), ipiv.data_ptr(), logabs.data_ptr(),
+                                         phase.data_ptr(), _stream_ptr(A.device))
+        _check("ltlt_pfaffian_complex", code)
+        return logabs, torch.view_as_complex(phase)
+    sign = torch.empty(1, dtype=torch.int32, device=A.device)
     code = lib.ltlt_pfaffian(n, A.data_ptr(), lda, _dtype_code(A), ipiv.data_ptr(), logabs.data_ptr(),
                              sign.data_ptr(), _stream_ptr(A.device))
     _check("ltlt_pfaffian", code)

@@ -16,6 +16,8 @@ using namespace ltlt;
 namespace {
 
 constexpr int kDefaultNb = 128;
+constexpr int kDefaultComplexNb = 64;           // complex: 32 register slots per lane, two lanes per row
+constexpr int kMaxComplexNb = 128;
 constexpr int64_t kMaxOrder = (1 << 21) - 1;   // exchange records pack indices in 21 bits
 constexpr size_t kLdsBudget = 160 * 1024 - 2048;   // dynamic LDS a panel workgroup may use
 
@@ -327,6 +329,146 @@ int pfaffian_direct_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, 
 }
 
 bool bad_dtype(int d) { return d != LTLT_F64 && d != LTLT_F32; }
+bool is_complex(int d) { return d == LTLT_C128 || d == LTLT_C64; }
+
+// Complex factorization: X is split into real and imaginary planes
+// (workspace, leading dimension ldw), every block runs the complex panel,
+// then each plane's trailing update as one real product of depth 2(bw+1)
+// (Re C += [Lr Li][Btr -Bti]^T, Im C += [Li Lr][Btr Bti]^T) with the real
+// update kernel, and the per-plane commit; the final row order is applied to
+// each plane and the planes are merged back into A.  T is the component type.
+template <typename T>
+int factor_complex_impl(int64_t n64, void* A, int64_t lda, int32_t* ipiv, int nb, hipStream_t s) {
+  if (n64 == 0) return 0;
+  if (n64 >= kMaxOrder) return LTLT_ERR_UNSUPPORTED;
+  const int n = (int)n64;
+  const int nsteps = std::max(n - 2, 0);
+  const int nblk = nsteps > 0 ? (nsteps + nb - 1) / nb : 0;
+  const int bw0 = std::min(nb, std::max(nsteps, 1));
+  const int R = cpanel_rows(bw0);
+  int Pmax = 1;
+  if (nblk > 0) {
+    const size_t lds = cpanel_lds_bytes<T>(bw0);
+    if (lds > kLdsBudget) return LTLT_ERR_UNSUPPORTED;
+    Pmax = (n - 1 + R - 1) / R;
+    const int cap = cpanel_max_blocks<T>(bw0, lds);
+    if (cap <= 0 || Pmax > cap) return LTLT_ERR_UNSUPPORTED;
+  }
+
+  const int64_t ldw = ((int64_t)n + 63) / 64 * 64;
+  const int K0 = nb + 1;
+  const int c_end = nblk >= 2 ? (nblk - 1) * nb : 0;
+  Carve cv;
+  const size_t o_Pr = cv.take<T>((size_t)ldw * n);
+  const size_t o_Pi = cv.take<T>((size_t)ldw * n);
+  const size_t o_LL = cv.take<T>((size_t)ldw * 3 * K0);
+  const size_t o_BA = cv.take<T>((size_t)ldw * 2 * K0);
+  const size_t o_BB = cv.take<T>((size_t)ldw * 2 * K0);
+  const size_t o_Gr = cv.take<T>((size_t)ldw * nb);
+  const size_t o_Gi = cv.take<T>((size_t)ldw * nb);
+  const size_t o_Vr = cv.take<T>((size_t)ldw);
+  const size_t o_Vi = cv.take<T>((size_t)ldw);
+  const size_t o_ar = cv.take<T>((size_t)nb);
+  const size_t o_ai = cv.take<T>((size_t)nb);
+  const size_t o_T = cv.take<int>((size_t)std::max(nblk, 1) * n);
+  const size_t o_GC = cv.take<int>((size_t)std::max(nblk, 1) * n);
+  const int nrec = Pmax;
+  const size_t o_rec = cv.take<uint64_t>((size_t)2 * kRecStride * nrec);
+  const size_t o_st = cv.take<T>(perm_stage_elems<T>(n, c_end));
+
+  void* ws = nullptr;
+  int* status = nullptr;
+  hipError_t e = workspace(cv.off, &ws, &status);
+  if (e != hipSuccess) return hip_err(e);
+  char* base = static_cast<char*>(ws);
+  T* Pr = reinterpret_cast<T*>(base + o_Pr);
+  T* Pi = reinterpret_cast<T*>(base + o_Pi);
+  T* LL = reinterpret_cast<T*>(base + o_LL);
+  T* BA = reinterpret_cast<T*>(base + o_BA);
+  T* BB = reinterpret_cast<T*>(base + o_BB);
+  T* Gr = reinterpret_cast<T*>(base + o_Gr);
+  T* Gi = reinterpret_cast<T*>(base + o_Gi);
+  T* Vr = reinterpret_cast<T*>(base + o_Vr);
+  T* Vi = reinterpret_cast<T*>(base + o_Vi);
+  T* alr = reinterpret_cast<T*>(base + o_ar);
+  T* ali = reinterpret_cast<T*>(base + o_ai);
+  int* Tblk = reinterpret_cast<int*>(base + o_T);
+  int* Gc = reinterpret_cast<int*>(base + o_GC);
+  uint64_t* rec = reinterpret_cast<uint64_t*>(base + o_rec);
+  T* stage = reinterpret_cast<T*>(base + o_st);
+
+  {
+    ProfScope ps(3, 0.0, s);
+    e = launch_init(ipiv, n, status, s);
+    if (e == hipSuccess && nblk > 0) e = launch_rec_init(rec, nrec, s);
+    if (e == hipSuccess) e = launch_cplx_split<T>(n, A, lda, Pr, Pi, ldw, s);
+  }
+  if (e != hipSuccess) return hip_err(e);
+
+  for (int J = 0; J < nblk; ++J) {
+    const int j = J * nb;
+    const int bw = std::min(nb, nsteps - j);
+    const int K = bw + 1;
+    const int m = n - j - 1;
+    CPanelArgs ca{};
+    PanelArgs& pa = ca.b;
+    pa.A = Pr; pa.lda = ldw; pa.n = n; pa.j = j; pa.bw = bw;
+    pa.R = cpanel_rows(bw);
+    pa.P = (m + pa.R - 1) / pa.R;
+    pa.nrec = nrec;
+    pa.G = Gr; pa.ldw = ldw; pa.alpha = alr;
+    pa.perm = Tblk + (int64_t)J * n;
+    pa.ipiv = ipiv;
+    pa.rec = rec;
+    pa.status = status;
+    ca.Ai = Pi; ca.Gi = Gi; ca.Vr = Vr; ca.Vi = Vi;
+    ca.LL = LL; ca.BtA = BA; ca.BtB = BB; ca.alpha_i = ali;
+    {
+      ProfScope ps(0, 0.0, s);
+      e = launch_cpanel<T>(ca, cpanel_lds_bytes<T>(bw), s);
+    }
+    if (e != hipSuccess) return hip_err(e);
+
+    const int i0 = j + bw + 1;
+    const int m2 = n - i0;
+    if (m2 >= 2) {
+      for (int plane = 0; plane < 2; ++plane) {
+        UpdateArgs ua{};
+        ua.C = (plane == 0 ? Pr : Pi) + (int64_t)i0 + (int64_t)i0 * ldw;
+        ua.ldc = ldw;
+        ua.m = m2;
+        ua.perm = Tblk + (int64_t)J * n + i0;
+        ua.perm_base = i0;
+        ua.K = 2 * K;
+        ua.Lx = LL + (plane == 0 ? 0 : (int64_t)K * ldw) + bw;
+        ua.ldl = ldw;
+        ua.Bt = plane == 0 ? BA : BB;
+        ua.ldb = ldw;
+        ua.pad_row = 1;    // row bw + m2 = n - j - 1 < ldw of every operand column lies inside its column
+        ProfScope ps(1, 2.0 * (double)m2 * (double)m2 * (double)bw, s);   // depth 2 bw: half the complex work
+        e = launch_update<T>(ua, s);
+        if (e != hipSuccess) return hip_err(e);
+      }
+    }
+    {
+      ProfScope ps(2, 0.0, s);
+      e = launch_commit<T>(Pr, ldw, n, j, bw, LL, ldw, alr, s);
+      if (e == hipSuccess) e = launch_commit<T>(Pi, ldw, n, j, bw, LL + (int64_t)K * ldw, ldw, ali, s);
+    }
+    if (e != hipSuccess) return hip_err(e);
+  }
+
+  {
+    ProfScope ps(3, 0.0, s);
+    if (nblk >= 2) {
+      e = launch_perm_chain(Tblk, nb, nblk, n, Gc, s);
+      if (e == hipSuccess) e = launch_perm_apply<T>(Pr, ldw, n, Gc, nb, c_end, stage, s);
+      if (e == hipSuccess) e = launch_perm_apply<T>(Pi, ldw, n, Gc, nb, c_end, stage, s);
+    }
+    if (e == hipSuccess) e = launch_cplx_merge<T>(n, A, lda, Pr, Pi, ldw, s);
+  }
+  return e == hipSuccess ? 0 : hip_err(e);
+}
 
 }  // namespace
 
@@ -336,16 +478,32 @@ int ltlt_factor_nb(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, in
   if (n < 0 || n > (int64_t)INT32_MAX / 2) return -1;
   if (A == nullptr && n > 0) return -2;
   if (lda < std::max<int64_t>(1, n)) return -3;
-  if (bad_dtype(dtype)) return -4;
+  if (bad_dtype(dtype) && !is_complex(dtype)) return -4;
   if (ipiv == nullptr && n > 0) return -5;
-  if (nb < 1 || nb > kMaxNb) return -6;
+  if (nb < 1 || nb > (is_complex(dtype) ? kMaxComplexNb : kMaxNb)) return -6;
   if (n == 0) return 0;
+  if (dtype == LTLT_C128) return factor_complex_impl<double>(n, A, lda, ipiv, (int)nb, stream);
+  if (dtype == LTLT_C64) return factor_complex_impl<float>(n, A, lda, ipiv, (int)nb, stream);
   if (dtype == LTLT_F64) return factor_impl<double>(n, static_cast<double*>(A), lda, ipiv, (int)nb, stream);
   return factor_impl<float>(n, static_cast<float*>(A), lda, ipiv, (int)nb, stream);
 }
 
 int ltlt_factor(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, hipStream_t stream) {
-  return ltlt_factor_nb(n, A, lda, dtype, ipiv, kDefaultNb, stream);
+  return ltlt_factor_nb(n, A, lda, dtype, ipiv, is_complex(dtype) ? kDefaultComplexNb : kDefaultNb, stream);
+}
+
+int ltlt_pfaffian_complex(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* ipiv, double* logabs,
+                          double* phase, hipStream_t stream) {
+  if (n < 0 || n > (int64_t)INT32_MAX / 2) return -1;
+  if (A == nullptr && n > 0) return -2;
+  if (lda < std::max<int64_t>(1, n)) return -3;
+  if (!is_complex(dtype)) return -4;
+  if (ipiv == nullptr && n > 0) return -5;
+  if (logabs == nullptr) return -6;
+  if (phase == nullptr) return -7;
+  hipError_t e = dtype == LTLT_C128 ? launch_cpfaffian<double>((int)n, A, lda, ipiv, logabs, phase, stream)
+                                    : launch_cpfaffian<float>((int)n, A, lda, ipiv, logabs, phase, stream);
+  return e == hipSuccess ? 0 : hip_err(e);
 }
 
 int ltlt_pfaffian(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* ipiv, double* logabs,

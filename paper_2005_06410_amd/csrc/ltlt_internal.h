@@ -70,8 +70,33 @@ hipError_t launch_perm_chain(const int* Tblk, int nb, int nblk, int n, int* G, h
 template <typename T> int panel_max_blocks(int bw, size_t lds);
 int panel_rows(int bw);
 
-// Pfaffian-only path (even column steps): the pair panel and the commit of
-// its alphas.
+// Complex matrices are factored as two real planes (real and imaginary parts,
+// leading dimension ldw).  The complex panel writes its outputs so that each
+// plane's trailing update is one real product of depth 2K (K = bw + 1):
+//   Re C += [Lr Li] [Btr -Bti]^T,   Im C += [Li Lr] [Btr Bti]^T,
+// with LL = [Lr Li Lr] holding both left operands as column windows.
+struct CPanelArgs {
+  PanelArgs b;        // A, G, alpha: real planes / parts; PO and Bm unused
+  const void* Ai;     // imaginary plane of the matrix (ld b.lda)
+  void* Gi;           // imaginary plane of the multiplier copy G
+  void* Vr;           // pivot candidates' values by block-start index:
+  void* Vi;           //   V[idx - j - 1] (real and imaginary parts)
+  void* LL;           // [Lr | Li | Lr], K columns each, ld b.ldw, rows from j+1
+  void* BtA;          // [Btr | -Bti] for rows >= j+bw+1, ld b.ldw
+  void* BtB;          // [Btr |  Bti]
+  void* alpha_i;      // imaginary parts of alpha_{j+t}
+};
+int cpanel_rows(int bw);
+template <typename T> size_t cpanel_lds_bytes(int bw);
+template <typename T> int cpanel_max_blocks(int bw, size_t lds);
+template <typename T> hipError_t launch_cpanel(const CPanelArgs& a, size_t lds, hipStream_t s);
+template <typename T> hipError_t launch_cplx_split(int n, const void* A, int64_t lda, T* Pr, T* Pi, int64_t ldp,
+                                                   hipStream_t s);
+template <typename T> hipError_t launch_cplx_merge(int n, void* A, int64_t lda, const T* Pr, const T* Pi,
+                                                   int64_t ldp, hipStream_t s);
+template <typename T> hipError_t launch_cpfaffian(int n, const void* A, int64_t lda, const int* ipiv,
+                                                  double* logabs, double* phase, hipStream_t s);
+
 // Solve with the factors.
 constexpr int kSolveRhs = 8;                    // right-hand sides per pass
 struct SolveWork {
@@ -90,6 +115,8 @@ struct SolveWork {
 template <typename T> hipError_t launch_solve(int n, const T* A, int64_t lda, const int* ipiv, int nrhs, T* B,
                                               int64_t ldb, const SolveWork& w, hipStream_t s);
 
+// Pfaffian-only path (even column steps): the pair panel and the commit of
+// its alphas.
 int pair_panel_rows(int bw);                     // rows per pair-panel workgroup
 template <typename T> size_t pair_lds_bytes(int bw, int R);
 template <typename T> int pair_max_blocks(int bw, size_t lds);

@@ -14,6 +14,9 @@ Comparison rules (the reading of "parity" used throughout the GPU tests):
   near n = 1000 for Gaussian input).
 * log|Pf|: |diff| <= 1e-9 |ref| (fp64); sign equal.
 * residual ||P X P^T - L T L^T||_F / (n eps ||X||_F) <= 10.
+* complex128 / complex64 factors follow the same rules with complex
+  differences (|.| the modulus) and, for the near-tie, the pivot magnitude
+  |re| + |im| the reduction searches by.
 """
 from __future__ import annotations
 
@@ -23,7 +26,16 @@ import torch
 import oracle
 import synth
 
-TOL = {np.float64: 1e-10, np.float32: 1e-4}
+TOL = {np.float64: 1e-10, np.float32: 1e-4, np.complex128: 1e-10, np.complex64: 1e-4}
+
+
+def _wide(a):
+    return np.complex128 if np.iscomplexobj(a) else np.float64
+
+
+def _pivot_mag(v):
+    """Magnitude the pivot search compares: |x|, or |re| + |im| for complex."""
+    return np.abs(v.real) + np.abs(v.imag) if np.iscomplexobj(v) else np.abs(v)
 
 
 def device_colmajor(X: np.ndarray, lda: int | None = None, fill=0.0, dtype=None):
@@ -69,16 +81,17 @@ def compare_factors(X: np.ndarray, packed_gpu: np.ndarray, ipiv_gpu, dtype, ref=
     tol = TOL[np.dtype(dtype).type]
     tol_a = tol
     Xd = X.astype(dtype)
+    W = _wide(Xd)
     if ref is None:
         ref = oracle.ltlt(Xd)
     packed_ref, ipiv_ref = ref
-    if np.dtype(dtype) == np.float32 and n >= 3:
-        p64, i64 = oracle.ltlt(Xd.astype(np.float64))
+    if np.dtype(dtype) in (np.float32, np.complex64) and n >= 3:
+        p64, i64 = oracle.ltlt(Xd.astype(W))
         if np.array_equal(i64, ipiv_ref):
             low = np.tril(np.ones((n, n), bool), -2)
             sub = np.arange(1, n), np.arange(n - 1)
-            d_l = np.abs(packed_ref[low].astype(np.float64) - p64[low]).max() if low.any() else 0.0
-            d_a = np.abs(packed_ref[sub].astype(np.float64) - p64[sub]).max() / np.abs(p64[sub]).max()
+            d_l = np.abs(packed_ref[low].astype(W) - p64[low]).max() if low.any() else 0.0
+            d_a = np.abs(packed_ref[sub].astype(W) - p64[sub]).max() / np.abs(p64[sub]).max()
             tol = max(tol, 2.0 * d_l)
             tol_a = max(tol_a, 2.0 * d_a)
     ipiv_gpu = np.asarray(ipiv_gpu)
@@ -87,17 +100,17 @@ def compare_factors(X: np.ndarray, packed_gpu: np.ndarray, ipiv_gpu, dtype, ref=
     if ks < n:
         k = ks - 1                                 # ipiv[k+1] is step k's pivot
         pre, _ = oracle.ltlt(Xd, nsteps=k)
-        col = np.abs(pre[:, k].astype(np.float64))
+        col = _pivot_mag(pre[:, k].astype(W))
         eps = np.finfo(dtype).eps
         assert col[ipiv_gpu[ks]] >= (1 - 64 * n * eps) * col[ipiv_ref[ks]], (
             f"pivot mismatch at step {k} is not a near-tie: |{col[ipiv_gpu[ks]]}| vs |{col[ipiv_ref[ks]]}|")
         ncols = k
-        cols_ref = carry_rows(pre[:, :ncols].astype(np.float64), ipiv_gpu, k, n)
+        cols_ref = carry_rows(pre[:, :ncols].astype(W), ipiv_gpu, k, n)
     else:
         ncols = max(n - 1, 0)
-        cols_ref = packed_ref[:, :ncols].astype(np.float64)
+        cols_ref = packed_ref[:, :ncols].astype(W)
     if ncols > 0:
-        g = packed_gpu[:, :ncols].astype(np.float64)
+        g = packed_gpu[:, :ncols].astype(W)
         mask = np.tril(np.ones((n, ncols), bool), -1)
         sub = np.zeros_like(mask)
         for c in range(ncols):
@@ -115,8 +128,8 @@ def compare_factors(X: np.ndarray, packed_gpu: np.ndarray, ipiv_gpu, dtype, ref=
             info["L_err"] = float(el)
             assert el <= tol, f"L normwise error {el:.3e} > {tol}"
     if ks >= n and n >= 2:
-        e_last = abs(float(packed_gpu[n - 1, n - 2]) - float(packed_ref[n - 1, n - 2]))
-        scale = max(np.abs(np.diag(packed_ref.astype(np.float64), -1)).max(), np.finfo(float).tiny)
+        e_last = abs(complex(packed_gpu[n - 1, n - 2]) - complex(packed_ref[n - 1, n - 2]))
+        scale = max(np.abs(np.diag(packed_ref.astype(W), -1)).max(), np.finfo(float).tiny)
         assert e_last / scale <= tol_a
     info["tol"], info["tol_alpha"] = tol, tol_a
     return info
@@ -128,7 +141,8 @@ def residual_probe(X: np.ndarray, packed: np.ndarray, ipiv, nprobe: int = 3, see
     estimates ||R||_F with O(n^2) work."""
     n = X.shape[0]
     eps = np.finfo(X.dtype).eps
-    Xd = X.astype(np.float64)
+    W = _wide(X)
+    Xd = X.astype(W)
     perm = np.arange(n)
     for i in range(n):
         j = int(ipiv[i])
@@ -137,14 +151,14 @@ def residual_probe(X: np.ndarray, packed: np.ndarray, ipiv, nprobe: int = 3, see
     PtZ = np.empty_like(Z)
     PtZ[perm] = Z                                  # P^T Z
     left = (Xd @ PtZ)[perm]                        # P X P^T Z
-    Lfull = np.eye(n)
+    Lfull = np.eye(n, dtype=W)
     if n > 2:
-        Lfull[:, 1:] += np.tril(packed.astype(np.float64), -2)[:, :-1]
-    alpha = np.diag(packed.astype(np.float64), -1)
-    W = Lfull.T @ Z
-    TW = np.zeros_like(W)
-    TW[1:] += alpha[:, None] * W[:-1]
-    TW[:-1] -= alpha[:, None] * W[1:]
+        Lfull[:, 1:] += np.tril(packed.astype(W), -2)[:, :-1]
+    alpha = np.diag(packed.astype(W), -1)
+    V = Lfull.T @ Z
+    TW = np.zeros_like(V)
+    TW[1:] += alpha[:, None] * V[:-1]
+    TW[:-1] -= alpha[:, None] * V[1:]
     right = Lfull @ TW
     est = np.linalg.norm(left - right) / np.sqrt(nprobe)
     return float(est / (n * eps * np.linalg.norm(Xd)))

@@ -32,7 +32,7 @@ def test_header_declares_the_entry_points():
     for must in ["ltlt_factor", "ltlt_factor_nb", "ltlt_pfaffian", "ltlt_factor_batched",
                  "ltlt_skew_update", "ltlt_device_status", "ltlt_profile_enable",
                  "ltlt_profile_read", "ltlt_release_workspace", "ltlt_mfma_probe",
-                 "ltlt_pfaffian_direct", "ltlt_solve"]:
+                 "ltlt_pfaffian_direct", "ltlt_solve", "ltlt_pfaffian_complex"]:
         assert must in names
 
 
@@ -66,6 +66,10 @@ NULL = None
     ((4, 1, 4, 0, 1, 0, NULL), -6),             # nb < 1
     ((4, 1, 4, 0, 1, 257, NULL), -6),           # nb too wide
     ((0, NULL, 1, 0, NULL, 128, NULL), 0),      # n = 0 is a no-op
+    ((4, 1, 4, 4, 1, 64, NULL), -4),            # no such dtype
+    ((4, 1, 4, 2, 1, 129, NULL), -6),           # complex panel holds at most 128 steps
+    ((4, 1, 4, 3, 1, 0, NULL), -6),
+    ((0, NULL, 1, 2, NULL, 64, NULL), 0),       # complex n = 0
 ])
 def test_factor_argument_checks(lib, args, code):
     assert lib.ltlt_factor_nb(*args) == code
@@ -99,6 +103,28 @@ def test_batched_argument_checks(lib, args, code):
 ])
 def test_pfaffian_argument_checks(lib, args, code):
     assert lib.ltlt_pfaffian(*args) == code
+
+
+@pytest.mark.parametrize("args,code", [
+    ((-1, 1, 1, 2, 1, 1, 1, NULL), -1),
+    ((4, NULL, 4, 2, 1, 1, 1, NULL), -2),
+    ((4, 1, 2, 2, 1, 1, 1, NULL), -3),
+    ((4, 1, 4, 0, 1, 1, 1, NULL), -4),          # real dtype: ltlt_pfaffian's job
+    ((4, 1, 4, 2, NULL, 1, 1, NULL), -5),
+    ((4, 1, 4, 3, 1, NULL, 1, NULL), -6),
+    ((4, 1, 4, 3, 1, 1, NULL, NULL), -7),
+])
+def test_pfaffian_complex_argument_checks(lib, args, code):
+    assert lib.ltlt_pfaffian_complex(*args) == code
+
+
+@pytest.mark.parametrize("dtype", [2, 3])
+def test_complex_dtypes_refused_where_not_supported(lib, dtype):
+    assert lib.ltlt_pfaffian(4, 1, 4, dtype, 1, 1, 1, NULL) == -4
+    assert lib.ltlt_pfaffian_direct(4, 1, 4, dtype, 1, 0, 1, 1, NULL) == -4
+    assert lib.ltlt_solve(4, 1, 4, dtype, 1, 1, 1, 4, NULL) == -4
+    assert lib.ltlt_factor_batched(4, 2, 1, 4, 16, dtype, 1, 4, 1, 1, NULL) == -6
+    assert lib.ltlt_skew_update(5, 1, 5, NULL, 2, 1, 5, 1, 5, dtype, NULL) == -10
 
 
 @pytest.mark.parametrize("args,code", [
