@@ -9,12 +9,13 @@ device copy (outside the timed events: the factorization works in place).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--nb 128]
                        [--n 16384] [--dtype f64|f32] [--no-cpu-baseline]
-                       [--workload factor|batched|pfaffian|solve] [--nrhs R]
+                       [--workload factor|batched|pfaffian|solve|complex] [--nrhs R]
 Prints one JSON line.  `--workload batched` instead times the batched path
 (8192 independent n=64 matrices, factors + Pfaffians) against HBM bandwidth;
 `--workload pfaffian` the Pfaffian by the even column steps alone;
 `--workload solve` the solve X x = b with the factors (R right-hand sides)
-against HBM bandwidth.
+against HBM bandwidth; `--workload complex` the factorization + Pfaffian of a
+complex128 (or, with --dtype f32, complex64) skew-symmetric matrix.
 """
 from __future__ import annotations
 
@@ -38,12 +39,12 @@ def parse():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--n", type=int, default=16384)
-    ap.add_argument("--nb", type=int, default=128)
+    ap.add_argument("--nb", type=int, default=None, help="panel width (default 128)")
     ap.add_argument("--dtype", choices=["f64", "f32"], default="f64")
     ap.add_argument("--seed", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--workload", choices=["factor", "batched", "pfaffian", "solve"], default="factor")
+    ap.add_argument("--workload", choices=["factor", "batched", "pfaffian", "solve", "complex"], default="factor")
     ap.add_argument("--nrhs", type=int, default=1)
     ap.add_argument("--batch", type=int, default=8192)
     return ap.parse_args()
@@ -393,10 +394,131 @@ def run_solve(args):
     print(json.dumps(out), flush=True)
 
 
+def cpu_baseline_complex(X, n, target_s):
+    """Time the CPU oracle's complex reduction (single-threaded scalar C) on
+    its first column steps and report GFLOP/s with the complex convention of
+    the GPU line: step k counts 4 (n-k-2)^2 real flops."""
+    import numpy as np
+
+    import oracle
+    oracle.build()
+    buf = np.ascontiguousarray(X.T)
+    b1 = buf.copy()
+    t0 = time.perf_counter()
+    oracle.ltlt_colmajor(b1, n, 1)
+    t1 = time.perf_counter() - t0
+    del b1
+    steps = int(max(1, min(n - 2, target_s / max(t1, 1e-6))))
+    t0 = time.perf_counter()
+    oracle.ltlt_colmajor(buf, n, steps)
+    dt = time.perf_counter() - t0
+    flops = sum(4.0 * float(n - k - 2) ** 2 for k in range(steps))
+    return {
+        "value": flops / dt / 1e9,
+        "unit": "GFLOP/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"first {steps} of {n - 2} column steps of the same complex n={n} input "
+                  f"({dt:.1f} s; nominal flops sum_k 4 (n-k-2)^2 = {flops:.3e})",
+    }
+
+
+def run_complex(args):
+    """Factorization + Pfaffian of one dense complex skew-symmetric matrix
+    (X^T = -X): the complex panel and, per block, the two real plane updates
+    of depth 2(nb+1).  Reported as GFLOP/s of real flops, 4 n^3 / 3 per
+    factorization (a complex multiply-add is four real ones)."""
+    import numpy as np
+    import torch
+
+    import paper_2005_06410_amd as lt
+    import synth
+
+    dev = torch.device("cuda:0")
+    n = args.n
+    nb = args.nb if args.nb is not None else 128
+    np_dt = np.complex128 if args.dtype == "f64" else np.complex64
+    name = "c128" if args.dtype == "f64" else "c64"
+    X = synth.skew_gauss_complex(n, args.seed, np_dt)
+    pristine = torch.from_numpy(synth.to_colmajor(X).ravel()).to(dev)
+    work = torch.empty_like(pristine)
+    A = work.as_strided((n, n), (1, n))
+    ipiv = torch.empty(n, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step():
+        work.copy_(pristine)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        lt.factor(A, ipiv=ipiv, nb=nb)
+        logabs, phase = lt.pfaffian(A, ipiv)
+        e1.record(stream)
+        return e0, e1, logabs, phase
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    lt.device_status()
+    lt.profile_enable(True)
+    torch.cuda.synchronize()
+    evs = [step() for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    lt.profile_enable(False)
+    lt.device_status()
+    prof = lt.profile_read()
+    ms_step = sum(a.elapsed_time(b) for a, b, _, _ in evs) / len(evs)
+    peak_tf = FP64_PEAK_TF if args.dtype == "f64" else FP32_PEAK_TF
+    gflops = 4.0 * float(n) ** 3 / 3.0 / (ms_step * 1e-3) / 1e9
+    up_launches, up_ms, up_flops = prof["update"]
+    achieved_tf = up_flops / (up_ms * 1e-3) / 1e12 if up_ms > 0 else 0.0
+    out = {
+        "metric": f"complex LTL^T factorization GFLOP/s (4 n^3/3 real flops) at n={n} {name}",
+        "value": round(gflops, 2),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": name,
+        "data": "synthetic",
+        "config": {
+            "workload": f"factorization + Pfaffian of one dense complex skew-symmetric n={n} {name} matrix, "
+                        f"strict upper real and imaginary parts iid N(0,1) (seed {args.seed}), {nb} columns per block",
+            "n": n,
+            "nb": nb,
+            "parallelism": "single GPU",
+        },
+        "pct_of_peak": round(100.0 * gflops / (peak_tf * 1e3), 2),
+        "roofline": {
+            "kernel": "update_kernel (trailing update, two real planes per block)",
+            "bound": "mfma",
+            "achieved": round(achieved_tf, 3),
+            "peak": peak_tf,
+            "unit": "TFLOP/s",
+            "frac": round(achieved_tf / peak_tf, 4),
+            "traffic": None,
+            "launches_per_step": up_launches // max(args.steps, 1),
+            "avg_launch_ms": round(up_ms / max(up_launches, 1), 5),
+        },
+        "breakdown_ms_per_step": {k: round(v[1] / args.steps, 3) for k, v in prof.items()},
+        "pfaffian": {"logabs": float(evs[-1][2].item()), "phase": [float(v) for v in
+                                                                 torch.view_as_real(evs[-1][3]).cpu().ravel()]},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_complex(X, n, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
+    if args.nb is None and args.workload != "complex":
+        args.nb = 128
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+        print(f"bench.py: runs on one GPU only (asked for --gpus {args.gpus}); "
               "the single-matrix factorization is not sharded across GPUs", file=sys.stderr)
         sys.exit(2)
 
@@ -418,6 +540,9 @@ def main():
         return
     if args.workload == "solve":
         run_solve(args)
+        return
+    if args.workload == "complex":
+        run_complex(args)
         return
     dev = torch.device("cuda:0")
     n, nb = args.n, args.nb

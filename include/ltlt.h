@@ -90,7 +90,7 @@ extern "C" {
  *              k (>= k+1), ipiv[n-1] = n-1.  P applies (i, ipiv[i]) for
  *              i = 0..n-1 in increasing order.
  *   stream (6) HIP stream.
- * Uses the default panel width (128 real, 64 complex).
+ * Uses the default panel width (128).
  */
 int ltlt_factor(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, hipStream_t stream);
 

@@ -16,7 +16,7 @@ using namespace ltlt;
 namespace {
 
 constexpr int kDefaultNb = 128;
-constexpr int kDefaultComplexNb = 64;           // complex: 32 register slots per lane, two lanes per row
+constexpr int kDefaultComplexNb = 128;          // complex: 32 register slots per lane, four lanes per row
 constexpr int kMaxComplexNb = 128;
 constexpr int64_t kMaxOrder = (1 << 21) - 1;   // exchange records pack indices in 21 bits
 constexpr size_t kLdsBudget = 160 * 1024 - 2048;   // dynamic LDS a panel workgroup may use
