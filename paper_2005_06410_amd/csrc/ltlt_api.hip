@@ -564,6 +564,7 @@ int ltlt_solve(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* 
   const size_t o_Y = cv.take<char>((size_t)ldy * kSolveRhs * esz);
   const size_t o_W = cv.take<char>((size_t)ldy * kSolveRhs * esz);
   const size_t o_box = cv.take<uint64_t>((size_t)nblk * kSolveRhs * 64 * 2);
+  const size_t o_dinv = cv.take<char>((size_t)(1 + 2 * 2) * nblk * 64 * 64 * esz);
   void* ws = nullptr;
   int* status = nullptr;
   hipError_t e = workspace(cv.off, &ws, &status);
@@ -580,6 +581,7 @@ int ltlt_solve(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* 
   w.W = base + o_W;
   w.ldy = ldy;
   w.box = reinterpret_cast<uint64_t*>(base + o_box);
+  w.dinv = base + o_dinv;
   w.status = status;
   e = launch_init(nullptr, 0, status, stream);    // clear the bounded-wait flag
   if (e == hipSuccess) {

@@ -111,6 +111,8 @@ struct SolveWork {
   int64_t ldy;
   uint64_t* box;      // [blocks][kSolveRhs][64][2] stamped solution words
   int* status;
+  void* dinv;         // [1 + 2 * 2][blocks][64 * 64]: inverses of the diagonal blocks of L and
+                      // the matrices of the last two dependencies of each substitution
 };
 template <typename T> hipError_t launch_solve(int n, const T* A, int64_t lda, const int* ipiv, int nrhs, T* B,
                                               int64_t ldb, const SolveWork& w, hipStream_t s);

@@ -13,19 +13,30 @@
 // gfx950 mapping:
 //  * perm: every row follows its own moves through the exchanges, in
 //    parallel (the steps bucketed by the position they target);
+//  * the inverses of the 64x64 unit lower diagonal blocks of L, and their
+//    products with the two nearest off-diagonal tiles, are formed first,
+//    all blocks at once (off the dependency chain);
 //  * the triangular solves are persistent cooperative kernels over 64-row
 //    blocks, left-looking: the workgroup of block b streams the 64x64 tiles
 //    of L to the left of its diagonal block (forward) or below it (backward)
 //    through LDS, waiting for the stamped solution words of the block each
-//    tile multiplies, then solves its diagonal block (one wave per
-//    right-hand side, the unknown broadcast by readlane) and publishes its
-//    own solution as stamped words.  A workgroup
+//    tile multiplies, except the two nearest ones; then each wave takes one
+//    right-hand side alone: the residual times the inverse of the diagonal
+//    block (its transpose, backward), minus the precomputed products with
+//    the two nearest blocks' solutions, waiting for each only then (one
+//    64-term product on the chain from block to block instead of a tile
+//    and a 64-step substitution), and publishes its solution as stamped
+//    words.  A workgroup
 //    takes its blocks in dependency order, so the earliest unfinished block
 //    always has its inputs and the grid cannot deadlock; every wait is
 //    bounded.  Each solve reads the lower triangle of L once: HBM-bound for
 //    few right-hand sides;
-//  * the recurrences of T run one lane per (right-hand side, chain), with
-//    the reciprocals of alpha formed in parallel beforehand.
+//  * each recurrence of T (w_s = a_s w_{s-1} + b_s along one parity) runs
+//    as a chunked scan: every lane of a wave composes the affine maps of its
+//    chunk of steps, the wave scans the 64 compositions, and every lane then
+//    re-runs its chunk from its exact starting value with the recurrence as
+//    written; one wave per (right-hand side, chain), the reciprocals of alpha
+//    formed in parallel beforehand.
 // Right-hand sides are taken kSolveRhs at a time.
 
 #include "ltlt_device.h"
@@ -137,71 +148,78 @@ __global__ void zero_ints_kernel(int* v, int count) {
 }
 
 // ---- skew tridiagonal recurrences -----------------------------------------
-// Wave 0 runs the odd unknowns forward, wave 1 the even unknowns backward;
-// lane q < nr takes right-hand side q.  Each chain reads the inputs of the
-// other chain's parity, so the result goes to a separate buffer W.  The
-// inputs of kTriChunk steps at a time are staged in LDS by the whole wave, so
-// that the chain itself waits only on its own arithmetic.
-constexpr int kTriChunk = 512;
+// One wave per (right-hand side q, chain): waves 2q run the odd unknowns
+// forward, waves 2q+1 the even unknowns backward.  Both chains are
+// w_s = a_s w_{s-1} + b_s over s = 1 .. n/2 - 1 after a first value w_0:
+//   odd:  i = 2s,        W[i+1] = (alpha_{i-1} W[i-1] - R[i]) / alpha_i,  w_0 = W[1] = -R[0] / alpha_0
+//   even: i = n-1-2s,    W[i-1] = (R[i] + alpha_i W[i+1]) / alpha_{i-1},  w_0 = W[n-2] = R[n-1] / alpha_{n-2}
+// Lane j takes the steps of chunk j (C consecutive steps): it composes their
+// maps (A, B) with w_end = A w_start + B, the wave forms the exclusive prefix
+// compositions by a shuffle scan, and each lane re-runs its chunk from
+// w_start = A_prefix w_0 + B_prefix, writing every unknown with the
+// recurrence as written above.  Each chain reads the other parity's inputs,
+// so the result goes to a separate buffer W.
 template <typename T>
-__global__ void __launch_bounds__(128) solve_tridiag_kernel(int n, int nr, const T* alpha, const T* ralpha,
-                                                            const T* Y, T* W, int64_t ldy) {
-  __shared__ T sbuf[2][kTriChunk * (2 + kSolveRhs)];
+__device__ __forceinline__ void tri_step_coeffs(bool odd, int n, int s, const T* alpha, const T* ralpha, const T* R,
+                                                T& ca, T& cb, T& cr, int& out) {
+  if (odd) {                                       // i = 2s: W[i+1] = (alpha_{i-1} w - R[i]) * ralpha[i]
+    const int i = 2 * s;
+    ca = alpha[i - 1]; cb = R[i]; cr = ralpha[i]; out = i + 1;
+  } else {                                         // i = n-1-2s: W[i-1] = (R[i] + alpha_i w) * ralpha[i-1]
+    const int i = n - 1 - 2 * s;
+    ca = alpha[i]; cb = R[i]; cr = ralpha[i - 1]; out = i - 1;
+  }
+}
+
+template <typename T>
+__global__ void __launch_bounds__(1024) solve_tridiag_kernel(int n, int nr, const T* alpha, const T* ralpha,
+                                                             const T* Y, T* W, int64_t ldy) {
   const int wave = threadIdx.x / kWave, lane = threadIdx.x & (kWave - 1);
-  T* sa = sbuf[wave];                              // multiplier alpha of each step
-  T* sr = sa + kTriChunk;                          // reciprocal alpha of each step
-  T* sy = sr + kTriChunk;                          // [step][rhs] right-hand side entry
+  const int q = wave >> 1;
+  if (q >= nr) return;                             // whole wave
+  const bool odd = (wave & 1) == 0;
+  const T* R = Y + (int64_t)q * ldy;
+  T* Wq = W + (int64_t)q * ldy;
   const int half = n / 2;                          // unknowns per chain
-  if (wave == 0) {
-    // W[1] = -R[0] / alpha_0;  step s >= 1, i = 2s:  W[i+1] = (alpha_{i-1} W[i-1] - R[i]) / alpha_i
-    T wprev = T(0);
-    if (lane < nr) {
-      wprev = -Y[(int64_t)lane * ldy] * ralpha[0];
-      W[1 + (int64_t)lane * ldy] = wprev;
+  const T w0 = odd ? -R[0] * ralpha[0] : R[n - 1] * ralpha[n - 2];
+  if (lane == 0) Wq[odd ? 1 : n - 2] = w0;
+  const int steps = half - 1;                      // s = 1 .. half-1
+  const int C = (steps + kWave - 1) / kWave;       // steps per lane
+  const int s_lo = 1 + lane * C, s_hi = min(half, s_lo + C);
+  // composition of this chunk's maps: w -> a w + b, a = ca cr (odd) / ca cr,
+  // b = -cb cr (odd) / cb cr (even)
+  T Ac = T(1), Bc = T(0);
+#pragma unroll 8
+  for (int s = s_lo; s < s_hi; ++s) {
+    T ca, cb, cr;
+    int out;
+    tri_step_coeffs(odd, n, s, alpha, ralpha, R, ca, cb, cr, out);
+    const T a = ca * cr, b = odd ? -cb * cr : cb * cr;
+    Ac = a * Ac;
+    Bc = fma(a, Bc, b);
+  }
+  // inclusive scan of the compositions in lane order (later maps applied
+  // after earlier ones: (A2, B2) o (A1, B1) = (A2 A1, A2 B1 + B2))
+  T Ai = Ac, Bi = Bc;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const T Ap = __shfl_up(Ai, off, kWave), Bp = __shfl_up(Bi, off, kWave);
+    if (lane >= off) {
+      Bi = fma(Ai, Bp, Bi);
+      Ai = Ai * Ap;
     }
-    for (int s0 = 1; s0 < half; s0 += kTriChunk) {
-      const int cnt = min(kTriChunk, half - s0);
-      for (int e = lane; e < cnt; e += kWave) {
-        const int i = 2 * (s0 + e);
-        sa[e] = alpha[i - 1];
-        sr[e] = ralpha[i];
-        for (int q = 0; q < nr; ++q) sy[e * kSolveRhs + q] = Y[(int64_t)i + (int64_t)q * ldy];
-      }
-      wave_lds_sync();
-      if (lane < nr) {
-        for (int e = 0; e < cnt; ++e) {
-          const T w = (sa[e] * wprev - sy[e * kSolveRhs + lane]) * sr[e];
-          W[(int64_t)(2 * (s0 + e) + 1) + (int64_t)lane * ldy] = w;
-          wprev = w;
-        }
-      }
-      wave_lds_sync();
-    }
-  } else {
-    // W[n-2] = R[n-1] / alpha_{n-2};  step s >= 1, i = n-1-2s:  W[i-1] = (R[i] + alpha_i W[i+1]) / alpha_{i-1}
-    T wnext = T(0);
-    if (lane < nr) {
-      wnext = Y[(int64_t)(n - 1) + (int64_t)lane * ldy] * ralpha[n - 2];
-      W[(int64_t)(n - 2) + (int64_t)lane * ldy] = wnext;
-    }
-    for (int s0 = 1; s0 < half; s0 += kTriChunk) {
-      const int cnt = min(kTriChunk, half - s0);
-      for (int e = lane; e < cnt; e += kWave) {
-        const int i = n - 1 - 2 * (s0 + e);
-        sa[e] = alpha[i];
-        sr[e] = ralpha[i - 1];
-        for (int q = 0; q < nr; ++q) sy[e * kSolveRhs + q] = Y[(int64_t)i + (int64_t)q * ldy];
-      }
-      wave_lds_sync();
-      if (lane < nr) {
-        for (int e = 0; e < cnt; ++e) {
-          const T w = (sy[e * kSolveRhs + lane] + sa[e] * wnext) * sr[e];
-          W[(int64_t)(n - 2 - 2 * (s0 + e)) + (int64_t)lane * ldy] = w;
-          wnext = w;
-        }
-      }
-      wave_lds_sync();
-    }
+  }
+  // exclusive prefix: the inclusive one of the previous lane
+  T Ae = __shfl_up(Ai, 1, kWave), Be = __shfl_up(Bi, 1, kWave);
+  if (lane == 0) { Ae = T(1); Be = T(0); }
+  T w = fma(Ae, w0, Be);                           // value entering this chunk
+#pragma unroll 8
+  for (int s = s_lo; s < s_hi; ++s) {
+    T ca, cb, cr;
+    int out;
+    tri_step_coeffs(odd, n, s, alpha, ralpha, R, ca, cb, cr, out);
+    w = odd ? (ca * w - cb) * cr : (cb + ca * w) * cr;
+    Wq[out] = w;
   }
 }
 
@@ -217,6 +235,9 @@ struct SolveTriArgs {
   uint64_t* box;      // [nblk][kSolveRhs][kSB][2] stamped solution words
   unsigned stamp;     // stamp of this launch (never 0)
   int* status;
+  const void* Dinv;   // inverses of the diagonal blocks of L: [nblk][64 * 64], column-major
+  const void* Mf;     // D_b^{-1} L_{b,b-d}: [kLook][nblk][64 * 64], column-major
+  const void* Mb;     // D_b^{-T} L_{b+d,b}^T: [kLook][nblk][64 * 64], column-major
 };
 
 // A solution value crosses workgroups as two 64-bit words, each holding one
@@ -255,70 +276,183 @@ __device__ __forceinline__ T l_entry(const T* A, int64_t lda, int n, int r, int 
   return A[(int64_t)r + (int64_t)(c - 1) * lda];
 }
 
-// Tile of L: rows r0 .. r0+63, columns c0 .. c0+63, into LDS column by column
-// (tile[cc * kSLd + r]); thread t loads column (t / 64) + 4 j, row t % 64, so
-// every wave instruction reads 64 consecutive rows of one column.
+// Per 64-row block b: the inverse of its unit lower diagonal block D_b of L
+// and the matrices that carry the last kLook dependencies of each
+// substitution, for d = 1 .. kLook,
+//   Mf_{b,d} = D_b^{-1} L_{b,b-d}        (forward, b >= d),
+//   Mb_{b,d} = D_b^{-T} L_{b+d,b}^T      (backward, b + d < nblk),
+// so that z_b = D_b^{-1} r_b - sum_d Mf_{b,d} z_{b-d} and
+// u_b = D_b^{-T} r_b - sum_d Mb_{b,d} u_{b+d}, where r_b is the block's
+// right-hand side less the contributions of every farther block.  All are
+// stored column-major per block, X[b*64*64 + k*64 + r] = X(r, k); rows and
+// columns past n give the identity (D_b^{-1}) or zeros (M), which the solves
+// never use.
+constexpr int kLook = 1;                          // dependencies carried by the waves
+
+// D_b^{-1}, one wave per block: lane c forms column c by forward
+// substitution, X(c,c) = 1, X(r,c) = -sum_{c<=k<r} D(r,k) X(k,c), D read from
+// LDS by broadcast.
 template <typename T>
-__device__ __forceinline__ void load_l_tile(const T* A, int64_t lda, int n, int r0, int c0, T* tile, int tid) {
-  const int r = tid & (kSB - 1);
-  const int g = tid / kSB;
+__global__ void __launch_bounds__(kWave) solve_dinv_kernel(const T* A, int64_t lda, int n, T* Dinv) {
+  __shared__ T d[kSB * kSLd];                      // D(r, c), then D^{-1}(r, c), at d[c * kSLd + r]
+  const int b = blockIdx.x, lane = threadIdx.x;
+  const int d0 = b * kSB;
+#pragma unroll 4
+  for (int cc = 0; cc < kSB; ++cc) d[cc * kSLd + lane] = l_entry(A, lda, n, d0 + lane, d0 + cc);
+  wave_lds_sync();
+  T x[kSB];
 #pragma unroll
-  for (int jj = 0; jj < kSCols; ++jj) {
-    const int cc = g + kSGroups * jj;
-    tile[cc * kSLd + r] = l_entry(A, lda, n, r0 + r, c0 + cc);
+  for (int r = 0; r < kSB; ++r) {
+    T acc = T(0);
+#pragma unroll
+    for (int k = 0; k < r; ++k) acc = fma(d[k * kSLd + r], x[k], acc);
+    x[r] = r < lane ? T(0) : (r == lane ? T(1) : -acc);
+  }
+  wave_lds_sync();                                 // every read of D is done
+#pragma unroll
+  for (int r = 0; r < kSB; ++r) d[lane * kSLd + r] = x[r];
+  wave_lds_sync();
+  T* out = Dinv + (size_t)b * kSB * kSB;
+#pragma unroll 4
+  for (int cc = 0; cc < kSB; ++cc) out[cc * kSB + lane] = d[cc * kSLd + lane];
+}
+
+// Mf_{b,d} and Mb_{b,d}, 2 kLook waves per block: D_b^{-1} into LDS; wave
+// 2(d-1) + e (e = 0 forward, 1 backward), lane k, loads column k of L_{b,b-d}
+// or row k of L_{b+d,b} and forms column k of its matrix with D_b^{-1} read
+// by broadcast.
+template <typename T>
+__global__ void __launch_bounds__(2 * kLook * kWave) solve_mmat_kernel(const T* A, int64_t lda, int n, int nblk,
+                                                                       const T* Dinv, T* Mf, T* Mb) {
+  __shared__ T d[kSB * kSLd];                      // D^{-1}(r, c) at d[c * kSLd + r]
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid & (kWave - 1);
+  const int d0 = b * kSB;
+  const size_t blk = (size_t)b * kSB * kSB;
+  for (int e = tid; e < kSB * kSB; e += blockDim.x) d[(e / kSB) * kSLd + e % kSB] = Dinv[blk + e];
+  const int dist = 1 + wave / 2;
+  const bool fwd = (wave & 1) == 0;
+  const bool has = fwd ? b >= dist : b + dist < nblk;
+  T lv[kSB];
+#pragma unroll 8
+  for (int j = 0; j < kSB; ++j)
+    lv[j] = !has ? T(0)
+                 : (fwd ? l_entry(A, lda, n, d0 + j, d0 - dist * kSB + lane)
+                        : l_entry(A, lda, n, d0 + dist * kSB + lane, d0 + j));
+  __syncthreads();
+  if (!has) return;                                // no barrier follows
+  T* out = (fwd ? Mf : Mb) + (size_t)(dist - 1) * nblk * kSB * kSB + blk + (size_t)lane * kSB;
+  // forward:  Mf(r, k) = sum_j D^{-1}(r, j) L_{b,b-d}(j, k)
+  // backward: Mb(r, k) = sum_j D^{-1}(j, r) L_{b+d,b}(k, j)
+  const int sj = fwd ? kSLd : 1, sr = fwd ? 1 : kSLd;   // LDS strides of j and r
+  for (int r = 0; r < kSB; ++r) {
+    T acc = T(0);
+#pragma unroll
+    for (int j = 0; j < kSB; ++j) acc = fma(d[j * sj + r * sr], lv[j], acc);
+    out[r] = acc;
   }
 }
 
+// Workgroup barrier for LDS only: it waits for this wave's LDS operations
+// but not for its outstanding global loads (__syncthreads does, and with
+// them every tile and solution prefetch in flight).
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Workgroup-wide AND of v over an LDS-only barrier: each wave's vote goes to
+// one of two flag sets, alternating per call (a set is rewritten two votes
+// later, after every wave has passed the barrier of the vote in between).
+struct Vote {
+  int* flags;        // LDS [2][waves]
+  int k;
+  __device__ bool all(bool v, int wave, int lane) {
+    int* f = flags + (k & 1) * (kSThreads / kWave);
+    ++k;
+    const int w = __ballot(!v) == 0;
+    if (lane == 0) f[wave] = w;
+    lds_barrier();
+    bool r = true;
+#pragma unroll
+    for (int i = 0; i < kSThreads / kWave; ++i) r = r && f[i] != 0;
+    return r;
+  }
+};
+
 // Poll the solution of block sb until every (row, right-hand side) entry
-// carries this launch's stamp; the values land in yc[row][rhs].  Bounded.
+// carries this launch's stamp; the values land in yc[row][rhs].  Bounded;
+// the whole workgroup returns false together when the wait gives up.  The
+// status word is read in the same round trip as the solution words, so an
+// unsuccessful poll costs one round trip, not two.
 template <typename T>
-__device__ __forceinline__ bool wait_box(const SolveTriArgs& a, int sb, T* yc, int tid) {
+__device__ __forceinline__ bool wait_box(const SolveTriArgs& a, int sb, T* yc, int tid, Vote& vote) {
+  const int wave = tid / kWave, lane = tid & (kWave - 1);
   const uint64_t* bx = a.box + (size_t)sb * kSolveRhs * kSB * 2;
   const uint64_t t0 = wall_ticks();
   for (;;) {
     bool ok = true;
+    const int st = tid == 0 ? ld_coh(a.status) : 0;
     for (int e = tid; e < kSB * a.nr; e += kSThreads) {
       const int rr = e % kSB, q = e / kSB;
       T v;
       if (box_get(&bx[((size_t)q * kSB + rr) * 2], a.stamp, v)) yc[rr * kSolveRhs + q] = v;
       else ok = false;
     }
-    if (__syncthreads_and(ok)) return true;
-    const bool late = tid == 0 && (ld_coh(a.status) != 0 || wall_ticks() - t0 > kWaitLimitTicks);
-    if (__syncthreads_or(late)) {
+    if (vote.all(ok, wave, lane)) return true;
+    const bool late = tid == 0 && (st != 0 || wall_ticks() - t0 > kWaitLimitTicks);
+    if (!vote.all(!late, wave, lane)) {
       if (tid == 0) atomicOr(a.status, 1);
       return false;
     }
-    __builtin_amdgcn_s_sleep(1);
   }
 }
 
-// Broadcast lane l's value (l wave-uniform) through scalar registers.
+// One wave polls the 64 solution entries of block sb for right-hand side q
+// (lane = row), reading the status word in the same round trip.  Bounded:
+// when the wait gives up (or an earlier wait already has) the status flag is
+// set and false is returned; the wave carries on with an unspecified value,
+// so that no wave leaves its workgroup's barriers.
 template <typename T>
-__device__ __forceinline__ T lane_bcast(T x, int l) {
-  if constexpr (sizeof(T) == 8) {
-    const int lo = __builtin_amdgcn_readlane(__double2loint(x), l);
-    const int hi = __builtin_amdgcn_readlane(__double2hiint(x), l);
-    return __hiloint2double(hi, lo);
-  } else {
-    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
+__device__ __forceinline__ bool wait_words(const SolveTriArgs& a, int sb, int q, int lane, T& v) {
+  const uint64_t* w = a.box + (((size_t)sb * kSolveRhs + q) * kSB + lane) * 2;
+  const uint64_t t0 = wall_ticks();
+  for (;;) {
+    const int st = ld_coh(a.status);
+    const bool ok = box_get(w, a.stamp, v);
+    if (__ballot(!ok) == 0) return true;
+    const int late = __builtin_amdgcn_readfirstlane((st != 0 || wall_ticks() - t0 > kWaitLimitTicks) ? 1 : 0);
+    if (late) {
+      if (lane == 0) atomicOr(a.status, 1);
+      return false;
+    }
   }
 }
 
-// Forward (UPPER = false): z_b = L_bb^{-1} (y_b - sum_{c<b} L_bc z_c).
+// Forward (UPPER = false): z_b = D_b^{-1} r_b - sum_{d<=kLook} Mf_{b,d} z_{b-d},
+//   r_b = y_b - sum_{c<b-kLook} L_bc z_c.
 // Backward (UPPER = true), blocks from the last one down:
-//   u_b = L_bb^{-T} (w_b - sum_{b'>b} L_{b'b}^T u_{b'}).
-// The off-diagonal tiles of a block are streamed through LDS with the next
-// tile's values already in registers (they do not depend on any flag); the
-// diagonal tile has its own buffer, loaded at the start of the block.
+//   u_b = D_b^{-T} r_b - sum_{d<=kLook} Mb_{b,d} u_{b+d},
+//   r_b = w_b - sum_{b'>b+kLook} L_{b'b}^T u_{b'}.
+// The workgroup multiplies the farther off-diagonal tiles of r_b straight
+// from registers (two tiles in flight, the next block's solution words
+// requested during the current tile, so that a tile whose inputs are long
+// published costs no round trip); then every wave takes its
+// right-hand sides alone: c = D_b^{-1} r_b (resp. D_b^{-T} r_b) with its row
+// of the inverse in registers and r broadcast from LDS, then, nearest block
+// last, waits for each of the kLook neighbouring blocks' solutions and
+// subtracts M times it.  Only the last of those products is on the chain
+// from block to block; the workgroup's own tiles have kLook blocks of slack.
 template <typename T, bool UPPER>
 __global__ void __launch_bounds__(kSThreads, 1) solve_tri_kernel(SolveTriArgs a) {
-  __shared__ T tile[kSB * kSLd];
-  __shared__ T dtile[kSB * kSLd];
+  __shared__ T dtile[kSB * kSLd];                  // D_b^{-1}, column-major
+  __shared__ T mtile[kLook][kSB * kSLd];           // Mf_{b,d} (forward) or Mb_{b,d} (backward), column-major
   __shared__ T yc[kSB * kSolveRhs];                // solution of the block a tile multiplies
   __shared__ T part[kSGroups * kSB * kSolveRhs];   // partial sums of the four groups
+  __shared__ T xs[kSThreads / kWave][kSB];         // vector broadcast to the lanes of a wave
+  __shared__ int vflags[2 * (kSThreads / kWave)];
+  Vote vote{vflags, 0};
   const T* A = static_cast<const T*>(a.A);
   T* Y = static_cast<T*>(a.Y);
+  const T* Dinv = static_cast<const T*>(a.Dinv);
+  const T* Mx = static_cast<const T*>(UPPER ? a.Mb : a.Mf);
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int r = tid & (kSB - 1), g = tid / kSB;
   const int n = a.n, nr = a.nr, nblk = a.nblk;
@@ -326,20 +460,70 @@ __global__ void __launch_bounds__(kSThreads, 1) solve_tri_kernel(SolveTriArgs a)
   for (int i = blockIdx.x; i < nblk; i += gridDim.x) {
     const int b = UPPER ? nblk - 1 - i : i;
     const int d0 = b * kSB;
-    const int ntile = UPPER ? nblk - 1 - b : b;
+    const int ntile = UPPER ? nblk - 1 - b : b;   // tiles of r_b and the chain's tile
+    const int nfull = ntile > kLook ? ntile - kLook : 0;   // tiles the workgroup multiplies itself
+    const int nlook = ntile - nfull;               // tiles the waves carry (nearest last)
     // tile t multiplies the solution of block src(t): forward t, backward nblk-1-t
     auto src = [&](int t) { return UPPER ? nblk - 1 - t : t; };
-    T regs[kSCols];
-    auto fetch = [&](int t) {
+    // thread (r, g) holds, jj < 16, forward L(d0 + r, s0 + g + 4 jj) (row r of
+    // the tile, coalesced), backward L(s0 + g + 4 jj, d0 + r) (column r of the
+    // tile: one row per instruction, each thread's 16 rows from a few lines);
+    // either way the thread's sum is over its own registers
+    auto fetch = [&](int t, T(&regs)[kSCols]) {
       const int s0 = src(t) * kSB;
-      const int rr0 = UPPER ? s0 : d0, cc0 = UPPER ? d0 : s0;
 #pragma unroll
-      for (int jj = 0; jj < kSCols; ++jj) regs[jj] = l_entry(A, lda, n, rr0 + r, cc0 + g + kSGroups * jj);
+      for (int jj = 0; jj < kSCols; ++jj)
+        regs[jj] = UPPER ? l_entry(A, lda, n, s0 + g + kSGroups * jj, d0 + r)
+                         : l_entry(A, lda, n, d0 + r, s0 + g + kSGroups * jj);
     };
-    load_l_tile(A, lda, n, d0, d0, dtile, tid);
-    // this wave's right-hand side entries of the block (rhs wave, wave + 4),
-    // read now: they are needed only at the diagonal step, which is on the
-    // chain from block to block
+    // the solution words of a tile's block, loaded one tile ahead: entry
+    // e = q * 64 + row of the block's words, kYE entries per thread
+    constexpr int kYE = kSB * kSolveRhs / kSThreads;
+    uint64_t yw[kYE][2];
+    auto ypf = [&](int t) {
+      const uint64_t* bx = a.box + (size_t)src(t) * kSolveRhs * kSB * 2;
+#pragma unroll
+      for (int e = 0; e < kYE; ++e) {
+        const int idx = tid + e * kSThreads;
+        if (idx < kSB * nr) {
+          yw[e][0] = ld_coh64(&bx[(size_t)idx * 2]);
+          yw[e][1] = ld_coh64(&bx[(size_t)idx * 2 + 1]);
+        }
+      }
+    };
+    // the prefetched words into yc when every one carries this launch's
+    // stamp (true for the whole workgroup), else false
+    auto ytake = [&]() {
+      bool ok = true;
+#pragma unroll
+      for (int e = 0; e < kYE; ++e) {
+        const int idx = tid + e * kSThreads;
+        if (idx < kSB * nr) {
+          const uint64_t w0 = yw[e][0], w1 = yw[e][1];
+          if ((unsigned)w0 != a.stamp || (unsigned)w1 != a.stamp) {
+            ok = false;
+          } else {
+            T v;
+            if constexpr (sizeof(T) == 8) v = __hiloint2double((int)(w0 >> 32), (int)(w1 >> 32));
+            else v = __uint_as_float((unsigned)(w0 >> 32));
+            yc[(idx % kSB) * kSolveRhs + idx / kSB] = v;
+          }
+        }
+      }
+      return vote.all(ok, wave, lane);
+    };
+    {
+      const T* Db = Dinv + (size_t)b * kSB * kSB;
+      const size_t mat = (size_t)nblk * kSB * kSB;
+#pragma unroll
+      for (int jj = 0; jj < kSCols; ++jj) {
+        const int cc = g + kSGroups * jj;
+        dtile[cc * kSLd + r] = Db[cc * kSB + r];
+#pragma unroll
+        for (int dd = 0; dd < kLook; ++dd)
+          if (dd < nlook) mtile[dd][cc * kSLd + r] = Mx[(size_t)dd * mat + (size_t)b * kSB * kSB + cc * kSB + r];
+      }
+    }
     constexpr int kQW = kSolveRhs / (kSThreads / kWave);
     T ypre[kQW];
 #pragma unroll
@@ -350,37 +534,44 @@ __global__ void __launch_bounds__(kSThreads, 1) solve_tri_kernel(SolveTriArgs a)
     T acc[kSolveRhs];
 #pragma unroll
     for (int q = 0; q < kSolveRhs; ++q) acc[q] = T(0);
-    if (ntile > 0) fetch(0);
-    for (int t = 0; t < ntile; ++t) {
+    // tile t: its block's solution in yc (prefetched words, else a poll),
+    // the next block's words requested, then the product; two tiles are in
+    // flight in registers (buffers ra and rb alternate)
+    auto step = [&](int t, T(&regs)[kSCols]) {
+      if (!ytake() && !wait_box<T>(a, src(t), yc, tid, vote)) return false;
+      if (t + 1 < nfull) ypf(t + 1);
+      // thread (r, g): output entry r, terms g + 4 jj, straight from registers;
+      // every right-hand side slot, branch-free (the sums of slots past nr are
+      // never read), so that the tile loads are not all waited for per term
 #pragma unroll
-      for (int jj = 0; jj < kSCols; ++jj) tile[(g + kSGroups * jj) * kSLd + r] = regs[jj];
-      if (t + 1 < ntile) fetch(t + 1);
-      if (!wait_box<T>(a, src(t), yc, tid)) return;
-      // forward: thread (row r, column group g); backward: (column r, row group g)
-#pragma unroll 4
       for (int jj = 0; jj < kSCols; ++jj) {
-        const int k = g * kSCols + jj;
-        const T lv = UPPER ? tile[r * kSLd + k] : tile[k * kSLd + r];
+        const int k = g + kSGroups * jj;
 #pragma unroll
-        for (int q = 0; q < kSolveRhs; ++q)
-          if (q < nr) acc[q] = fma(lv, yc[k * kSolveRhs + q], acc[q]);
+        for (int q = 0; q < kSolveRhs; ++q) acc[q] = fma(regs[jj], yc[k * kSolveRhs + q], acc[q]);
       }
-      __syncthreads();
+      lds_barrier();                               // yc is rewritten by the next tile
+      return true;
+    };
+    T ra[kSCols], rb[kSCols];
+    if (nfull > 0) { fetch(0, ra); ypf(0); }
+    if (nfull > 1) fetch(1, rb);
+    for (int t = 0; t < nfull; t += 2) {
+      if (!step(t, ra)) return;
+      if (t + 2 < nfull) fetch(t + 2, ra);
+      if (t + 1 < nfull) {
+        if (!step(t + 1, rb)) return;
+        if (t + 3 < nfull) fetch(t + 3, rb);
+      }
     }
 #pragma unroll
     for (int q = 0; q < kSolveRhs; ++q) part[(g * kSB + r) * kSolveRhs + q] = acc[q];
-    __syncthreads();
-    // diagonal block: wave w solves right-hand sides w, w+4; lane = row
-    // (forward) or column (backward) of the block.  The lane's entries of
-    // the diagonal tile go to registers first, so that the 64 dependent steps
-    // wait only on the scalar broadcast and the FMA.
+    lds_barrier();
+    // wave w takes right-hand sides w, w+4; lane = row (forward) or column
+    // (backward) of the block
 #pragma unroll
     for (int k = 0; k < kQW; ++k) {
       const int q = wave + (kSThreads / kWave) * k;
       if (q >= nr) break;
-      T dl[kSB];
-#pragma unroll
-      for (int cc = 0; cc < kSB; ++cc) dl[cc] = UPPER ? dtile[lane * kSLd + cc] : dtile[cc * kSLd + lane];
       T x = T(0);
       if (d0 + lane < n) {
         T sum = T(0);
@@ -388,23 +579,37 @@ __global__ void __launch_bounds__(kSThreads, 1) solve_tri_kernel(SolveTriArgs a)
         for (int gg = 0; gg < kSGroups; ++gg) sum += part[(gg * kSB + lane) * kSolveRhs + q];
         x = ypre[k] - sum;
       }
-      if constexpr (!UPPER) {
+      xs[wave][lane] = x;
+      wave_lds_sync();
+      {
+        T dl[kSB];
 #pragma unroll
-        for (int cc = 0; cc < kSB; ++cc) {
-          const T xc = lane_bcast(x, cc);
-          if (lane > cc) x = fma(-dl[cc], xc, x);                    // L(d0+lane, d0+cc)
-        }
-      } else {
+        for (int cc = 0; cc < kSB; ++cc) dl[cc] = UPPER ? dtile[lane * kSLd + cc] : dtile[cc * kSLd + lane];
+        T s4[4] = {T(0), T(0), T(0), T(0)};
 #pragma unroll
-        for (int rr = kSB - 1; rr >= 0; --rr) {
-          const T xr = lane_bcast(x, rr);
-          if (lane < rr) x = fma(-dl[rr], xr, x);                    // L(d0+rr, d0+lane)
-        }
+        for (int cc = 0; cc < kSB; ++cc) s4[cc & 3] = fma(dl[cc], xs[wave][cc], s4[cc & 3]);
+        x = (s4[0] + s4[1]) + (s4[2] + s4[3]);
+      }
+      wave_lds_sync();                             // xs is rewritten below
+      // distance d = nlook .. 1: tile ntile-d multiplies block src(ntile-d)
+      for (int dd = nlook - 1; dd >= 0; --dd) {
+        T ml[kSB];
+#pragma unroll
+        for (int kk = 0; kk < kSB; ++kk) ml[kk] = mtile[dd][kk * kSLd + lane];
+        T yp;
+        wait_words<T>(a, src(ntile - 1 - dd), q, lane, yp);
+        xs[wave][lane] = yp;
+        wave_lds_sync();
+        T s4[4] = {T(0), T(0), T(0), T(0)};
+#pragma unroll
+        for (int kk = 0; kk < kSB; ++kk) s4[kk & 3] = fma(ml[kk], xs[wave][kk], s4[kk & 3]);
+        x -= (s4[0] + s4[1]) + (s4[2] + s4[3]);
+        wave_lds_sync();
       }
       if (d0 + lane < n) Y[(int64_t)(d0 + lane) + (int64_t)q * ldy] = x;
       box_put(&a.box[(((size_t)b * kSolveRhs + q) * kSB + lane) * 2], d0 + lane < n ? x : T(0), a.stamp);
     }
-    __syncthreads();                               // part and dtile are reused by the next block
+    lds_barrier();                                 // part, dtile and mtile are reused by the next block
   }
 }
 
@@ -458,6 +663,12 @@ hipError_t launch_solve(int n, const T* A, int64_t lda, const int* ipiv, int nrh
   hipLaunchKernelGGL(solve_alpha_kernel<T>, dim3((n + 255) / 256), dim3(256), 0, s, n, A, lda, alpha, ralpha);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int nblk = (n + kSB - 1) / kSB;
+  T* Dinv = static_cast<T*>(w.dinv);
+  T* Mf = Dinv + (size_t)nblk * kSB * kSB;
+  T* Mb = Mf + (size_t)kLook * nblk * kSB * kSB;
+  hipLaunchKernelGGL(solve_dinv_kernel<T>, dim3(nblk), dim3(kWave), 0, s, A, lda, n, Dinv);
+  hipLaunchKernelGGL(solve_mmat_kernel<T>, dim3(nblk), dim3(2 * kLook * kWave), 0, s, A, lda, n, nblk, Dinv, Mf, Mb);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
   for (int q0 = 0; q0 < nrhs; q0 += kSolveRhs) {
     const int nr = nrhs - q0 < kSolveRhs ? nrhs - q0 : kSolveRhs;
     T* Bq = B + (int64_t)q0 * ldb;
@@ -466,10 +677,11 @@ hipError_t launch_solve(int n, const T* A, int64_t lda, const int* ipiv, int nrh
     if ((e = hipGetLastError()) != hipSuccess) return e;
     SolveTriArgs ta{};
     ta.A = A; ta.lda = lda; ta.n = n; ta.nblk = nblk; ta.Y = Y; ta.ldy = w.ldy; ta.nr = nr;
-    ta.box = w.box; ta.status = w.status;
+    ta.box = w.box; ta.status = w.status; ta.Dinv = Dinv; ta.Mf = Mf; ta.Mb = Mb;
     ta.stamp = next_stamp();
     if ((e = launch_solve_tri<T, false>(ta, s)) != hipSuccess) return e;
-    hipLaunchKernelGGL(solve_tridiag_kernel<T>, dim3(1), dim3(128), 0, s, n, nr, alpha, ralpha, Y, W, w.ldy);
+    hipLaunchKernelGGL(solve_tridiag_kernel<T>, dim3(1), dim3(2 * nr * kWave), 0, s, n, nr, alpha, ralpha, Y, W,
+                       w.ldy);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     ta.Y = W;
     ta.stamp = next_stamp();
