@@ -98,3 +98,14 @@ def test_odd_order_is_refused():
     b = torch.ones(5, dtype=torch.float64, device="cuda")
     with pytest.raises(lt().LtltError):
         lt().solve(A, ipiv, b)
+
+
+def test_full_size_n16384():
+    """The configuration bench.py times: the factors of the n = 16384 Gaussian
+    matrix (nb = 128) and one right-hand side: x against the oracle's solve on
+    the same factors (normwise 1e-9) and the backward error against X."""
+    n = 16384
+    X = synth.skew_gauss(n, 5)
+    b = synth.rng_for(6).standard_normal((n, 1))
+    packed, ipiv, x = gpu_factor_solve(X, b)
+    check(X, b, x, packed, ipiv, 1e-9)
