@@ -6,6 +6,8 @@
 #include <algorithm>
 #include <map>
 #include <mutex>
+#include <set>
+#include <utility>
 #include <vector>
 
 #include "ltlt.h"
@@ -72,6 +74,25 @@ struct Carve {
     return at;
   }
 };
+
+}  // namespace
+
+namespace ltlt {
+hipError_t ensure_dynamic_lds(const void* kernel, int bytes) {
+  static std::mutex mu;
+  static std::set<std::pair<const void*, int>> done;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(mu);
+  if (done.count({kernel, dev})) return hipSuccess;
+  e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e == hipSuccess) done.insert({kernel, dev});
+  return e;
+}
+}  // namespace ltlt
+
+namespace {
 
 // ---- profiling ---------------------------------------------------------------
 struct ProfRec {

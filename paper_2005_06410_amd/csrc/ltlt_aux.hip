@@ -145,13 +145,8 @@ hipError_t launch_perm_apply(T* A, int64_t lda, int n, const int* G, int nb, int
   if (c_end <= 0) return hipSuccess;
   const size_t bytes = (size_t)n * sizeof(T);
   if (bytes <= kPermLds) {
-    static bool attr = false;
-    if (!attr) {
-      hipError_t e = hipFuncSetAttribute((const void*)perm_apply_kernel<T, true>,
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)kPermLds);
-      if (e != hipSuccess) return e;
-      attr = true;
-    }
+    const hipError_t e = ensure_dynamic_lds((const void*)perm_apply_kernel<T, true>, (int)kPermLds);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL((perm_apply_kernel<T, true>), dim3(c_end), dim3(256), bytes, s, A, lda, n, G, nb, c_end,
                        (T*)nullptr);
   } else {

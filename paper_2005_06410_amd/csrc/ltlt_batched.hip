@@ -207,13 +207,8 @@ hipError_t launch_batched(int n, int batch, T* A, int64_t lda, int64_t strideA, 
                           double* logabs, int* sign, hipStream_t s) {
   if (batch <= 0) return hipSuccess;
   const size_t lds = (size_t)kBWaves * kBWaveLds * sizeof(T);
-  static bool attr_set = false;
-  if (!attr_set) {
-    const hipError_t e =
-        hipFuncSetAttribute((const void*)batched_kernel<T>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
+  const hipError_t e = ensure_dynamic_lds((const void*)batched_kernel<T>, (int)lds);
+  if (e != hipSuccess) return e;
   const int grid = (batch + kBWaves - 1) / kBWaves;
   hipLaunchKernelGGL(batched_kernel<T>, dim3(grid), dim3(256), lds, s, n, batch, A, lda, strideA, ipiv, strideIpiv,
                      logabs, sign);

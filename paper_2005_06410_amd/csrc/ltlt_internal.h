@@ -65,6 +65,9 @@ template <typename T> hipError_t launch_batched(int n, int batch, T* A, int64_t 
                                                 int64_t strideIpiv, double* logabs, int* sign, hipStream_t s);
 
 hipError_t launch_init(int* ipiv, int n, int* status, hipStream_t s);
+// Raises a kernel's dynamic-LDS limit to `bytes` on the current device, once
+// per (kernel, device): the attribute is per device.  Thread-safe.
+hipError_t ensure_dynamic_lds(const void* kernel, int bytes);
 hipError_t launch_rec_init(uint64_t* rec, int nrec_per_slot, hipStream_t s);
 hipError_t launch_perm_chain(const int* Tblk, int nb, int nblk, int n, int* G, hipStream_t s);
 template <typename T> int panel_max_blocks(int bw, size_t lds);

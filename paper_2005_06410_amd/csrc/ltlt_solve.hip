@@ -663,6 +663,15 @@ hipError_t launch_solve(int n, const T* A, int64_t lda, const int* ipiv, int nrh
   hipLaunchKernelGGL(solve_alpha_kernel<T>, dim3((n + 255) / 256), dim3(256), 0, s, n, A, lda, alpha, ralpha);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int nblk = (n + kSB - 1) / kSB;
+  {
+    // The solution words validate by the stamp of their launch, and stamps are
+    // small integers: clear the words first, so that whatever an earlier call
+    // left in this part of the workspace can never carry a current stamp.
+    const int words = nblk * kSolveRhs * kSB * 2 * 2;   // as 32-bit halves
+    hipLaunchKernelGGL(zero_ints_kernel, dim3((words + 255) / 256), dim3(256), 0, s, reinterpret_cast<int*>(w.box),
+                       words);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   T* Dinv = static_cast<T*>(w.dinv);
   T* Mf = Dinv + (size_t)nblk * kSB * kSB;
   T* Mb = Mf + (size_t)kLook * nblk * kSB * kSB;
