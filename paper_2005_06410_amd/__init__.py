@@ -139,6 +139,20 @@ def _require_gpu(t):
         raise ValueError("tensor must live on a GPU (the library has no CPU path)")
 
 
+def _same_device(A, *others):
+    """Every tensor argument must live on A's GPU: a host or other-device
+    pointer handed to a kernel faults the device instead of raising."""
+    for t in others:
+        if t is not None and (not t.is_cuda or t.device != A.device):
+            raise ValueError("all tensor arguments must be on the same GPU as A")
+
+
+def _check_ipiv(ipiv, n: int):
+    torch = _torch()
+    if ipiv.dtype != torch.int32 or not ipiv.is_contiguous() or ipiv.numel() < n:
+        raise ValueError("ipiv must be a contiguous int32 tensor with at least n entries")
+
+
 def _colmajor_lda(A) -> int:
     if A.dim() != 2 or A.shape[0] != A.shape[1]:
         raise ValueError("A must be a square 2-D tensor")
@@ -165,8 +179,8 @@ def factor(A, ipiv=None, nb: int | None = None):
     n = A.shape[0]
     if ipiv is None:
         ipiv = torch.empty(max(n, 1), dtype=torch.int32, device=A.device)
-    if ipiv.dtype != torch.int32 or not ipiv.is_contiguous() or ipiv.numel() < n:
-        raise ValueError("ipiv must be a contiguous int32 tensor with at least n entries")
+    _same_device(A, ipiv)
+    _check_ipiv(ipiv, n)
     lib = load()
     s = _stream_ptr(A.device)
     if nb is None:
@@ -184,6 +198,8 @@ def pfaffian(A, ipiv):
     _require_gpu(A)
     lda = _colmajor_lda(A)
     n = A.shape[0]
+    _same_device(A, ipiv)
+    _check_ipiv(ipiv, n)
     logabs = torch.empty(1, dtype=torch.float64, device=A.device)
     lib = load()
     if A.is_complex():
@@ -210,6 +226,8 @@ def pfaffian_direct(A, nb: int = 0, ipiv=None):
     n = A.shape[0]
     if ipiv is None:
         ipiv = torch.empty(max(n, 1), dtype=torch.int32, device=A.device)
+    _same_device(A, ipiv)
+    _check_ipiv(ipiv, n)
     logabs = torch.empty(1, dtype=torch.float64, device=A.device)
     sign = torch.empty(1, dtype=torch.int32, device=A.device)
     code = load().ltlt_pfaffian_direct(n, A.data_ptr(), lda, _dtype_code(A), ipiv.data_ptr(), int(nb),
@@ -225,6 +243,8 @@ def solve(A, ipiv, B):
     _require_gpu(B)
     lda = _colmajor_lda(A)
     n = A.shape[0]
+    _same_device(A, B, ipiv)
+    _check_ipiv(ipiv, n)
     if B.dtype != A.dtype:
         raise ValueError("B must have A's dtype")
     if B.dim() == 1:
@@ -262,6 +282,10 @@ def factor_batched(A, ipiv=None):
     strideA = A.stride(0) if batch > 1 else lda * max(n, 1)
     if ipiv is None:
         ipiv = torch.empty((batch, max(n, 1)), dtype=torch.int32, device=A.device)
+    _same_device(A, ipiv)
+    if (ipiv.dtype != torch.int32 or ipiv.dim() != 2 or ipiv.shape[0] != batch or ipiv.shape[1] < n
+            or (n > 1 and ipiv.stride(1) != 1)):
+        raise ValueError("ipiv must be an int32 (batch, >= n) tensor with unit stride along each row")
     logabs = torch.empty(batch, dtype=torch.float64, device=A.device)
     sign = torch.empty(batch, dtype=torch.int32, device=A.device)
     lib = load()
@@ -283,9 +307,18 @@ def skew_update(C, Lx, Bt, perm=None, offset: int = 0):
         raise ValueError("C must be column-major")
     m, K = Lx.shape
     ldc = C.stride(1)
+    _same_device(C, Lx, Bt, perm)
     for t in (Lx, Bt):
         if t.dim() != 2 or (t.shape[0] > 1 and t.stride(0) != 1):
             raise ValueError("Lx and Bt must be column-major")
+        if t.dtype != C.dtype:
+            raise ValueError("Lx and Bt must have C's dtype")
+    if tuple(Bt.shape) != (m, K):
+        raise ValueError("Bt must have Lx's shape (m, K)")
+    if offset < 0 or offset + m > min(C.shape[0], C.shape[1]):
+        raise ValueError("the m x m block at `offset` must lie inside C")
+    if perm is not None and (perm.dtype != torch.int32 or not perm.is_contiguous() or perm.numel() < m):
+        raise ValueError("perm must be a contiguous int32 tensor with at least m entries")
     elem = C.element_size()
     ptr = C.data_ptr() + (offset + offset * ldc) * elem
     pp = 0 if perm is None else perm.data_ptr()

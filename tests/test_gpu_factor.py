@@ -363,3 +363,31 @@ def test_mfma_probe_rate(dtype, published):
     published dense peak and the peak itself (plus clock headroom)."""
     rate = lt().mfma_probe(dtype, iters=4000)
     assert 0.5 * published <= rate <= 1.1 * published, rate
+
+
+def test_binding_rejects_mismatched_arguments():
+    """Host tensors, other dtypes and short pivot vectors are refused by the
+    binding before any kernel sees their pointers."""
+    n = 16
+    flat, A = device_colmajor(synth.skew_gauss(n, 3))
+    with pytest.raises(ValueError):
+        lt().factor(A, ipiv=torch.empty(n, dtype=torch.int32))            # host tensor
+    with pytest.raises(ValueError):
+        lt().factor(A, ipiv=torch.empty(n, dtype=torch.int64, device="cuda"))
+    with pytest.raises(ValueError):
+        lt().factor(A, ipiv=torch.empty(n - 1, dtype=torch.int32, device="cuda"))
+    ipiv = lt().factor(A)
+    with pytest.raises(ValueError):
+        lt().pfaffian(A, ipiv.cpu())
+    with pytest.raises(ValueError):
+        lt().solve(A, ipiv, torch.ones(n, dtype=torch.float32, device="cuda"))
+    with pytest.raises(ValueError):
+        lt().solve(A, ipiv.cpu(), torch.ones(n, dtype=torch.float64, device="cuda"))
+    C = torch.zeros((8, 8), dtype=torch.float64, device="cuda").t().contiguous().t()
+    Lx = torch.zeros((8, 3), dtype=torch.float32, device="cuda").t().contiguous().t()
+    with pytest.raises(ValueError):
+        lt().skew_update(C, Lx, Lx)                                    # operands of another dtype
+    Lx64 = torch.zeros((8, 3), dtype=torch.float64, device="cuda").t().contiguous().t()
+    with pytest.raises(ValueError):
+        lt().skew_update(C, Lx64, Lx64, offset=1)                      # block past the end of C
+    torch.cuda.synchronize()
