@@ -47,11 +47,23 @@ __global__ void __launch_bounds__(256, 2) batched_kernel(int n, int batch, T* Aa
   T* my_lrowp = my_alpha + (kBSlots + 1);        // my_lrowp[u + 1] = Lrow[u]
   int* my_piv = reinterpret_cast<int*>(my_lrowp + (kBSlots + 2));   // ipiv, written out at the end
 
-  // original strict lower triangle into LDS, column by column (coalesced)
-  for (int c = 0; c + 1 < n; ++c) {
-    const int len = n - 1 - c;
-    const int base = pack_idx(n, c + 1, c);
-    for (int r = lane; r < len; r += kWave) orig[base + r] = A[(int64_t)(c + 1 + r) + (int64_t)c * lda];
+  // original strict lower triangle into LDS.  Column c holds n-1-c < 64
+  // entries, one per lane (coalesced); the loads of 16 columns are issued
+  // before any of them is written, so a matrix costs four memory round trips
+  // instead of one per column.
+  constexpr int kBFill = 16;
+  for (int c0 = 0; c0 + 1 < n; c0 += kBFill) {
+    T v[kBFill];
+#pragma unroll
+    for (int cc = 0; cc < kBFill; ++cc) {
+      const int c = c0 + cc;
+      v[cc] = (c + 1 < n && lane < n - 1 - c) ? A[(int64_t)(c + 1 + lane) + (int64_t)c * lda] : T(0);
+    }
+#pragma unroll
+    for (int cc = 0; cc < kBFill; ++cc) {
+      const int c = c0 + cc;
+      if (c + 1 < n && lane < n - 1 - c) orig[pack_idx(n, c + 1, c) + lane] = v[cc];
+    }
   }
   if (lane == 0) my_lrowp[0] = T(0);
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
