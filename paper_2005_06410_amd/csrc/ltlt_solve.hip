@@ -513,15 +513,25 @@ __global__ void __launch_bounds__(kSThreads, 1) solve_tri_kernel(SolveTriArgs a)
       return vote.all(ok, wave, lane);
     };
     {
+      // every load issued before the first LDS store, so that the block's
+      // start costs one memory round trip
       const T* Db = Dinv + (size_t)b * kSB * kSB;
       const size_t mat = (size_t)nblk * kSB * kSB;
+      T dv[kSCols], mv[kLook][kSCols];
 #pragma unroll
       for (int jj = 0; jj < kSCols; ++jj) {
         const int cc = g + kSGroups * jj;
-        dtile[cc * kSLd + r] = Db[cc * kSB + r];
+        dv[jj] = Db[cc * kSB + r];
 #pragma unroll
         for (int dd = 0; dd < kLook; ++dd)
-          if (dd < nlook) mtile[dd][cc * kSLd + r] = Mx[(size_t)dd * mat + (size_t)b * kSB * kSB + cc * kSB + r];
+          mv[dd][jj] = dd < nlook ? Mx[(size_t)dd * mat + (size_t)b * kSB * kSB + cc * kSB + r] : T(0);
+      }
+#pragma unroll
+      for (int jj = 0; jj < kSCols; ++jj) {
+        const int cc = g + kSGroups * jj;
+        dtile[cc * kSLd + r] = dv[jj];
+#pragma unroll
+        for (int dd = 0; dd < kLook; ++dd) mtile[dd][cc * kSLd + r] = mv[dd][jj];
       }
     }
     constexpr int kQW = kSolveRhs / (kSThreads / kWave);
