@@ -131,15 +131,20 @@ __device__ __forceinline__ void dma_chunk(const double* __restrict__ X, int64_t 
 template <typename T>
 __device__ __forceinline__ void gather_slice(const T* __restrict__ C, int64_t ldc, int m, int i, int pr,
                                              const int* pcol, int c0, int cl0, T (&out)[16]) {
+  // the slice's 16 column sources first (one LDS round trip), then the
+  // addresses without branches: S(pr, pc) = C(max, min), negated above the
+  // diagonal
+  int pcs[16];
+#pragma unroll
+  for (int cc = 0; cc < 16; ++cc) pcs[cc] = pcol[cl0 + cc];
 #pragma unroll
   for (int cc = 0; cc < 16; ++cc) {
-    const int cl = cl0 + cc;
-    const int c = c0 + cl;
-    const int pc = pcol[cl];
+    const int c = c0 + cl0 + cc;
+    const int pc = pcs[cc];
     const bool in = (i > c) && (i < m);
-    const bool low = pr > pc;   // S(pr, pc) = C(pr,pc), or -C(pc,pr) above the diagonal
-    int64_t off = low ? (int64_t)pr + (int64_t)pc * ldc : (int64_t)pc + (int64_t)pr * ldc;
-    off = in ? off : 1;
+    const bool low = pr > pc;
+    const int hi = low ? pr : pc, lo = low ? pc : pr;
+    const int64_t off = in ? (int64_t)hi + (int64_t)lo * ldc : 1;
     const T val = C[off];
     out[cc] = low ? val : -val;
   }
