@@ -95,7 +95,9 @@ __global__ void __launch_bounds__(kPanelThreads, 1) panel_kernel(PanelArgs a) {
 
   T* my_alpha = reinterpret_cast<T*>(smem) + wave * panel_wave_lds_elems(TOT);   // alpha_{j+u}
   T* my_lrowp = my_alpha + (TOT + 1);              // my_lrowp[u + 1] = Lrow[u]
-  __shared__ int s_p, s_posw, s_abort;
+  // the agreement's results, read back together in one LDS round trip
+  struct __align__(16) XRes { int p, posw, abort, pad; };
+  __shared__ XRes s_x;
   __shared__ double red_v[kPanelWaves];
   __shared__ uint64_t red_k[kPanelWaves];
   __shared__ T s_alpha;
@@ -113,7 +115,7 @@ __global__ void __launch_bounds__(kPanelThreads, 1) panel_kernel(PanelArgs a) {
   for (int k = 0; k < NG; ++k) gr[k] = T(0);
   if (lane == 0) my_lrowp[0] = T(0);               // Lrow[-1]: only ever multiplied, kept finite
   T cv = T(0);
-  if (tid == 0) s_abort = 0;
+  if (tid == 0) s_x.abort = 0;
   // stored column value of this row and its sign (S(a,b) = -A(b,a) above the
   // diagonal); the sign is applied in the refresh so that no code waits for
   // the load before then.  First column: index j, rows >= j+1 (lower part).
@@ -158,11 +160,13 @@ __global__ void __launch_bounds__(kPanelThreads, 1) panel_kernel(PanelArgs a) {
         red_k[wave] = ((uint64_t)(uint32_t)bi << 32) | ((uint64_t)wpos << 1) | (uint64_t)wsg;
       }
     }
-    exchange_pivot<T>(a, k + 1, k, wave, lane, w, red_v, red_k, s_p, s_posw, s_alpha, s_abort);
-    if (s_abort) return;
-    const int p = s_p;
-    const int posw = s_posw;                      // block-start index of the pivot row
+    exchange_pivot<T>(a, k + 1, k, wave, lane, w, red_v, red_k, s_x.p, s_x.posw, s_alpha, s_x.abort);
+    const int4 xr = *reinterpret_cast<const int4*>(&s_x);
     const T alph = s_alpha;
+    asm volatile("" ::"v"(xr.x), "v"(xr.y), "v"(xr.z), "v"(alph));   // both reads issued before the branch
+    if (xr.z) return;
+    const int p = xr.x;
+    const int posw = xr.y;                         // block-start index of the pivot row
 
     // ---- exchange positions k+1 and p (logical only) ----
     if (my_row && p != k + 1) {
@@ -210,16 +214,17 @@ __global__ void __launch_bounds__(kPanelThreads, 1) panel_kernel(PanelArgs a) {
     wave_lds_sync();
     {
       const int c = lane & 15;
+      // every group's reads issued at once (in bounds for any u < TOT; the
+      // entries past step t are discarded by the selects, never multiplied
+      // into a kept value), rather than one group's round trip after another
 #pragma unroll
       for (int kk = 0; kk < NG; ++kk) {
-        if (kk * 16 * S <= t) {
-          const int u = (16 * kk + c) * S + part;  // < TOT
-          const T a0 = my_alpha[u], a1 = my_alpha[u + 1];
-          const T lm = my_lrowp[u], l1 = my_lrowp[u + 2];
-          const T up = (u <= t - 1) ? a1 * l1 : T(0);
-          const T g = (u >= 1) ? up - a0 * lm : up;
-          gr[kk] = (u <= t) ? g : T(0);
-        }
+        const int u = (16 * kk + c) * S + part;    // < TOT
+        const T a0 = my_alpha[u], a1 = my_alpha[u + 1];
+        const T lm = my_lrowp[u], l1 = my_lrowp[u + 2];
+        const T up = (u <= t - 1) ? a1 * l1 : T(0);
+        const T g = (u >= 1) ? up - a0 * lm : up;
+        gr[kk] = (u <= t) ? g : T(0);
       }
     }
     {
