@@ -47,6 +47,9 @@ def parse():
     ap.add_argument("--workload", choices=["factor", "batched", "pfaffian", "solve", "complex"], default="factor")
     ap.add_argument("--nrhs", type=int, default=1)
     ap.add_argument("--batch", type=int, default=8192)
+    ap.add_argument("--input", choices=["gauss", "graded", "blockdiag4"], default="gauss",
+                    help="factor workload input: strict upper iid N(0,1); times 10^U(-3,3) per entry; "
+                         "or 4x4 Gaussian skew blocks on the diagonal")
     return ap.parse_args()
 
 
@@ -80,20 +83,40 @@ def cpu_baseline(X, n, target_s):
     }
 
 
+INPUT_TEXT = {
+    "gauss": "strict upper iid N(0,1)",
+    "graded": "strict upper N(0,1) times 10^U(-3,3) per entry",
+    "blockdiag4": "4x4 Gaussian skew-symmetric blocks on the diagonal",
+}
+
+
+# headers every kernel source includes; a kernel's code depends on them too
+KERNEL_HEADERS = ("ltlt_device.h", "ltlt_internal.h")
+
+
+def kernel_source_hash(source):
+    """sha256 of a kernel source followed by the shared headers it includes."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in (source, *KERNEL_HEADERS):
+        with open(os.path.join(ROOT, "paper_2005_06410_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
 def measured_traffic(summary, source):
     """HBM bytes per launch from a committed counter summary under profiles/
     (two rocprofv3 --pmc passes, FETCH_SIZE and WRITE_SIZE, scaled by a copy of
-    known size), or None when the kernel source has changed since."""
-    import hashlib
+    known size), or None when the kernel's code (its source or the headers it
+    includes) has changed since."""
     summ = os.path.join(ROOT, "profiles", summary)
-    src = os.path.join(ROOT, "paper_2005_06410_amd", "csrc", source)
     try:
         fields = {}
         for line in open(summ):
             if ":" in line and not line.startswith(("|", "#", " ", "-", "`")):
                 k, v = line.split(":", 1)
                 fields[k.strip()] = v.strip()
-        h = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        h = kernel_source_hash(source)
         if not h.startswith(fields.get("source_sha256_prefix", "-")):
             return None
         return float(fields["traffic_bytes_per_launch"])
@@ -549,7 +572,8 @@ def main():
     np_dt = np.float64 if args.dtype == "f64" else np.float32
     t_dt = torch.float64 if args.dtype == "f64" else torch.float32
 
-    X = synth.skew_gauss(n, args.seed).astype(np_dt)
+    gen = {"gauss": synth.skew_gauss, "graded": synth.skew_graded, "blockdiag4": synth.skew_blockdiag4}[args.input]
+    X = gen(n, args.seed).astype(np_dt)
     buf = synth.to_colmajor(X)                        # (n, n): buf[c, i] = X[i, c]
     pristine = torch.from_numpy(buf.ravel()).to(dev)
     del buf
@@ -591,6 +615,7 @@ def main():
 
     flops = float(n) ** 3 / 3.0
     gflops = flops / (ms_step * 1e-3) / 1e9
+    nb_eff = nb if nb is not None else 128
     peak_tf = FP64_PEAK_TF if args.dtype == "f64" else FP32_PEAK_TF
 
     # dominant kernel: the trailing update.  Algorithmic flops per launch =
@@ -613,10 +638,11 @@ def main():
         "dtype": args.dtype,
         "data": "synthetic",
         "config": {
-            "workload": f"one dense skew-symmetric n={n} {args.dtype} matrix, strict upper iid N(0,1) "
-                        f"(seed {args.seed}), blocked LTL^T with panel width {nb}, plus Pfaffian",
+            "workload": f"one dense skew-symmetric n={n} {args.dtype} matrix, {INPUT_TEXT[args.input]} "
+                        f"(seed {args.seed}), blocked LTL^T with panel width {nb_eff}, plus Pfaffian",
             "n": n,
-            "nb": nb,
+            "nb": nb_eff,
+            "input": args.input,
             "parallelism": "single GPU",
         },
         "pct_of_peak": round(100.0 * gflops / (peak_tf * 1e3), 2),
@@ -629,7 +655,9 @@ def main():
             "frac": round(achieved_tf / peak_tf, 4),
             "measured_loop_peak": round(loop_peak_tf, 2),
             "frac_of_measured_loop_peak": round(achieved_tf / loop_peak_tf, 4) if loop_peak_tf > 0 else None,
-            "traffic": measured_traffic("update_kernel_hbm_traffic_n16384_f64_nb128.md", "ltlt_update.hip"),
+            # counter passes exist for the headline workload only
+            "traffic": (measured_traffic("update_kernel_hbm_traffic_n16384_f64_nb128.md", "ltlt_update.hip")
+                        if (n, nb_eff, args.dtype, args.input) == (16384, 128, "f64", "gauss") else None),
             "launches_per_step": up_launches // max(args.steps, 1),
             "avg_launch_ms": round(up_ms / max(up_launches, 1), 5),
         },

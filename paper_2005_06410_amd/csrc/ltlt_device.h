@@ -148,27 +148,41 @@ __device__ __forceinline__ unsigned wave_umax(unsigned x) {
   return (unsigned)__builtin_amdgcn_readlane((int)x, 63);
 }
 // First maximum of (value, key) over the wave: the largest value, and among
-// equal values the smallest key.  Values are >= 0 for candidates and -1 for
-// lanes without one (NaN is never passed).  The wave maximum is found on the
-// high 32 bits of the value (order-preserving for non-negative doubles, +1 so
-// that 0 means "no candidate"); lanes that tie there are resolved exactly
-// (full value, then key) one by one, which is rare.  Returns the winning lane
-// (-1 when no lane has a candidate) and sets vmax / kmin to its value and key.
+// equal values the smallest key (then the lowest lane).  Values are >= 0 for
+// candidates and -1 for lanes without one (NaN is never passed); keys are >= 0
+// (INT32_MAX for no candidate).  The wave maximum is found on the high 32 bits
+// of the value (order-preserving for non-negative doubles, +1 so that 0 means
+// "no candidate").  Lanes that tie there are resolved exactly: when every
+// tied value is +0 -- a stretch of zeros, which zero-structured input gives
+// every wave at every step -- by one more wave reduction of the keys;
+// otherwise (equal high words of nonzero values, rare) one lane at a time.
+// A two-reduction form for every tie was measured slower on dense input: its
+// code changes the schedule of the step loop around it.  Returns the winning
+// lane (-1 when no lane has a candidate) and sets vmax / kmin to its value
+// and key.
 __device__ __forceinline__ int wave_first_max(double v, int key, double& vmax, int& kmin) {
   const unsigned hk = v >= 0.0 ? (unsigned)__double2hiint(v) + 1u : 0u;
   const unsigned mh = wave_umax(hk);
   if (mh == 0) { vmax = -1.0; kmin = INT32_MAX; return -1; }
-  unsigned long long hit = __ballot(hk == mh);
+  const bool tie_hi = hk == mh;
+  unsigned long long hit = __ballot(tie_hi);
   int src = __ffsll(hit) - 1;
   unsigned blo = (unsigned)__builtin_amdgcn_readlane(__double2loint(v), src);
   kmin = __builtin_amdgcn_readlane(key, src);
   hit &= hit - 1;
-  while (hit) {                                    // equal high words (rare)
-    const int l2 = __ffsll(hit) - 1;
-    const unsigned lo2 = (unsigned)__builtin_amdgcn_readlane(__double2loint(v), l2);
-    const int k2 = __builtin_amdgcn_readlane(key, l2);
-    if (lo2 > blo || (lo2 == blo && k2 < kmin)) { blo = lo2; kmin = k2; src = l2; }
-    hit &= hit - 1;
+  if (hit) {
+    if (mh == 1u && __ballot(tie_hi && __double2loint(v) != 0) == 0) {   // every tied value is +0
+      kmin = (int)~wave_umax(tie_hi ? ~(unsigned)key : 0u);
+      src = __ffsll(__ballot(tie_hi && key == kmin)) - 1;
+    } else {
+      while (hit) {
+        const int l2 = __ffsll(hit) - 1;
+        const unsigned lo2 = (unsigned)__builtin_amdgcn_readlane(__double2loint(v), l2);
+        const int k2 = __builtin_amdgcn_readlane(key, l2);
+        if (lo2 > blo || (lo2 == blo && k2 < kmin)) { blo = lo2; kmin = k2; src = l2; }
+        hit &= hit - 1;
+      }
+    }
   }
   vmax = __hiloint2double((int)(mh - 1u), (int)blo);
   return src;
