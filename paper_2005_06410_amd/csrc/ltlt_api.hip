@@ -6,7 +6,6 @@
 #include <algorithm>
 #include <map>
 #include <mutex>
-#include <set>
 #include <utility>
 #include <vector>
 
@@ -80,14 +79,15 @@ struct Carve {
 namespace ltlt {
 hipError_t ensure_dynamic_lds(const void* kernel, int bytes) {
   static std::mutex mu;
-  static std::set<std::pair<const void*, int>> done;
+  static std::map<std::pair<const void*, int>, int> set_to;   // (kernel, device) -> bytes allowed
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   std::lock_guard<std::mutex> lk(mu);
-  if (done.count({kernel, dev})) return hipSuccess;
+  const auto it = set_to.find({kernel, dev});
+  if (it != set_to.end() && it->second >= bytes) return hipSuccess;
   e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-  if (e == hipSuccess) done.insert({kernel, dev});
+  if (e == hipSuccess) set_to[{kernel, dev}] = bytes;
   return e;
 }
 }  // namespace ltlt

@@ -356,6 +356,48 @@ def test_batched_parity(n, batch, dtype):
     assert np.array_equal(full[:, iu[0], iu[1]], Xs[:, iu[0], iu[1]])
 
 
+def test_batched_zero_structured_matrices():
+    """Zero-structured members of a batch: 4x4 block-diagonal matrices (every
+    column step ties on zeros outside one block, and every k = 3 mod 4 column
+    is exactly zero) and the zero matrix, beside Gaussian ones.  ipiv matches
+    the oracle bit for bit, factors to 1e-10, Pf = the product of the blocks'
+    closed-form 4x4 Pfaffians, and each matrix gives the same result as when
+    it is factored alone (batch of one)."""
+    n = 64
+    Xs = synth.skew_batch(n, 48, 777)
+    for b in range(0, 48, 3):
+        Xs[b] = synth.skew_blockdiag4(n, 500 + b)
+    Xs[1] = 0.0
+    ref_p, ref_i, ref_l, ref_s = oracle.ltlt_batched(Xs)
+    buf = np.ascontiguousarray(np.transpose(Xs, (0, 2, 1)))
+    d = torch.from_numpy(buf).cuda()
+    A = d.as_strided((48, n, n), (n * n, 1, n))
+    ipiv, logabs, sign = lt().factor_batched(A)
+    torch.cuda.synchronize()
+    got = np.tril(np.transpose(d.cpu().numpy(), (0, 2, 1)), -1)
+    gi, la, sg = ipiv.cpu().numpy(), logabs.cpu().numpy(), sign.cpu().numpy()
+    assert np.array_equal(gi, ref_i)
+    for b in range(48):
+        scale = max(np.abs(ref_p[b]).max(), 1e-300)
+        assert np.abs(got[b] - ref_p[b]).max() <= 1e-10 * scale
+    assert np.array_equal(sg, ref_s)
+    for b in range(0, 48, 3):                       # closed forms of the block-diagonal members
+        pf = 1.0
+        for q in range(n // 4):
+            blk = Xs[b][4 * q:4 * q + 4, 4 * q:4 * q + 4]
+            pf *= blk[0, 1] * blk[2, 3] - blk[0, 2] * blk[1, 3] + blk[0, 3] * blk[1, 2]
+        assert sg[b] == np.sign(pf)
+        assert abs(la[b] - np.log(abs(pf))) <= 1e-12 * max(abs(np.log(abs(pf))), 1.0)
+    assert sg[1] == 0 and la[1] == -np.inf and np.all(gi[1] == np.arange(n))
+    for b in (0, 1, 3):                             # alone vs in the batch
+        d1 = torch.from_numpy(np.ascontiguousarray(Xs[b].T)).cuda()
+        A1 = d1.as_strided((1, n, n), (n * n, 1, n))
+        i1, l1, s1 = lt().factor_batched(A1)
+        torch.cuda.synchronize()
+        assert np.array_equal(np.tril(d1.cpu().numpy().T, -1), got[b])
+        assert np.array_equal(i1.cpu().numpy()[0], gi[b]) and s1.item() == sg[b]
+
+
 # --------------------------------------------------------------------------
 @pytest.mark.parametrize("dtype,published", [("f64", 78.6), ("f32", 157.3)])
 def test_mfma_probe_rate(dtype, published):
