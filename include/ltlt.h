@@ -90,7 +90,14 @@ extern "C" {
  *              k (>= k+1), ipiv[n-1] = n-1.  P applies (i, ipiv[i]) for
  *              i = 0..n-1 in increasing order.
  *   stream (6) HIP stream.
- * Uses the default panel width (128).
+ * Uses the default panel width (128), narrowed when it does not fit: the
+ * panel keeps every row of a block in registers of workgroups that are all
+ * resident at once (one per CU), R rows each, so a width w needs
+ * ceil((n-1)/R) <= CUs with R = 512, 256, 128 for w <= 64, 128, 256
+ * (complex: w <= 32, 64, 128).  When the default width needs more
+ * workgroups than that, ltlt_factor halves it, down to 32: on a 256-CU
+ * device the default width serves n <= 65537 (complex: 32769) and the
+ * narrowed ones n <= 131073; larger orders return LTLT_ERR_UNSUPPORTED.
  */
 int ltlt_factor(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, hipStream_t stream);
 
@@ -101,6 +108,9 @@ int ltlt_factor(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, hipSt
  *          rank-(nb+1) lower-triangular product (complex: one real product of
  *          depth 2(nb+1) per plane).
  *   stream is argument 7.
+ * Returns LTLT_ERR_UNSUPPORTED (nothing enqueued) when the panel of width nb
+ * needs more co-resident workgroups than the device holds (see ltlt_factor);
+ * ltlt_factor itself narrows the width instead.
  */
 int ltlt_factor_nb(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, int64_t nb,
                    hipStream_t stream);

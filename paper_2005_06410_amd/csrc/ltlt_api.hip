@@ -17,6 +17,7 @@ using namespace ltlt;
 namespace {
 
 constexpr int kDefaultNb = 128;
+constexpr int kMinFallbackNb = 32;       // narrowest width ltlt_factor falls back to
 constexpr int kDefaultComplexNb = 128;          // complex: 32 register slots per lane, four lanes per row
 constexpr int kMaxComplexNb = 128;
 constexpr int64_t kMaxOrder = (1 << 21) - 1;   // exchange records pack indices in 21 bits
@@ -510,7 +511,18 @@ int ltlt_factor_nb(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, in
 }
 
 int ltlt_factor(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, hipStream_t stream) {
-  return ltlt_factor_nb(n, A, lda, dtype, ipiv, is_complex(dtype) ? kDefaultComplexNb : kDefaultNb, stream);
+  // The panel holds every row of the block in registers of co-resident
+  // workgroups; narrower blocks fit more rows per workgroup.  When the default
+  // width needs more workgroups than the device holds, halve it (the size
+  // checks come before any allocation or launch, so a refused width leaves
+  // nothing behind).
+  int64_t nb = is_complex(dtype) ? kDefaultComplexNb : kDefaultNb;
+  int r = ltlt_factor_nb(n, A, lda, dtype, ipiv, nb, stream);
+  while (r == LTLT_ERR_UNSUPPORTED && nb > kMinFallbackNb && n < kMaxOrder) {
+    nb /= 2;
+    r = ltlt_factor_nb(n, A, lda, dtype, ipiv, nb, stream);
+  }
+  return r;
 }
 
 int ltlt_pfaffian_complex(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* ipiv, double* logabs,

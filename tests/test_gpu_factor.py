@@ -398,6 +398,66 @@ def test_batched_zero_structured_matrices():
         assert np.array_equal(i1.cpu().numpy()[0], gi[b]) and s1.item() == sg[b]
 
 
+def _triu_rows(M, k, ch=8192):
+    """torch.triu(M, k) built on row chunks: on this PyTorch build torch.triu of
+    a tensor past 2^32 elements returns wrong entries (a quarter of a sample at
+    66000^2), while every chunk here stays below 2^31."""
+    out = torch.empty_like(M)
+    for r0 in range(0, M.shape[0], ch):
+        out[r0:r0 + ch] = torch.triu(M[r0:r0 + ch], k + r0)
+    return out
+
+
+@pytest.mark.parametrize("n,dtype", [(70000, torch.float64), (33000, torch.complex128)])
+def test_large_order_default_width_fallback(n, dtype):
+    """Orders past what the default width's panel holds on one device (real:
+    n - 1 > 256 workgroups x 256 rows at nb = 128; complex: 256 x 128 rows):
+    ltlt_factor narrows the width and factors them.  The input is generated
+    on the device (its strict lower triangle is a seeded Gaussian buffer);
+    checked by the pivot invariants and a two-probe residual estimate in the
+    factor's precision, computed on the device (the oracle would take hours)."""
+    elt = 16 if dtype == torch.complex128 else 8
+    free, _ = torch.cuda.mem_get_info()
+    if free < 2.6 * n * n * elt + 8e9:
+        pytest.skip("needs about %.0f GB of free device memory" % (2.6 * n * n * elt / 1e9))
+    dev = torch.device("cuda")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(n)
+    buf = torch.randn(n * n, dtype=dtype, device=dev, generator=gen)
+    R = buf.view(n, n)                              # R[c, i] = A(i, c)
+    U = _triu_rows(R, 1)                            # X = U^T - U
+    A = buf.as_strided((n, n), (1, n))
+    ipiv = lt().factor(A)
+    torch.cuda.synchronize()
+    piv = ipiv.cpu().numpy()
+    assert piv[0] == 0 and piv[n - 1] == n - 1
+    assert np.all(piv[1:-1] >= np.arange(1, n - 1)) and np.all(piv < n)
+    perm = np.arange(n)
+    for i, j in enumerate(piv.tolist()):
+        perm[i], perm[j] = perm[j], perm[i]
+    perm_t = torch.from_numpy(perm).to(dev)
+    Z = torch.randn(n, 2, dtype=dtype, device=dev, generator=gen)
+    PtZ = torch.empty_like(Z)
+    PtZ[perm_t] = Z                                 # P^T Z
+    left = ((PtZ.T @ U).T - U @ PtZ)[perm_t]        # P X P^T Z
+    normX = 2 ** 0.5 * torch.linalg.norm(U).item()
+    del U
+    Lp = _triu_rows(R, 2)                           # Lp[c, r] = A(r, c) = L(r, c + 1), r >= c + 2
+    alpha = torch.diagonal(R, 1)                    # alpha_k = A(k + 1, k)
+    V = Z.clone()
+    V[1:] += (Lp @ Z)[:-1]                          # L^T Z
+    TV = torch.zeros_like(V)
+    TV[1:] += alpha[:, None] * V[:-1]               # T(k + 1, k) = alpha_k
+    TV[:-1] -= alpha[:, None] * V[1:]               # T(k, k + 1) = -alpha_k
+    sh = torch.zeros_like(TV)
+    sh[:-1] = TV[1:]
+    right = TV + (sh.T @ Lp).T                      # L (T L^T Z)
+    eps = torch.finfo(torch.float64).eps
+    est = torch.linalg.norm(left - right).item() / 2 ** 0.5 / (n * eps * normX)
+    assert est <= 10.0, est
+    assert torch.isfinite(alpha).all()
+
+
 # --------------------------------------------------------------------------
 @pytest.mark.parametrize("dtype,published", [("f64", 78.6), ("f32", 157.3)])
 def test_mfma_probe_rate(dtype, published):
