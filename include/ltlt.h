@@ -160,7 +160,12 @@ int ltlt_pfaffian_complex(int64_t n, const void* A, int64_t lda, int dtype, cons
  *   ipiv (device int32[n]): ipiv[k+1] = pivot of even step k (first index of
  *       the largest magnitude in the current column k, rows >= k+1),
  *       ipiv[i] = i elsewhere.
- *   nb: columns per block, even, 2 .. 256; 0 selects the default (128).
+ *   nb: columns per block, even, 2 .. 256; 0 selects the default (128),
+ *       halved down to 32 when its panel does not fit on the device (the
+ *       pair panel holds 448, 224, 112 rows per workgroup, one workgroup
+ *       per CU, for nb <= 64, 128, 256: on 256 CUs the default serves
+ *       n <= 57345 and the narrowed widths n <= 114689); an explicit nb that
+ *       does not fit returns LTLT_ERR_UNSUPPORTED.
  *   logabs, sign: DEVICE double / int32 outputs as in ltlt_pfaffian (odd n:
  *       sign 0, logabs -inf; n = 0: sign 1, logabs 0).
  * Returns 0, -i when argument i is invalid (nb odd or out of range: -6), or

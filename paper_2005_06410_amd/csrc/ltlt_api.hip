@@ -563,13 +563,24 @@ int ltlt_pfaffian_direct(int64_t n, void* A, int64_t lda, int dtype, int32_t* ip
   if (lda < std::max<int64_t>(1, n)) return -3;
   if (bad_dtype(dtype)) return -4;
   if (ipiv == nullptr && n > 0) return -5;
-  if (nb == 0) nb = kDefaultNb;
+  const bool default_width = nb == 0;
+  if (default_width) nb = kDefaultNb;
   if (nb < 2 || nb > kMaxNb || (nb & 1)) return -6;
   if (logabs == nullptr) return -7;
   if (sign == nullptr) return -8;
-  if (dtype == LTLT_F64)
-    return pfaffian_direct_impl<double>(n, static_cast<double*>(A), lda, ipiv, (int)nb, logabs, sign, stream);
-  return pfaffian_direct_impl<float>(n, static_cast<float*>(A), lda, ipiv, (int)nb, logabs, sign, stream);
+  auto run = [&](int64_t w) {
+    return dtype == LTLT_F64
+               ? pfaffian_direct_impl<double>(n, static_cast<double*>(A), lda, ipiv, (int)w, logabs, sign, stream)
+               : pfaffian_direct_impl<float>(n, static_cast<float*>(A), lda, ipiv, (int)w, logabs, sign, stream);
+  };
+  int r = run(nb);
+  // as ltlt_factor: a default width whose pair panel does not fit is halved
+  // (the size checks precede any launch)
+  while (default_width && r == LTLT_ERR_UNSUPPORTED && nb > kMinFallbackNb && n < kMaxOrder) {
+    nb /= 2;
+    r = run(nb);
+  }
+  return r;
 }
 
 int ltlt_solve(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* ipiv, int64_t nrhs, void* B,

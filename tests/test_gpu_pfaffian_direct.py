@@ -148,3 +148,30 @@ def test_full_size_n16384():
     torch.cuda.synchronize()
     assert sign == int(fs.item())
     assert abs(logabs - float(fl.item())) <= 1e-9 * abs(logabs)
+
+
+def test_large_order_default_width_fallback():
+    """n = 60000 is past what the default width's pair panel holds on one
+    device (256 workgroups x 224 rows): the default call narrows the width.
+    Its Pfaffian agrees with the one from the full factorization of the same
+    device-generated matrix (whose default width still fits)."""
+    n = 60000
+    free, _ = torch.cuda.mem_get_info()
+    if free < 2.2 * n * n * 8 + 8e9:
+        pytest.skip("needs about 65 GB of free device memory")
+    dev = torch.device("cuda")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(n)
+    buf = torch.randn(n * n, dtype=torch.float64, device=dev, generator=gen)
+    work = buf.clone()
+    A = buf.as_strided((n, n), (1, n))
+    W = work.as_strided((n, n), (1, n))
+    lib = lt()
+    ipiv = lib.factor(A)
+    la_f, sg_f = lib.pfaffian(A, ipiv)
+    _, la_d, sg_d = lib.pfaffian_direct(W)
+    torch.cuda.synchronize()
+    lib.device_status()
+    la_f, la_d = float(la_f.item()), float(la_d.item())
+    assert int(sg_f.item()) == int(sg_d.item()) != 0
+    assert abs(la_f - la_d) <= 1e-9 * abs(la_f)
