@@ -441,6 +441,21 @@ def test_large_order_default_width_fallback(n, dtype):
     PtZ[perm_t] = Z                                 # P^T Z
     left = ((PtZ.T @ U).T - U @ PtZ)[perm_t]        # P X P^T Z
     normX = 2 ** 0.5 * torch.linalg.norm(U).item()
+    if dtype == torch.float64:
+        # the solve on the same factors: backward error against X
+        b = torch.randn(2, n, dtype=dtype, device=dev, generator=gen).t()   # n x 2, column-major
+        x = b.clone().t().contiguous().t()
+        lt().solve(A, ipiv, x)
+        torch.cuda.synchronize()
+        Xx = (x.T @ U).T - U @ x
+        absU_rows = torch.cat([U[r0:r0 + 8192].abs().sum(1) for r0 in range(0, n, 8192)])
+        absU_cols = sum(U[r0:r0 + 8192].abs().sum(0) for r0 in range(0, n, 8192))
+        normXinf = (absU_rows + absU_cols).max().item()     # largest row sum of |U^T - U|
+        eps = torch.finfo(torch.float64).eps
+        for c in range(2):
+            be = (Xx[:, c] - b[:, c]).abs().max().item() / (normXinf * x[:, c].abs().max().item() * n * eps)
+            assert be <= 10.0, be
+        del b, x, Xx
     del U
     Lp = _triu_rows(R, 2)                           # Lp[c, r] = A(r, c) = L(r, c + 1), r >= c + 2
     alpha = torch.diagonal(R, 1)                    # alpha_k = A(k + 1, k)
