@@ -88,9 +88,9 @@ int run_probe(int64_t iters, double* tflops, hipStream_t s) {
   if (e == hipSuccess) e = hipEventRecord(e1, s);
   if (e == hipSuccess) e = hipEventSynchronize(e1);
   if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
-  if (e0) hipEventDestroy(e0);
-  if (e1) hipEventDestroy(e1);
-  if (out) hipFree(out);
+  if (e0) (void)hipEventDestroy(e0);                // cleanup: the first error is the one reported
+  if (e1) (void)hipEventDestroy(e1);
+  if (out) (void)hipFree(out);
   if (e != hipSuccess) return LTLT_ERR_HIP_BASE - (int)e;
   // 4 waves per workgroup, 16 MFMAs per iteration, 2*16*16*4 flops each
   const double flops = (double)grid * 4.0 * (double)iters * 16.0 * 2048.0;
