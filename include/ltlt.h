@@ -258,8 +258,10 @@ int ltlt_device_status(hipStream_t stream);
 /*
  * Per-kernel timing of ltlt_factor, measured with HIP events recorded on the
  * stream each kernel runs on.
- *   ltlt_profile_enable(1) starts recording (and clears earlier records),
- *   ltlt_profile_enable(0) stops.
+ *   ltlt_profile_enable(1) starts recording every launch (and clears earlier
+ *   records), ltlt_profile_enable(2) the trailing-update launches only (each
+ *   recorded launch adds two event records, about 2 us each, to the
+ *   stream), ltlt_profile_enable(0) stops; other values return -1.
  *   ltlt_profile_read synchronizes the recorded events and writes, for each
  *   kernel kind k < nkinds (0 = panel, 1 = trailing update, 2 = commit,
  *   3 = other), the launch count, the summed milliseconds and the summed

@@ -339,8 +339,11 @@ def device_status(device=None):
     _check("ltlt_device_status", lib.ltlt_device_status(_stream_ptr(device or torch.cuda.current_device())))
 
 
-def profile_enable(on: bool = True):
-    load().ltlt_profile_enable(1 if on else 0)
+def profile_enable(on=True):
+    """Record per-launch event timings: True (every launch), "update" (the
+    trailing-update launches only), or False (stop)."""
+    mode = 2 if on == "update" else (1 if on else 0)
+    _check("ltlt_profile_enable", load().ltlt_profile_enable(mode))
 
 
 def profile_read():

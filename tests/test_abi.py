@@ -197,4 +197,7 @@ def test_error_messages():
 
 def test_profile_enable_is_host_only(lib):
     assert lib.ltlt_profile_enable(1) == 0
+    assert lib.ltlt_profile_enable(2) == 0          # trailing updates only
     assert lib.ltlt_profile_enable(0) == 0
+    assert lib.ltlt_profile_enable(3) == -1
+    assert lib.ltlt_profile_enable(-1) == -1
