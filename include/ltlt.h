@@ -276,6 +276,22 @@ int ltlt_profile_read(int nkinds, int64_t* launches, double* ms, double* flops);
 int ltlt_release_workspace(void);
 
 /*
+ * ltlt_set_cooperative_panels -- how the panel kernels are launched (host
+ * call, process-wide; returns 0, or -1 for a value other than 0 or 1).
+ * A panel's workgroups (at most one per CU, never more than the device's
+ * CUs) wait on each other at every column step, so they must all be
+ * resident at once.  on = 0 (the default): ordinary launches.  Issued in
+ * stream order onto a device that runs nothing else, every workgroup is
+ * dispatched at once; when other streams or processes hold CUs during a
+ * call, the panel waits for them, and if it cannot become resident within
+ * its bounded wait (2 s) the call reports LTLT_ERR_DEVICE_TIMEOUT through
+ * ltlt_device_status instead of hanging.  on = 1: the runtime's cooperative
+ * launch, which guarantees co-residency on a shared device at about 20 us
+ * per panel launch (2-3 % of an n = 16384 factorization).
+ */
+int ltlt_set_cooperative_panels(int on);
+
+/*
  * ltlt_mfma_probe -- measured matrix-core rate of the current device.  A
  * diagnostic, not part of the factorization: it runs, on `stream`, one
  * kernel in which every wave executes `iters` iterations of 16 independent

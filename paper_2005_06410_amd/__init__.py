@@ -62,6 +62,7 @@ _SYMBOLS = {
     "ltlt_profile_enable": ([ctypes.c_int], ctypes.c_int),
     "ltlt_profile_read": ([ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "ltlt_release_workspace": ([], ctypes.c_int),
+    "ltlt_set_cooperative_panels": ([ctypes.c_int], ctypes.c_int),
     "ltlt_mfma_probe": ([ctypes.c_int, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "ltlt_pfaffian_direct": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
                               ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
@@ -361,6 +362,13 @@ def profile_read():
 
 def release_workspace():
     _check("ltlt_release_workspace", load().ltlt_release_workspace())
+
+
+def set_cooperative_panels(on: bool = True):
+    """Launch the panel kernels with the runtime's cooperative launch (its
+    co-residency guarantee, for devices shared with other work) or, the
+    default, as ordinary launches (see ``ltlt_set_cooperative_panels``)."""
+    _check("ltlt_set_cooperative_panels", load().ltlt_set_cooperative_panels(1 if on else 0))
 
 
 def mfma_probe(dtype: str = "f64", iters: int = 20000, device=None) -> float:

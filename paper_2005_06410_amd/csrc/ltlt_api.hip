@@ -4,6 +4,7 @@
 // this library; nothing here touches matrix data on the host.
 
 #include <algorithm>
+#include <atomic>
 #include <map>
 #include <mutex>
 #include <utility>
@@ -78,6 +79,11 @@ struct Carve {
 }  // namespace
 
 namespace ltlt {
+namespace {
+std::atomic<bool> g_cooperative_panels{false};
+}  // namespace
+bool cooperative_panels() { return g_cooperative_panels.load(std::memory_order_relaxed); }
+
 hipError_t ensure_dynamic_lds(const void* kernel, int bytes) {
   static std::mutex mu;
   static std::map<std::pair<const void*, int>, int> set_to;   // (kernel, device) -> bytes allowed
@@ -753,6 +759,12 @@ int ltlt_profile_read(int nkinds, int64_t* launches, double* ms, double* flops) 
     }
   }
   return kinds;
+}
+
+int ltlt_set_cooperative_panels(int on) {
+  if (on != 0 && on != 1) return -1;
+  ltlt::g_cooperative_panels.store(on == 1, std::memory_order_relaxed);
+  return 0;
 }
 
 int ltlt_release_workspace(void) {

@@ -360,10 +360,7 @@ __global__ void __launch_bounds__(kPanelThreads, 1) cpanel_kernel(CPanelArgs ca)
 
 template <typename T, int S>
 hipError_t launch_cpanel_s(const CPanelArgs& a, size_t lds, hipStream_t st) {
-  CPanelArgs copy = a;
-  void* args[] = {&copy};
-  return hipLaunchCooperativeKernel((const void*)cpanel_kernel<T, S>, dim3(a.b.P), dim3(kPanelThreads), args,
-                                    (unsigned)lds, st);
+  return launch_resident_grid(cpanel_kernel<T, S>, (unsigned)a.b.P, kPanelThreads, lds, st, a);
 }
 
 template <typename T>

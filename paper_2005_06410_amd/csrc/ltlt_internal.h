@@ -50,6 +50,25 @@ struct UpdateArgs {
   int tiles;          // number of 128-row tile rows
 };
 
+// Launch of a grid whose workgroups wait on each other every step (the
+// panels: at most one workgroup per CU, never more workgroups than the
+// device holds at once).  By default an ordinary launch: issued in stream
+// order onto an otherwise idle device, every workgroup is dispatched at
+// once, and every wait is bounded, so a grid that cannot become resident
+// (other streams or processes holding CUs for seconds) fails with the
+// bounded-wait status instead of hanging.  ltlt_set_cooperative_panels(1)
+// selects the runtime's cooperative launch, which guarantees co-residency
+// at a cost of about 20 us per launch.
+bool cooperative_panels();
+template <typename K, typename A>
+hipError_t launch_resident_grid(K kernel, unsigned grid, unsigned block, size_t lds, hipStream_t s, const A& arg) {
+  A copy = arg;
+  void* args[] = {&copy};
+  if (cooperative_panels())
+    return hipLaunchCooperativeKernel((const void*)kernel, dim3(grid), dim3(block), args, (unsigned)lds, s);
+  return hipLaunchKernel((const void*)kernel, dim3(grid), dim3(block), args, lds, s);
+}
+
 template <typename T> hipError_t launch_panel(const PanelArgs& a, size_t lds, hipStream_t s);
 template <typename T> size_t panel_lds_bytes(int bw, int R);
 template <typename T> hipError_t launch_update(const UpdateArgs& a, hipStream_t s);

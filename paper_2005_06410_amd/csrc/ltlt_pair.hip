@@ -404,10 +404,7 @@ __global__ void __launch_bounds__(kPanelThreads, 1) pair_panel_kernel(PanelArgs 
 
 template <typename T, int S>
 hipError_t launch_pair_panel_s(const PanelArgs& a, size_t lds, hipStream_t st) {
-  PanelArgs copy = a;
-  void* args[] = {&copy};
-  return hipLaunchCooperativeKernel((const void*)pair_panel_kernel<T, S>, dim3(a.P), dim3(kPanelThreads), args,
-                                    (unsigned)lds, st);
+  return launch_resident_grid(pair_panel_kernel<T, S>, (unsigned)a.P, kPanelThreads, lds, st, a);
 }
 
 template <typename T>

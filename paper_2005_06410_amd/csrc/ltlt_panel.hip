@@ -301,10 +301,7 @@ __global__ void __launch_bounds__(kPanelThreads, 1) panel_kernel(PanelArgs a) {
 
 template <typename T, int S>
 hipError_t launch_panel_s(const PanelArgs& a, size_t lds, hipStream_t st) {
-  PanelArgs copy = a;
-  void* args[] = {&copy};
-  return hipLaunchCooperativeKernel((const void*)panel_kernel<T, S>, dim3(a.P), dim3(kPanelThreads), args,
-                                    (unsigned)lds, st);
+  return launch_resident_grid(panel_kernel<T, S>, (unsigned)a.P, kPanelThreads, lds, st, a);
 }
 
 template <typename T>

@@ -32,7 +32,8 @@ def test_header_declares_the_entry_points():
     for must in ["ltlt_factor", "ltlt_factor_nb", "ltlt_pfaffian", "ltlt_factor_batched",
                  "ltlt_skew_update", "ltlt_device_status", "ltlt_profile_enable",
                  "ltlt_profile_read", "ltlt_release_workspace", "ltlt_mfma_probe",
-                 "ltlt_pfaffian_direct", "ltlt_solve", "ltlt_pfaffian_complex"]:
+                 "ltlt_pfaffian_direct", "ltlt_solve", "ltlt_pfaffian_complex",
+                 "ltlt_set_cooperative_panels"]:
         assert must in names
 
 
@@ -196,6 +197,9 @@ def test_error_messages():
 
 
 def test_profile_enable_is_host_only(lib):
+    assert lib.ltlt_set_cooperative_panels(2) == -1
+    assert lib.ltlt_set_cooperative_panels(1) == 0
+    assert lib.ltlt_set_cooperative_panels(0) == 0   # back to the default
     assert lib.ltlt_profile_enable(1) == 0
     assert lib.ltlt_profile_enable(2) == 0          # trailing updates only
     assert lib.ltlt_profile_enable(0) == 0

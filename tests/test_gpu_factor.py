@@ -473,6 +473,34 @@ def test_large_order_default_width_fallback(n, dtype):
     assert torch.isfinite(alpha).all()
 
 
+@pytest.mark.parametrize("kind", ["factor", "pfaffian_direct", "complex"])
+def test_panel_launch_modes_agree(kind):
+    """The panels' ordinary launch (default) and the cooperative launch give
+    bit-identical results (only the launch path differs)."""
+    lib = lt()
+    n = 1030
+    X = synth.skew_gauss_complex(n, 31) if kind == "complex" else synth.skew_gauss(n, 31)
+    out = []
+    try:
+        for coop in (False, True):
+            lib.set_cooperative_panels(coop)
+            flat, A = device_colmajor(X)
+            if kind == "pfaffian_direct":
+                ipiv, la, sg = lib.pfaffian_direct(A, nb=64)
+                res = [flat, ipiv, la, sg]
+            else:
+                ipiv = lib.factor(A)
+                la, sg = lib.pfaffian(A, ipiv)
+                res = [flat, ipiv, la, sg]
+            torch.cuda.synchronize()
+            lib.device_status()
+            out.append([r.cpu().clone() for r in res])
+    finally:
+        lib.set_cooperative_panels(False)
+    for a, b in zip(*out):
+        assert torch.equal(a, b)
+
+
 # --------------------------------------------------------------------------
 @pytest.mark.parametrize("dtype,published", [("f64", 78.6), ("f32", 157.3)])
 def test_mfma_probe_rate(dtype, published):
