@@ -501,6 +501,29 @@ def test_panel_launch_modes_agree(kind):
         assert torch.equal(a, b)
 
 
+@pytest.mark.parametrize("n,reps", [(1000, 40), (16384, 3)])
+def test_repeated_runs_bit_identical(n, reps):
+    """Back-to-back factorizations with the default panel launch finish
+    inside the panels' bounded waits and give bit-identical factors and
+    pivots every time (the grid exchange fixes the reduction order)."""
+    lib = lt()
+    X = synth.skew_gauss(n, 11)
+    src, _ = device_colmajor(X)
+    w = torch.empty_like(src)
+    A = w.as_strided((n, n), (1, n))
+    ipiv = torch.empty(n, dtype=torch.int32, device="cuda")
+    ref = None
+    for _ in range(reps):
+        w.copy_(src)
+        lib.factor(A, ipiv=ipiv)
+        torch.cuda.synchronize()
+        lib.device_status()
+        if ref is None:
+            ref = (w.clone(), ipiv.clone())
+        else:
+            assert torch.equal(w, ref[0]) and torch.equal(ipiv, ref[1])
+
+
 # --------------------------------------------------------------------------
 @pytest.mark.parametrize("dtype,published", [("f64", 78.6), ("f32", 157.3)])
 def test_mfma_probe_rate(dtype, published):
