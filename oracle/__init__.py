@@ -55,7 +55,7 @@ _LIB = os.path.join(_HERE, "libltlt_oracle.so")
 _lock = threading.Lock()
 _lib = None
 
-GCC_FLAGS = ["-O2", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared", "-std=c99"]
+GCC_FLAGS = ["-O2", "-ffp-contract=off", "-fno-fast-math", "-fopenmp", "-fPIC", "-shared", "-std=c99"]
 
 
 def build(force: bool = False) -> str:
@@ -94,8 +94,26 @@ def _load():
             for name in ("oracle_ltlt_batched_f64", "oracle_ltlt_batched_f32"):
                 getattr(lib, name).argtypes = [i64, i64, p, i64, i64, p, i64, p, p]
                 getattr(lib, name).restype = None
+            for name in ("oracle_ltlt_trace_f64", "oracle_ltlt_trace_f32"):
+                getattr(lib, name).argtypes = [i64, p, i64, p, i64, p, p, p]
+                getattr(lib, name).restype = None
+            lib.oracle_set_threads.argtypes = [ctypes.c_int32]
+            lib.oracle_set_threads.restype = None
+            lib.oracle_get_threads.argtypes = []
+            lib.oracle_get_threads.restype = ctypes.c_int32
             _lib = lib
     return _lib
+
+
+def set_threads(t: int) -> None:
+    """Threads for the real rank-2 update (OpenMP over its columns); the
+    results are bitwise the same for any count."""
+    _load().oracle_set_threads(int(t))
+
+
+def get_threads() -> int:
+    """Threads the real rank-2 update will use."""
+    return int(_load().oracle_get_threads())
 
 
 def _sfx(dtype) -> str:
@@ -138,6 +156,30 @@ def ltlt(X: np.ndarray, nsteps: int = -1):
     ipiv = ltlt_colmajor(buf, n, nsteps)
     packed = np.tril(buf.T, -1)
     return np.ascontiguousarray(packed), ipiv
+
+
+def ltlt_trace(X: np.ndarray, nsteps: int = -1):
+    """``ltlt`` that also records each column step's pivot decision (real
+    dtypes only).  Returns ``(packed, ipiv, best, runner, runner_mag)``:
+    ``best[k]`` = |X(p_k, k)| at step k, ``runner[k]`` the first row of the
+    largest magnitude among the other candidate rows (-1 if none) and
+    ``runner_mag[k]`` its magnitude, in the input's precision."""
+    lib = _load()
+    n = X.shape[0]
+    buf = np.ascontiguousarray(X.T)
+    sfx = _sfx(buf.dtype)
+    if sfx not in ("f64", "f32"):
+        raise TypeError("ltlt_trace takes real matrices")
+    ipiv = np.zeros(max(n, 1), dtype=np.int32)
+    ns = max(n - 2, 1)
+    best = np.zeros(ns, dtype=buf.dtype)
+    runner = np.full(ns, -1, dtype=np.int32)
+    rmag = np.zeros(ns, dtype=buf.dtype)
+    getattr(lib, "oracle_ltlt_trace_" + sfx)(n, buf.ctypes.data, n, ipiv.ctypes.data, int(nsteps),
+                                            best.ctypes.data, runner.ctypes.data, rmag.ctypes.data)
+    packed = np.ascontiguousarray(np.tril(buf.T, -1))
+    k = max(n - 2, 0)
+    return packed, ipiv[:n], best[:k], runner[:k], rmag[:k]
 
 
 def pfaffian_packed(packed: np.ndarray, ipiv: np.ndarray):

@@ -10,13 +10,17 @@
  * Complex matrices (complex skew-symmetric, X^T = -X) use the same steps
  * with written-out complex arithmetic (ltlt_oracle_complex.h).
  *
- * Build: gcc -O2 -ffp-contract=off -fno-fast-math -shared -fPIC
+ * Build: gcc -O2 -ffp-contract=off -fno-fast-math -fopenmp -shared -fPIC
  * (no contraction into FMA, no reassociation: every operation rounds once,
- * in the order written).
+ * in the order written).  OpenMP only splits the columns of the real rank-2
+ * update between threads; results do not depend on the thread count.
  */
 #include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 #define CAT_(a, b) a##b
 #define CAT(a, b) CAT_(a, b)
@@ -55,11 +59,38 @@
 #undef FABS
 
 /* Exported entry points (ctypes). */
+void oracle_set_threads(int32_t t)
+{
+#ifdef _OPENMP
+    omp_set_num_threads(t > 0 ? t : 1);
+#else
+    (void)t;
+#endif
+}
+
+int32_t oracle_get_threads(void)
+{
+#ifdef _OPENMP
+    return (int32_t)omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
 void oracle_ltlt_f64(int64_t n, double* A, int64_t lda, int32_t* ipiv, int64_t nsteps)
-{ ltlt_f64(n, A, lda, ipiv, nsteps); }
+{ ltlt_f64(n, A, lda, ipiv, nsteps, NULL, NULL, NULL); }
 
 void oracle_ltlt_f32(int64_t n, float* A, int64_t lda, int32_t* ipiv, int64_t nsteps)
-{ ltlt_f32(n, A, lda, ipiv, nsteps); }
+{ ltlt_f32(n, A, lda, ipiv, nsteps, NULL, NULL, NULL); }
+
+/* The same, recording each step's pivot magnitude and runner-up. */
+void oracle_ltlt_trace_f64(int64_t n, double* A, int64_t lda, int32_t* ipiv, int64_t nsteps,
+                           double* best_mag, int32_t* runner, double* runner_mag)
+{ ltlt_f64(n, A, lda, ipiv, nsteps, best_mag, runner, runner_mag); }
+
+void oracle_ltlt_trace_f32(int64_t n, float* A, int64_t lda, int32_t* ipiv, int64_t nsteps,
+                           float* best_mag, int32_t* runner, float* runner_mag)
+{ ltlt_f32(n, A, lda, ipiv, nsteps, best_mag, runner, runner_mag); }
 
 void oracle_swap_f64(int64_t n, double* A, int64_t lda, int64_t r, int64_t p)
 { swap_indices_f64(n, A, lda, r, p); }
@@ -85,7 +116,7 @@ void oracle_ltlt_batched_f64(int64_t n, int64_t batch, double* A, int64_t lda, i
 {
     int64_t b;
     for (b = 0; b < batch; ++b) {
-        ltlt_f64(n, A + b * strideA, lda, ipiv + b * strideIpiv, -1);
+        ltlt_f64(n, A + b * strideA, lda, ipiv + b * strideIpiv, -1, NULL, NULL, NULL);
         pfaffian_f64(n, A + b * strideA, lda, ipiv + b * strideIpiv, logabs + b, sign + b);
     }
 }
@@ -95,7 +126,7 @@ void oracle_ltlt_batched_f32(int64_t n, int64_t batch, float* A, int64_t lda, in
 {
     int64_t b;
     for (b = 0; b < batch; ++b) {
-        ltlt_f32(n, A + b * strideA, lda, ipiv + b * strideIpiv, -1);
+        ltlt_f32(n, A + b * strideA, lda, ipiv + b * strideIpiv, -1, NULL, NULL, NULL);
         pfaffian_f32(n, A + b * strideA, lda, ipiv + b * strideIpiv, logabs + b, sign + b);
     }
 }

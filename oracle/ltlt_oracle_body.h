@@ -37,6 +37,26 @@ static void CAT(swap_indices, SFX)(int64_t n, REAL* A, int64_t lda, int64_t r, i
     }
 }
 
+/* Skew rank-2 update of the trailing strict lower triangle after column k
+ * is eliminated: X(i, j) += l_i v_j - v_i l_j for i > j >= k+2, with the
+ * multipliers l in column k of A and v = X(k+2:, k+1) copied beforehand.
+ * Columns j are independent (each writes only its own column and reads
+ * column k and v), so they may run on several threads: every entry is still
+ * formed by the same two products and two additions in the same order, and
+ * the result is bitwise the same for any thread count. */
+static void CAT(rank2_update, SFX)(int64_t n, REAL* A, int64_t lda, int64_t k, const REAL* v)
+{
+    int64_t j;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (j = k + 2; j < n; ++j) {
+        const REAL lj = AT(j, k), vj = v[j];
+        int64_t i;
+        for (i = j + 1; i < n; ++i) {
+            AT(i, j) = AT(i, j) + (AT(i, k) * vj - v[i] * lj);
+        }
+    }
+}
+
 /* Unblocked Parlett-Reid reduction with partial pivoting,
  * P X P^T = L T L^T, run for `nsteps` column steps (all n-2 steps when
  * nsteps < 0 or nsteps > n-2).
@@ -51,11 +71,15 @@ static void CAT(swap_indices, SFX)(int64_t n, REAL* A, int64_t lda, int64_t r, i
  *      X(i, j) += l_i v_j - v_i l_j,  v = X(k+2:, k+1)
  *      (column k+1 itself is unchanged because X(k+1, k+1) = 0).
  * On exit A(k+1, k) = alpha_k = T(k+1, k) and A(r, k) = l_r = L(r, k+1) for
- * r >= k+2, with rows of earlier columns carried through later exchanges. */
-static void CAT(ltlt, SFX)(int64_t n, REAL* A, int64_t lda, int32_t* ipiv, int64_t nsteps)
+ * r >= k+2, with rows of earlier columns carried through later exchanges.
+ * When best_mag is not NULL, step k also records |X(p, k)| in best_mag[k] and
+ * the runner-up row and magnitude in runner[k], runner_mag[k] (arrays of
+ * n-2 entries); the factorization itself is the same either way. */
+static void CAT(ltlt, SFX)(int64_t n, REAL* A, int64_t lda, int32_t* ipiv, int64_t nsteps,
+                          REAL* best_mag, int32_t* runner, REAL* runner_mag)
 {
-    int64_t i, j, k, r, p, last;
-    REAL best, alpha;
+    int64_t i, k, r, p, q, last;
+    REAL best, second, alpha;
     REAL* v;
 
     for (i = 0; i < n; ++i) ipiv[i] = (int32_t)i;
@@ -72,6 +96,19 @@ static void CAT(ltlt, SFX)(int64_t n, REAL* A, int64_t lda, int32_t* ipiv, int64
         for (r = k + 2; r < n; ++r) {
             if (FABS(AT(r, k)) > best) { best = FABS(AT(r, k)); p = r; }
         }
+        /* optional record of the decision: the pivot's magnitude and the
+         * runner-up (first index of the largest magnitude among the other
+         * rows; -1 when there is none) */
+        if (best_mag) {
+            q = -1;
+            second = (REAL)0;
+            for (r = k + 1; r < n; ++r) {
+                if (r != p && (q < 0 || FABS(AT(r, k)) > second)) { second = FABS(AT(r, k)); q = r; }
+            }
+            best_mag[k] = best;
+            runner[k] = (int32_t)q;
+            runner_mag[k] = second;
+        }
         /* 2. exchange */
         ipiv[k + 1] = (int32_t)p;
         if (p != k + 1) CAT(swap_indices, SFX)(n, A, lda, k + 1, p);
@@ -80,12 +117,7 @@ static void CAT(ltlt, SFX)(int64_t n, REAL* A, int64_t lda, int32_t* ipiv, int64
         for (r = k + 2; r < n; ++r) AT(r, k) = (alpha != (REAL)0) ? AT(r, k) / alpha : (REAL)0;
         /* 4. skew rank-2 update of the trailing strict lower triangle */
         for (r = k + 2; r < n; ++r) v[r] = AT(r, k + 1);
-        for (j = k + 2; j < n; ++j) {
-            REAL lj = AT(j, k), vj = v[j];
-            for (i = j + 1; i < n; ++i) {
-                AT(i, j) = AT(i, j) + (AT(i, k) * vj - v[i] * lj);
-            }
-        }
+        CAT(rank2_update, SFX)(n, A, lda, k, v);
     }
     free(v);
 }
@@ -135,7 +167,7 @@ static void CAT(pfaffian, SFX)(int64_t n, const REAL* A, int64_t lda, const int3
  * (Pf = 0). */
 static void CAT(pfaffian_direct, SFX)(int64_t n, REAL* A, int64_t lda, int32_t* ipiv, int64_t nsteps)
 {
-    int64_t i, j, k, r, p, done;
+    int64_t i, k, r, p, done;
     REAL best, alpha;
     REAL* v;
 
@@ -155,12 +187,7 @@ static void CAT(pfaffian_direct, SFX)(int64_t n, REAL* A, int64_t lda, int32_t* 
         alpha = AT(k + 1, k);
         for (r = k + 2; r < n; ++r) AT(r, k) = (alpha != (REAL)0) ? AT(r, k) / alpha : (REAL)0;
         for (r = k + 2; r < n; ++r) v[r] = AT(r, k + 1);
-        for (j = k + 2; j < n; ++j) {
-            REAL lj = AT(j, k), vj = v[j];
-            for (i = j + 1; i < n; ++i) {
-                AT(i, j) = AT(i, j) + (AT(i, k) * vj - v[i] * lj);
-            }
-        }
+        CAT(rank2_update, SFX)(n, A, lda, k, v);
     }
     free(v);
 }

@@ -331,3 +331,72 @@ def test_batched_matches_single():
         ref = pf_matchings(Xs[b])
         assert sign[b] == int(np.sign(ref))
         assert logabs[b] == pytest.approx(math.log(abs(ref)), rel=1e-11)
+
+
+# --- threads and the decision trace ---------------------------------------------
+
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+def test_thread_count_does_not_change_bits(dtype):
+    # OpenMP splits the rank-2 update's columns: every entry is still formed by
+    # the same operations in the same order, so any thread count gives the same
+    # bits (checked against one thread, with more threads than columns at the end)
+    X = synth.skew_graded(300, 41).astype(dtype)
+    old = oracle.get_threads()
+    try:
+        oracle.set_threads(1)
+        p1, i1 = oracle.ltlt(X)
+        oracle.set_threads(5)
+        p5, i5 = oracle.ltlt(X)
+        oracle.set_threads(64)
+        p64, i64 = oracle.ltlt(X)
+    finally:
+        oracle.set_threads(old)
+    assert np.array_equal(i1, i5) and np.array_equal(i1, i64)
+    assert np.array_equal(p1.view(np.uint8), p5.view(np.uint8))
+    assert np.array_equal(p1.view(np.uint8), p64.view(np.uint8))
+
+
+def test_trace_worked_example():
+    # column 0 of the worked example is (-1, -2, -3) below row 0: pivot row 3
+    # (|-3|), runner-up row 2 (|-2|); after the exchange and update, column 1
+    # below row 1 is (6, 5): pivot row 2, runner-up row 3
+    g = _golden("ltlt_worked_4x4.txt")
+    X = np.zeros((4, 4))
+    X[np.triu_indices(4, 1)] = [float(x) for x in g["upper"].split()]
+    X = X - X.T
+    packed, ipiv, best, runner, rmag = oracle.ltlt_trace(X)
+    assert list(best) == [3.0, 6.0] and list(runner) == [2, 3] and list(rmag) == [2.0, 5.0]
+    p0, i0 = oracle.ltlt(X)
+    assert np.array_equal(packed, p0) and np.array_equal(ipiv, i0)
+
+
+@pytest.mark.parametrize("gen", ["gauss", "ints"])
+def test_trace_against_columns(gen):
+    # brute force: run the oracle k steps, read column k of the partly reduced
+    # matrix, and rank its magnitudes with a stable sort (first index first)
+    n = 40
+    if gen == "gauss":
+        X = synth.skew_gauss(n, 77)
+    else:
+        U = synth.rng_for(78).integers(-2, 3, size=(n, n)).astype(np.float64)
+        X = synth.skew_from_upper(U)
+    packed, ipiv, best, runner, rmag = oracle.ltlt_trace(X)
+    for k in range(n - 2):
+        pre, _ = oracle.ltlt(X, nsteps=k)
+        col = np.abs(pre[k + 1:, k])
+        order = np.argsort(-col, kind="stable")
+        assert ipiv[k + 1] == k + 1 + order[0]
+        assert best[k] == col[order[0]]
+        assert runner[k] == k + 1 + order[1] and rmag[k] == col[order[1]]
+
+
+def test_trace_smallest_orders():
+    # n = 3: one step with candidate rows 1 and 2; n = 2: no step at all
+    X = synth.skew_gauss(3, 5)
+    _, ipiv, best, runner, rmag = oracle.ltlt_trace(X)
+    a1, a2 = abs(X[1, 0]), abs(X[2, 0])
+    win, lose = (1, 2) if a1 >= a2 else (2, 1)
+    assert ipiv[1] == win and runner[0] == lose
+    assert best[0] == max(a1, a2) and rmag[0] == min(a1, a2)
+    _, _, best2, runner2, _ = oracle.ltlt_trace(synth.skew_gauss(2, 5))
+    assert len(best2) == 0 and len(runner2) == 0
