@@ -34,6 +34,16 @@
  *     LTLT_ERR_UNSUPPORTED when the size cannot be run (e.g. the panel would
  *     need more co-resident workgroups than the device holds).
  *   - Non-finite input gives unspecified factors but every call terminates.
+ *   - Device-side waits.  The panels of ltlt_factor and
+ *     ltlt_pfaffian_direct, and ltlt_solve, run workgroups that wait on each
+ *     other; every wait is bounded (2 s).  When one gives up (a grid that
+ *     could not become resident), the call still runs to its end with every
+ *     access in bounds, but its results are poisoned: the factor columns
+ *     committed after the failure are NaN and ltlt_pfaffian /
+ *     ltlt_pfaffian_direct / ltlt_pfaffian_complex return logabs = NaN with
+ *     sign 0 (phase 0).  The failure is recorded in a sticky per-device flag
+ *     that ltlt_device_status reports (and clears); the return code of an
+ *     asynchronous call cannot carry it.
  */
 #ifndef LTLT_H
 #define LTLT_H
@@ -112,7 +122,7 @@ int ltlt_factor(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, hipSt
  * needs more co-resident workgroups than the device holds (see ltlt_factor);
  * ltlt_factor itself narrows the width instead.
  */
-int ltlt_factor_nb(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, int64_t nb,
+int ltlt_factor_nb(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, int nb,
                    hipStream_t stream);
 
 /*
@@ -171,7 +181,7 @@ int ltlt_pfaffian_complex(int64_t n, const void* A, int64_t lda, int dtype, cons
  * Returns 0, -i when argument i is invalid (nb odd or out of range: -6), or
  * a runtime / device-wait error as ltlt_factor.  Stream-ordered.
  */
-int ltlt_pfaffian_direct(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, int64_t nb,
+int ltlt_pfaffian_direct(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, int nb,
                          double* logabs, int32_t* sign, hipStream_t stream);
 
 /*
@@ -249,11 +259,22 @@ int ltlt_skew_update(int64_t m, void* C, int64_t ldc, const int32_t* perm, int64
 
 /*
  * ltlt_device_status -- synchronizes `stream` and reports whether a
- * device-side bounded wait of an earlier ltlt_factor on this device gave up
- * (LTLT_ERR_DEVICE_TIMEOUT; the factors are then invalid) and clears the flag.
- * Returns 0 when no wait gave up.
+ * device-side bounded wait of any call on the current device gave up since
+ * the last ltlt_device_status (LTLT_ERR_DEVICE_TIMEOUT: the results of that
+ * call are poisoned, see the common rules) and clears that sticky flag.
+ * Returns 0 when no wait gave up, or a HIP runtime error.
  */
 int ltlt_device_status(hipStream_t stream);
+
+/*
+ * ltlt_test_force_timeout -- for tests of the failure path only (host call,
+ * process-wide).  on = 1: every following ltlt_factor, ltlt_pfaffian_direct
+ * and ltlt_solve starts as if one of its device-side waits had already given
+ * up (waits end at their first poll, outputs are poisoned, the sticky flag
+ * is raised), without any kernel waiting for long; on = 0 (the default)
+ * restores normal operation.  Returns 0, or -1 for another value.
+ */
+int ltlt_test_force_timeout(int on);
 
 /*
  * Per-kernel timing of ltlt_factor, measured with HIP events recorded on the

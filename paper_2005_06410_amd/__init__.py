@@ -14,6 +14,13 @@ column-major it would be X^T = -X (same L and P, T negated, Pf times
 
 If the library is not built, or no GPU is visible, every call raises; there
 is no CPU fallback.
+
+Calls are asynchronous.  ``factor``, ``pfaffian_direct`` and ``solve`` run
+device-side waits that are bounded; when one gives up, the results of that
+call are poisoned (NaN factor columns, log|Pf| NaN with sign 0) and a sticky
+per-device flag is raised.  Pass ``check=True`` to synchronize and raise
+``LtltError`` at once, or call ``device_status()`` later: it raises if any
+call since the previous ``device_status()`` failed.
 """
 from __future__ import annotations
 
@@ -29,6 +36,7 @@ __all__ = [
     "factor_batched",
     "skew_update",
     "device_status",
+    "test_force_timeout",
     "profile_enable",
     "profile_read",
     "release_workspace",
@@ -47,7 +55,7 @@ _SYMBOLS = {
     "ltlt_factor": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
                      ctypes.c_void_p], ctypes.c_int),
     "ltlt_factor_nb": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
-                        ctypes.c_int64, ctypes.c_void_p], ctypes.c_int),
+                        ctypes.c_int, ctypes.c_void_p], ctypes.c_int),
     "ltlt_pfaffian": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "ltlt_pfaffian_complex": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
@@ -65,7 +73,8 @@ _SYMBOLS = {
     "ltlt_set_cooperative_panels": ([ctypes.c_int], ctypes.c_int),
     "ltlt_mfma_probe": ([ctypes.c_int, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "ltlt_pfaffian_direct": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
-                              ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
+                              ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
+    "ltlt_test_force_timeout": ([ctypes.c_int], ctypes.c_int),
     "ltlt_solve": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_int64,
                     ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p], ctypes.c_int),
 }
@@ -166,14 +175,15 @@ def _colmajor_lda(A) -> int:
     return A.stride(1)
 
 
-def factor(A, ipiv=None, nb: int | None = None):
+def factor(A, ipiv=None, nb: int | None = None, check: bool = False):
     """In-place P X P^T = L T L^T of the column-major skew matrix ``A``
     (float64, float32, or complex128 / complex64 for a complex X with
     X^T = -X).
 
     Returns the int32 pivot tensor (0-based, LAPACK laswp order).  On return
     A's strict lower triangle holds alpha_k at (k+1, k) and L(r, k+1) at (r, k);
-    its strict upper triangle is never touched."""
+    its strict upper triangle is never touched.  ``check=True`` synchronizes
+    and raises if a device-side wait gave up (see the module docstring)."""
     torch = _torch()
     _require_gpu(A)
     lda = _colmajor_lda(A)
@@ -189,6 +199,8 @@ def factor(A, ipiv=None, nb: int | None = None):
     else:
         code = lib.ltlt_factor_nb(n, A.data_ptr(), lda, _dtype_code(A), ipiv.data_ptr(), int(nb), s)
     _check("ltlt_factor", code)
+    if check:
+        device_status(A.device)
     return ipiv[:n] if ipiv.numel() != n else ipiv
 
 
@@ -216,11 +228,12 @@ def pfaffian(A, ipiv):
     return logabs, sign
 
 
-def pfaffian_direct(A, nb: int = 0, ipiv=None):
+def pfaffian_direct(A, nb: int = 0, ipiv=None, check: bool = False):
     """Pf(X) of the column-major skew matrix ``A`` from the even column steps
     only (see ``ltlt_pfaffian_direct``); ``A`` is used as workspace.
 
-    Returns (ipiv int32 (n,), logabs f64 (1,), sign int32 (1,)) device tensors."""
+    Returns (ipiv int32 (n,), logabs f64 (1,), sign int32 (1,)) device tensors.
+    ``check=True`` synchronizes and raises if a device-side wait gave up."""
     torch = _torch()
     _require_gpu(A)
     lda = _colmajor_lda(A)
@@ -234,12 +247,15 @@ def pfaffian_direct(A, nb: int = 0, ipiv=None):
     code = load().ltlt_pfaffian_direct(n, A.data_ptr(), lda, _dtype_code(A), ipiv.data_ptr(), int(nb),
                                        logabs.data_ptr(), sign.data_ptr(), _stream_ptr(A.device))
     _check("ltlt_pfaffian_direct", code)
+    if check:
+        device_status(A.device)
     return ipiv[:n], logabs, sign
 
 
-def solve(A, ipiv, B):
+def solve(A, ipiv, B, check: bool = False):
     """Overwrite B (column-major n or n x nrhs, same dtype and device as A)
-    with X^{-1} B from ``factor``'s output (see ``ltlt_solve``)."""
+    with X^{-1} B from ``factor``'s output (see ``ltlt_solve``).
+    ``check=True`` synchronizes and raises if a device-side wait gave up."""
     _require_gpu(A)
     _require_gpu(B)
     lda = _colmajor_lda(A)
@@ -264,6 +280,8 @@ def solve(A, ipiv, B):
     code = load().ltlt_solve(n, A.data_ptr(), lda, _dtype_code(A), ipiv.data_ptr(), nrhs, B.data_ptr(), ldb,
                              _stream_ptr(A.device))
     _check("ltlt_solve", code)
+    if check:
+        device_status(A.device)
     return B
 
 
@@ -334,10 +352,20 @@ def skew_update(C, Lx, Bt, perm=None, offset: int = 0):
 
 
 def device_status(device=None):
-    """Synchronize and raise if a device-side bounded wait gave up."""
+    """Synchronize and raise if a device-side bounded wait of any call on the
+    device gave up since the previous ``device_status`` (clears that flag)."""
     torch = _torch()
     lib = load()
-    _check("ltlt_device_status", lib.ltlt_device_status(_stream_ptr(device or torch.cuda.current_device())))
+    dev = device if device is not None else torch.cuda.current_device()
+    with torch.cuda.device(dev):
+        _check("ltlt_device_status", lib.ltlt_device_status(_stream_ptr(dev)))
+
+
+def test_force_timeout(on: bool = True):
+    """Failure-path tests only: while on, every factor / pfaffian_direct /
+    solve call behaves as if a device-side wait had given up at its start
+    (see ``ltlt_test_force_timeout``)."""
+    _check("ltlt_test_force_timeout", load().ltlt_test_force_timeout(1 if on else 0))
 
 
 def profile_enable(on=True):

@@ -35,18 +35,35 @@ struct Workspace {
 std::mutex g_ws_mu;
 std::map<int, Workspace> g_ws;
 
+// The two bounded-wait status words (see raise_wait_status) of the current
+// device; caller holds g_ws_mu.
+hipError_t status_locked(Workspace& w) {
+  if (w.status) return hipSuccess;
+  hipError_t e = hipMalloc(&w.status, 256);
+  if (e != hipSuccess) { w.status = nullptr; return e; }
+  e = hipMemset(w.status, 0, 256);
+  if (e != hipSuccess) { (void)hipFree(w.status); w.status = nullptr; }
+  return e;
+}
+
+hipError_t status_words(int** status) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  e = status_locked(g_ws[dev]);
+  if (e == hipSuccess) *status = g_ws[dev].status;
+  return e;
+}
+
 hipError_t workspace(size_t bytes, void** out, int** status) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   std::lock_guard<std::mutex> lk(g_ws_mu);
   Workspace& w = g_ws[dev];
-  if (!w.status) {
-    e = hipMalloc(&w.status, 256);
-    if (e != hipSuccess) { w.status = nullptr; return e; }
-    e = hipMemset(w.status, 0, 256);
-    if (e != hipSuccess) return e;
-  }
+  e = status_locked(w);
+  if (e != hipSuccess) return e;
   if (w.bytes < bytes) {
     if (w.ptr) {
       e = hipDeviceSynchronize();       // earlier work may still use it
@@ -81,8 +98,10 @@ struct Carve {
 namespace ltlt {
 namespace {
 std::atomic<bool> g_cooperative_panels{false};
+std::atomic<bool> g_forced_timeout{false};
 }  // namespace
 bool cooperative_panels() { return g_cooperative_panels.load(std::memory_order_relaxed); }
+bool forced_timeout() { return g_forced_timeout.load(std::memory_order_relaxed); }
 
 hipError_t ensure_dynamic_lds(const void* kernel, int bytes) {
   static std::mutex mu;
@@ -249,6 +268,8 @@ int factor_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, hipStream
       ua.m = m2;
       ua.perm = Tblk + (int64_t)J * n + i0;
       ua.perm_base = i0;
+      ua.perm_lo = (j + 1) - i0;     // rows held since block start: j+1 .. n-1
+      ua.perm_hi = m2 - 1;
       ua.K = bw + 1;
       ua.Lx = PO + bw;
       ua.ldl = ldw;
@@ -261,7 +282,7 @@ int factor_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, hipStream
     }
     {
       ProfScope ps(2, 0.0, s);
-      e = launch_commit<T>(A, lda, n, j, bw, PO, ldw, al, s);
+      e = launch_commit<T>(A, lda, n, j, bw, PO, ldw, al, status, s);
     }
     if (e != hipSuccess) return hip_err(e);
   }
@@ -291,7 +312,7 @@ int pfaffian_direct_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, 
     int* status = nullptr;
     e = workspace(256, &ws, &status);
     if (e == hipSuccess && n > 0) e = launch_init(ipiv, n, status, s);
-    if (e == hipSuccess) e = launch_pfaffian<T>(n, A, lda, ipiv, logabs, sign, s);
+    if (e == hipSuccess) e = launch_pfaffian<T>(n, A, lda, ipiv, logabs, sign, status, s);
     return e == hipSuccess ? 0 : hip_err(e);
   }
   const int bw0 = std::min(nb, n);
@@ -355,6 +376,8 @@ int pfaffian_direct_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, 
       ua.m = m2;
       ua.perm = Tperm + i0;
       ua.perm_base = i0;
+      ua.perm_lo = (j + 1) - i0;
+      ua.perm_hi = m2 - 1;
       ua.K = bw;
       ua.Lx = PO;
       ua.ldl = ldw;
@@ -367,13 +390,13 @@ int pfaffian_direct_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, 
     }
     {
       ProfScope ps(2, 0.0, s);
-      e = launch_pair_commit<T>(A, lda, j, bw / 2, al, s);
+      e = launch_pair_commit<T>(A, lda, j, bw / 2, al, status, s);
     }
     if (e != hipSuccess) return hip_err(e);
   }
   {
     ProfScope ps(3, 0.0, s);
-    e = launch_pfaffian<T>(n, A, lda, ipiv, logabs, sign, s);
+    e = launch_pfaffian<T>(n, A, lda, ipiv, logabs, sign, status, s);
   }
   return e == hipSuccess ? 0 : hip_err(e);
 }
@@ -489,6 +512,8 @@ int factor_complex_impl(int64_t n64, void* A, int64_t lda, int32_t* ipiv, int nb
         ua.m = m2;
         ua.perm = Tblk + (int64_t)J * n + i0;
         ua.perm_base = i0;
+        ua.perm_lo = (j + 1) - i0;
+        ua.perm_hi = m2 - 1;
         ua.K = 2 * K;
         ua.Lx = LL + (plane == 0 ? 0 : (int64_t)K * ldw) + bw;
         ua.ldl = ldw;
@@ -502,8 +527,8 @@ int factor_complex_impl(int64_t n64, void* A, int64_t lda, int32_t* ipiv, int nb
     }
     {
       ProfScope ps(2, 0.0, s);
-      e = launch_commit<T>(Pr, ldw, n, j, bw, LL, ldw, alr, s);
-      if (e == hipSuccess) e = launch_commit<T>(Pi, ldw, n, j, bw, LL + (int64_t)K * ldw, ldw, ali, s);
+      e = launch_commit<T>(Pr, ldw, n, j, bw, LL, ldw, alr, status, s);
+      if (e == hipSuccess) e = launch_commit<T>(Pi, ldw, n, j, bw, LL + (int64_t)K * ldw, ldw, ali, status, s);
     }
     if (e != hipSuccess) return hip_err(e);
   }
@@ -524,7 +549,7 @@ int factor_complex_impl(int64_t n64, void* A, int64_t lda, int32_t* ipiv, int nb
 
 extern "C" {
 
-int ltlt_factor_nb(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, int64_t nb, hipStream_t stream) {
+int ltlt_factor_nb(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, int nb, hipStream_t stream) {
   if (n < 0 || n > (int64_t)INT32_MAX / 2) return -1;
   if (A == nullptr && n > 0) return -2;
   if (lda < std::max<int64_t>(1, n)) return -3;
@@ -544,7 +569,7 @@ int ltlt_factor(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, hipSt
   // width needs more workgroups than the device holds, halve it (the size
   // checks come before any allocation or launch, so a refused width leaves
   // nothing behind).
-  int64_t nb = is_complex(dtype) ? kDefaultComplexNb : kDefaultNb;
+  int nb = is_complex(dtype) ? kDefaultComplexNb : kDefaultNb;
   int r = ltlt_factor_nb(n, A, lda, dtype, ipiv, nb, stream);
   while (r == LTLT_ERR_UNSUPPORTED && nb > kMinFallbackNb && n < kMaxOrder) {
     nb /= 2;
@@ -562,8 +587,11 @@ int ltlt_pfaffian_complex(int64_t n, const void* A, int64_t lda, int dtype, cons
   if (ipiv == nullptr && n > 0) return -5;
   if (logabs == nullptr) return -6;
   if (phase == nullptr) return -7;
-  hipError_t e = dtype == LTLT_C128 ? launch_cpfaffian<double>((int)n, A, lda, ipiv, logabs, phase, stream)
-                                    : launch_cpfaffian<float>((int)n, A, lda, ipiv, logabs, phase, stream);
+  int* status = nullptr;
+  hipError_t e = status_words(&status);
+  if (e != hipSuccess) return hip_err(e);
+  e = dtype == LTLT_C128 ? launch_cpfaffian<double>((int)n, A, lda, ipiv, logabs, phase, status, stream)
+                         : launch_cpfaffian<float>((int)n, A, lda, ipiv, logabs, phase, status, stream);
   return e == hipSuccess ? 0 : hip_err(e);
 }
 
@@ -576,15 +604,17 @@ int ltlt_pfaffian(int64_t n, const void* A, int64_t lda, int dtype, const int32_
   if (ipiv == nullptr && n > 0) return -5;
   if (logabs == nullptr) return -6;
   if (sign == nullptr) return -7;
-  hipError_t e;
+  int* status = nullptr;
+  hipError_t e = status_words(&status);
+  if (e != hipSuccess) return hip_err(e);
   if (dtype == LTLT_F64)
-    e = launch_pfaffian<double>((int)n, static_cast<const double*>(A), lda, ipiv, logabs, sign, stream);
+    e = launch_pfaffian<double>((int)n, static_cast<const double*>(A), lda, ipiv, logabs, sign, status, stream);
   else
-    e = launch_pfaffian<float>((int)n, static_cast<const float*>(A), lda, ipiv, logabs, sign, stream);
+    e = launch_pfaffian<float>((int)n, static_cast<const float*>(A), lda, ipiv, logabs, sign, status, stream);
   return e == hipSuccess ? 0 : hip_err(e);
 }
 
-int ltlt_pfaffian_direct(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, int64_t nb, double* logabs,
+int ltlt_pfaffian_direct(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, int nb, double* logabs,
                          int32_t* sign, hipStream_t stream) {
   if (n < 0 || n > (int64_t)INT32_MAX / 2) return -1;
   if (A == nullptr && n > 0) return -2;
@@ -596,7 +626,7 @@ int ltlt_pfaffian_direct(int64_t n, void* A, int64_t lda, int dtype, int32_t* ip
   if (nb < 2 || nb > kMaxNb || (nb & 1)) return -6;
   if (logabs == nullptr) return -7;
   if (sign == nullptr) return -8;
-  auto run = [&](int64_t w) {
+  auto run = [&](int w) {
     return dtype == LTLT_F64
                ? pfaffian_direct_impl<double>(n, static_cast<double*>(A), lda, ipiv, (int)w, logabs, sign, stream)
                : pfaffian_direct_impl<float>(n, static_cast<float*>(A), lda, ipiv, (int)w, logabs, sign, stream);
@@ -704,6 +734,7 @@ int ltlt_skew_update(int64_t m, void* C, int64_t ldc, const int32_t* perm, int64
   if (m < 2) return 0;
   UpdateArgs ua{};
   ua.C = C; ua.ldc = ldc; ua.m = (int)m; ua.perm = perm; ua.perm_base = 0;
+  ua.perm_lo = INT32_MIN; ua.perm_hi = INT32_MAX;   // the caller's sources, as given
   ua.K = (int)K; ua.Lx = Lx; ua.ldl = ldl; ua.Bt = Bt; ua.ldb = ldb;
   hipError_t e = dtype == LTLT_F64 ? launch_update<double>(ua, stream) : launch_update<float>(ua, stream);
   return e == hipSuccess ? 0 : hip_err(e);
@@ -722,14 +753,21 @@ int ltlt_device_status(hipStream_t stream) {
     if (it == g_ws.end() || !it->second.status) return 0;
     st = it->second.status;
   }
+  // the sticky word: raised by any wait that gave up since the last read
   int h = 0;
-  e = hipMemcpy(&h, st, sizeof(int), hipMemcpyDeviceToHost);
+  e = hipMemcpy(&h, st + 1, sizeof(int), hipMemcpyDeviceToHost);
   if (e != hipSuccess) return hip_err(e);
   if (h != 0) {
-    e = hipMemset(st, 0, sizeof(int));
+    e = hipMemset(st + 1, 0, sizeof(int));
     if (e != hipSuccess) return hip_err(e);
     return LTLT_ERR_DEVICE_TIMEOUT;
   }
+  return 0;
+}
+
+int ltlt_test_force_timeout(int on) {
+  if (on != 0 && on != 1) return -1;
+  ltlt::g_forced_timeout.store(on == 1, std::memory_order_relaxed);
   return 0;
 }
 

@@ -24,42 +24,54 @@
 
 namespace ltlt {
 
-__global__ void init_kernel(int* ipiv, int n, int* status) {
+// status[0] (this call's abort flag) starts cleared; with `force` both words
+// are raised instead, as if a wait had already given up (the host-side switch
+// that tests the failure path without any kernel waiting for long).
+__global__ void init_kernel(int* ipiv, int n, int* status, int force) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = t; i < n; i += stride) ipiv[i] = (int)i;
-  if (t == 0) status[0] = 0;
+  if (t == 0) {
+    status[0] = force;
+    if (force) status[1] = 1;
+  }
 }
 
 hipError_t launch_init(int* ipiv, int n, int* status, hipStream_t s) {
   int blocks = (int)((n + 255) / 256);
   if (blocks < 1) blocks = 1;
   if (blocks > 1024) blocks = 1024;
-  hipLaunchKernelGGL(init_kernel, dim3(blocks), dim3(256), 0, s, ipiv, n, status);
+  hipLaunchKernelGGL(init_kernel, dim3(blocks), dim3(256), 0, s, ipiv, n, status, forced_timeout() ? 1 : 0);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
+// After a panel whose wait gave up (status[0] raised) the block's outputs were
+// never formed: NaN is committed instead, so that no aborted call leaves
+// plausible factors behind.
 template <typename T>
-__global__ void commit_kernel(T* A, int64_t lda, int n, int j, int bw, const T* PO, int64_t ldw, const T* alpha) {
+__global__ void commit_kernel(T* A, int64_t lda, int n, int j, int bw, const T* PO, int64_t ldw, const T* alpha,
+                              const int* status) {
   const int u = blockIdx.y;                   // 0..bw (bw = carry column)
   const int col = j + u;
+  const bool failed = status[0] != 0;
   for (int i = col + 1 + blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
     T v;
     if (u < bw && i == col + 1) v = alpha[u];
     else v = PO[(int64_t)(i - (j + 1)) + (int64_t)u * ldw];
-    A[(int64_t)i + (int64_t)col * lda] = v;
+    A[(int64_t)i + (int64_t)col * lda] = failed ? T(NAN) : v;
   }
 }
 
 template <typename T>
 hipError_t launch_commit(T* A, int64_t lda, int n, int j, int bw, const T* PO, int64_t ldw, const T* alpha,
-                         hipStream_t s) {
+                         const int* status, hipStream_t s) {
   const int rows = n - (j + 1);
   if (rows <= 0) return hipSuccess;
   int bx = (rows + 255) / 256;
   if (bx > 64) bx = 64;
-  hipLaunchKernelGGL(commit_kernel<T>, dim3(bx, bw + 1), dim3(256), 0, s, A, lda, n, j, bw, PO, ldw, alpha);
+  hipLaunchKernelGGL(commit_kernel<T>, dim3(bx, bw + 1), dim3(256), 0, s, A, lda, n, j, bw, PO, ldw, alpha,
+                     status);
   return hipGetLastError();
 }
 
@@ -67,13 +79,17 @@ hipError_t launch_commit(T* A, int64_t lda, int n, int j, int bw, const T* PO, i
 // Blocks are uniform: block J starts at column J*nb.
 // Tblk[J*n + i] = index held at the start of block J by position i (i > J*nb);
 // G[J*n + i] = source row of position i for the columns of block J (J < nblk-1).
+// Every looked-up index is clamped into the positions of its block,
+// [nxt*nb + 1, n): a complete block order is unchanged by that, and an order
+// left unfinished by a panel that gave up (status raised) cannot send a later
+// lookup, or perm_apply's gather, out of bounds.
 __global__ void perm_chain_kernel(const int* Tblk, int nb, int nblk, int n, int* G) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   int g = i;
   for (int J = nblk - 2; J >= 0; --J) {
     const int nxt = J + 1;
-    if (g > nxt * nb) g = Tblk[(int64_t)nxt * n + g];
+    if (g > nxt * nb) g = min(max(Tblk[(int64_t)nxt * n + g], nxt * nb + 1), n - 1);
     G[(int64_t)J * n + i] = g;
   }
 }
@@ -122,7 +138,7 @@ __global__ void __launch_bounds__(256) perm_apply_kernel(T* A, int64_t lda, int 
 #pragma unroll
       for (int e = 0; e < kU; ++e) {
         const int i = i0 + e * blockDim.x;
-        src[e] = g[i < len ? i : 0] - r0;
+        src[e] = min(max(g[i < len ? i : 0] - r0, 0), len - 1);   // in the column whatever G holds
       }
 #pragma unroll
       for (int e = 0; e < kU; ++e) {
@@ -157,9 +173,11 @@ hipError_t launch_perm_apply(T* A, int64_t lda, int n, const int* G, int nb, int
 }
 
 // ---------------------------------------------------------------------------
+// A raised abort flag (status[0]: a wait of the last factorization gave up)
+// gives log|Pf| = NaN and sign 0.
 template <typename T>
 __global__ void __launch_bounds__(1024) pfaffian_kernel(int n, const T* A, int64_t lda, const int* ipiv,
-                                                        double* logabs, int* sign) {
+                                                        double* logabs, int* sign, const int* status) {
   __shared__ double s_log[1024];
   __shared__ int s_neg[1024], s_zero[1024];
   const int tid = threadIdx.x;
@@ -189,23 +207,26 @@ __global__ void __launch_bounds__(1024) pfaffian_kernel(int n, const T* A, int64
     __syncthreads();
   }
   if (tid == 0) {
-    if (n & 1 || s_zero[0]) { *logabs = -INFINITY; *sign = 0; }
+    if (status[0] != 0) { *logabs = NAN; *sign = 0; }
+    else if (n & 1 || s_zero[0]) { *logabs = -INFINITY; *sign = 0; }
     else { *logabs = s_log[0]; *sign = s_neg[0] ? -1 : 1; }
   }
 }
 
 template <typename T>
 hipError_t launch_pfaffian(int n, const T* A, int64_t lda, const int* ipiv, double* logabs, int* sign,
-                           hipStream_t s) {
-  hipLaunchKernelGGL(pfaffian_kernel<T>, dim3(1), dim3(1024), 0, s, n, A, lda, ipiv, logabs, sign);
+                           const int* status, hipStream_t s) {
+  hipLaunchKernelGGL(pfaffian_kernel<T>, dim3(1), dim3(1024), 0, s, n, A, lda, ipiv, logabs, sign, status);
   return hipGetLastError();
 }
 
 #define LTLT_INST(T)                                                                                         \
-  template hipError_t launch_commit<T>(T*, int64_t, int, int, int, const T*, int64_t, const T*, hipStream_t); \
+  template hipError_t launch_commit<T>(T*, int64_t, int, int, int, const T*, int64_t, const T*, const int*,   \
+                                      hipStream_t);                                                         \
   template hipError_t launch_perm_apply<T>(T*, int64_t, int, const int*, int, int, T*, hipStream_t);        \
   template size_t perm_stage_elems<T>(int, int);                                                            \
-  template hipError_t launch_pfaffian<T>(int, const T*, int64_t, const int*, double*, int*, hipStream_t);
+  template hipError_t launch_pfaffian<T>(int, const T*, int64_t, const int*, double*, int*, const int*,     \
+                                         hipStream_t);
 LTLT_INST(double)
 LTLT_INST(float)
 #undef LTLT_INST

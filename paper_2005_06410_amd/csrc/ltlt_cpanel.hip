@@ -446,9 +446,10 @@ hipError_t launch_cplx_merge(int n, void* A, int64_t lda, const T* Pr, const T* 
 // |z| by hypot) and the phase Pf/|Pf| = det(P) prod_j (-alpha_{2j})/|alpha_{2j}|,
 // both by one fixed-order tree reduction (sums of logs, products of unit
 // complex numbers).
+// A raised abort flag (status[0]) gives log|Pf| = NaN and phase 0.
 template <typename T>
 __global__ void __launch_bounds__(1024) cpfaffian_kernel(int n, const T* A, int64_t lda, const int* ipiv,
-                                                         double* logabs, double* phase) {
+                                                         double* logabs, double* phase, const int* status) {
   __shared__ double s_log[1024], s_pr[1024], s_pi[1024];
   __shared__ int s_zero[1024];
   const int tid = threadIdx.x;
@@ -486,7 +487,8 @@ __global__ void __launch_bounds__(1024) cpfaffian_kernel(int n, const T* A, int6
     __syncthreads();
   }
   if (tid == 0) {
-    if ((n & 1) || s_zero[0]) { *logabs = -INFINITY; phase[0] = 0.0; phase[1] = 0.0; }
+    if (status[0] != 0) { *logabs = NAN; phase[0] = 0.0; phase[1] = 0.0; }
+    else if ((n & 1) || s_zero[0]) { *logabs = -INFINITY; phase[0] = 0.0; phase[1] = 0.0; }
     else {
       // renormalise the product of unit factors (rounding drift only)
       const double m = hypot(s_pr[0], s_pi[0]);
@@ -499,9 +501,9 @@ __global__ void __launch_bounds__(1024) cpfaffian_kernel(int n, const T* A, int6
 
 template <typename T>
 hipError_t launch_cpfaffian(int n, const void* A, int64_t lda, const int* ipiv, double* logabs, double* phase,
-                            hipStream_t s) {
+                            const int* status, hipStream_t s) {
   hipLaunchKernelGGL(cpfaffian_kernel<T>, dim3(1), dim3(1024), 0, s, n, static_cast<const T*>(A), lda, ipiv, logabs,
-                     phase);
+                     phase, status);
   return hipGetLastError();
 }
 
@@ -511,7 +513,8 @@ hipError_t launch_cpfaffian(int n, const void* A, int64_t lda, const int* ipiv, 
   template hipError_t launch_cpanel<T>(const CPanelArgs&, size_t, hipStream_t);                             \
   template hipError_t launch_cplx_split<T>(int, const void*, int64_t, T*, T*, int64_t, hipStream_t);        \
   template hipError_t launch_cplx_merge<T>(int, void*, int64_t, const T*, const T*, int64_t, hipStream_t);  \
-  template hipError_t launch_cpfaffian<T>(int, const void*, int64_t, const int*, double*, double*, hipStream_t);
+  template hipError_t launch_cpfaffian<T>(int, const void*, int64_t, const int*, double*, double*, const int*,  \
+                                          hipStream_t);
 LTLT_CINST(double)
 LTLT_CINST(float)
 #undef LTLT_CINST

@@ -42,6 +42,19 @@ __device__ __forceinline__ void wait_stores() {
 __device__ __forceinline__ uint64_t wall_ticks() { return __builtin_amdgcn_s_memrealtime(); }
 constexpr uint64_t kWaitLimitTicks = 200000000ull;   // 2 s at 100 MHz
 
+// Bounded-wait status, two words per device:
+//   status[0]  this call's abort flag: cleared when a call starts, raised when
+//              one of its waits gives up; every later wait of the call gives up
+//              at once, and the kernels that write results (commit, Pfaffian)
+//              write NaN / sign 0 instead;
+//   status[1]  sticky: raised together with status[0], cleared only when the
+//              host reads it (ltlt_device_status), so a failed call is seen
+//              even if later calls succeed.
+__device__ __forceinline__ void raise_wait_status(int* status) {
+  atomicOr(status, 1);
+  atomicOr(status + 1, 1);
+}
+
 // (|value|, index) pair reduction: larger magnitude wins, ties go to the
 // smaller index.  Magnitudes are compared as doubles (exact for fp32 input).
 __device__ __forceinline__ void argmax_merge(double& bv, int& bi, double ov, int oi) {

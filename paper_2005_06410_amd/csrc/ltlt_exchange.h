@@ -78,8 +78,8 @@ __device__ __forceinline__ T part_sum(T v) {
 // reduces them (largest magnitude, then smallest position); the result lands
 // in s_p (pivot position), s_posw (its block-start index) and s_alpha
 // (signed pivot value; NaN and p = k+1 when no finite candidate exists),
-// handed to the other waves by a barrier.  A wait that exceeds its bound sets
-// the status flag and s_abort.
+// handed to the other waves by a barrier.  A wait that exceeds its bound, or
+// finds the call's abort flag raised, raises the status words and s_abort.
 __device__ __forceinline__ void exchange_publish(const PanelArgs& a, int s, int wave, int lane, int w,
                                                  const double* red_v, const uint64_t* red_k) {
   uint64_t* recs = a.rec + (size_t)(s & 1) * (size_t)a.nrec * kRecStride;
@@ -131,11 +131,13 @@ __device__ __forceinline__ void exchange_collect(const PanelArgs& a, int s, int 
         const int u = q * kWave + lane;
         if (q < q_n && u < P) ok = ok && rec_valid(ra[q], rb[q], s);
       }
-      if (__ballot(!ok) == 0) break;
-      if (stv != 0 || wall_ticks() - t0 > kWaitLimitTicks) {
-        if (lane == 0) { atomicOr(a.status, 1); s_abort = 1; }
+      // a wait of this call that gave up elsewhere ends this one too, even
+      // when every record has arrived
+      if (stv != 0 || (__ballot(!ok) != 0 && wall_ticks() - t0 > kWaitLimitTicks)) {
+        if (lane == 0) { raise_wait_status(a.status); s_abort = 1; }
         break;
       }
+      if (__ballot(!ok) == 0) break;
       __builtin_amdgcn_s_sleep(0);
     }
     double gv = -1.0;

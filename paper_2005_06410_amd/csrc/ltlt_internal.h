@@ -41,6 +41,7 @@ struct UpdateArgs {
   int m;
   const int* perm;    // source index per row/column (minus perm_base), or nullptr
   int perm_base;
+  int perm_lo, perm_hi;   // relative sources are clamped into [perm_lo, perm_hi]
   int K;
   const void* Lx;
   int64_t ldl;
@@ -74,16 +75,19 @@ template <typename T> size_t panel_lds_bytes(int bw, int R);
 template <typename T> hipError_t launch_update(const UpdateArgs& a, hipStream_t s);
 
 template <typename T> hipError_t launch_commit(T* A, int64_t lda, int n, int j, int bw, const T* PO,
-                                               int64_t ldw, const T* alpha, hipStream_t s);
+                                               int64_t ldw, const T* alpha, const int* status, hipStream_t s);
 template <typename T> hipError_t launch_perm_apply(T* A, int64_t lda, int n, const int* G, int nb, int c_end,
                                                    T* stage, hipStream_t s);
 template <typename T> size_t perm_stage_elems(int n, int c_end);
 template <typename T> hipError_t launch_pfaffian(int n, const T* A, int64_t lda, const int* ipiv, double* logabs,
-                                                 int* sign, hipStream_t s);
+                                                 int* sign, const int* status, hipStream_t s);
 template <typename T> hipError_t launch_batched(int n, int batch, T* A, int64_t lda, int64_t strideA, int* ipiv,
                                                 int64_t strideIpiv, double* logabs, int* sign, hipStream_t s);
 
 hipError_t launch_init(int* ipiv, int n, int* status, hipStream_t s);
+// Host-side switch for the failure-path test: while set, every call's init
+// raises the status words as if a wait had given up (ltlt_test_force_timeout).
+bool forced_timeout();
 // Raises a kernel's dynamic-LDS limit to `bytes` on the current device, once
 // per (kernel, device): the attribute is per device.  Thread-safe.
 hipError_t ensure_dynamic_lds(const void* kernel, int bytes);
@@ -117,7 +121,7 @@ template <typename T> hipError_t launch_cplx_split(int n, const void* A, int64_t
 template <typename T> hipError_t launch_cplx_merge(int n, void* A, int64_t lda, const T* Pr, const T* Pi,
                                                    int64_t ldp, hipStream_t s);
 template <typename T> hipError_t launch_cpfaffian(int n, const void* A, int64_t lda, const int* ipiv,
-                                                  double* logabs, double* phase, hipStream_t s);
+                                                  double* logabs, double* phase, const int* status, hipStream_t s);
 
 // Solve with the factors.
 constexpr int kSolveRhs = 8;                    // right-hand sides per pass
@@ -145,6 +149,7 @@ int pair_panel_rows(int bw);                     // rows per pair-panel workgrou
 template <typename T> size_t pair_lds_bytes(int bw, int R);
 template <typename T> int pair_max_blocks(int bw, size_t lds);
 template <typename T> hipError_t launch_pair_panel(const PanelArgs& a, size_t lds, hipStream_t s);
-template <typename T> hipError_t launch_pair_commit(T* A, int64_t lda, int j, int nt, const T* alpha, hipStream_t s);
+template <typename T> hipError_t launch_pair_commit(T* A, int64_t lda, int j, int nt, const T* alpha,
+                                                    const int* status, hipStream_t s);
 
 }  // namespace ltlt

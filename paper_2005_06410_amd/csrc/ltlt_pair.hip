@@ -443,17 +443,18 @@ int pair_max_blocks(int bw, size_t lds) {
 }
 
 // alpha_k of the block's steps into A(k+1, k) (after the block's trailing
-// update, which may still read the block's original entries).
+// update, which may still read the block's original entries); NaN when a
+// wait of this call gave up (status[0] raised).
 template <typename T>
-__global__ void pair_commit_kernel(T* A, int64_t lda, int j, int nt, const T* alpha) {
+__global__ void pair_commit_kernel(T* A, int64_t lda, int j, int nt, const T* alpha, const int* status) {
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
-  if (t < nt) A[(int64_t)(j + 2 * t + 1) + (int64_t)(j + 2 * t) * lda] = alpha[t];
+  if (t < nt) A[(int64_t)(j + 2 * t + 1) + (int64_t)(j + 2 * t) * lda] = status[0] != 0 ? T(NAN) : alpha[t];
 }
 
 template <typename T>
-hipError_t launch_pair_commit(T* A, int64_t lda, int j, int nt, const T* alpha, hipStream_t s) {
+hipError_t launch_pair_commit(T* A, int64_t lda, int j, int nt, const T* alpha, const int* status, hipStream_t s) {
   if (nt <= 0) return hipSuccess;
-  hipLaunchKernelGGL(pair_commit_kernel<T>, dim3((nt + 255) / 256), dim3(256), 0, s, A, lda, j, nt, alpha);
+  hipLaunchKernelGGL(pair_commit_kernel<T>, dim3((nt + 255) / 256), dim3(256), 0, s, A, lda, j, nt, alpha, status);
   return hipGetLastError();
 }
 
@@ -463,7 +464,7 @@ template int pair_max_blocks<double>(int, size_t);
 template int pair_max_blocks<float>(int, size_t);
 template hipError_t launch_pair_panel<double>(const PanelArgs&, size_t, hipStream_t);
 template hipError_t launch_pair_panel<float>(const PanelArgs&, size_t, hipStream_t);
-template hipError_t launch_pair_commit<double>(double*, int64_t, int, int, const double*, hipStream_t);
-template hipError_t launch_pair_commit<float>(float*, int64_t, int, int, const float*, hipStream_t);
+template hipError_t launch_pair_commit<double>(double*, int64_t, int, int, const double*, const int*, hipStream_t);
+template hipError_t launch_pair_commit<float>(float*, int64_t, int, int, const float*, const int*, hipStream_t);
 
 }  // namespace ltlt

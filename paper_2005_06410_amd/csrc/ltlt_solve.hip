@@ -399,7 +399,7 @@ __device__ __forceinline__ bool wait_box(const SolveTriArgs& a, int sb, T* yc, i
     if (vote.all(ok, wave, lane)) return true;
     const bool late = tid == 0 && (st != 0 || wall_ticks() - t0 > kWaitLimitTicks);
     if (!vote.all(!late, wave, lane)) {
-      if (tid == 0) atomicOr(a.status, 1);
+      if (tid == 0) raise_wait_status(a.status);
       return false;
     }
   }
@@ -420,7 +420,7 @@ __device__ __forceinline__ bool wait_words(const SolveTriArgs& a, int sb, int q,
     if (__ballot(!ok) == 0) return true;
     const int late = __builtin_amdgcn_readfirstlane((st != 0 || wall_ticks() - t0 > kWaitLimitTicks) ? 1 : 0);
     if (late) {
-      if (lane == 0) atomicOr(a.status, 1);
+      if (lane == 0) raise_wait_status(a.status);
       return false;
     }
   }

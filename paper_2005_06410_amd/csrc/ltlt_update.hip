@@ -263,9 +263,13 @@ __global__ void __launch_bounds__(kThreads, kUpdateWgPerCu) update_kernel(Update
     store_chunk<T>(Bs[0], rb, tid);
   }
   if (tid < kMT) {
+    // sources clamped into the caller's range (in the factorization, the
+    // positions held since block start): a complete order is unchanged, and
+    // one left unfinished by a panel that gave up cannot take the gather
+    // outside the matrix
     const int ri = r0 + tid, ci = c0 + tid;
-    prow[tid] = (a.perm && ri < m) ? a.perm[ri] - a.perm_base : ri;
-    pcol[tid] = (a.perm && ci < m) ? a.perm[ci] - a.perm_base : ci;
+    prow[tid] = (a.perm && ri < m) ? min(max(a.perm[ri] - a.perm_base, a.perm_lo), a.perm_hi) : ri;
+    pcol[tid] = (a.perm && ci < m) ? min(max(a.perm[ci] - a.perm_base, a.perm_lo), a.perm_hi) : ci;
   }
   if constexpr (DMA) __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0): this wave's chunk copies landed
   __syncthreads();

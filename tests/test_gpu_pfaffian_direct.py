@@ -129,27 +129,6 @@ def test_parity_fp32(n, nb):
     assert abs(logabs - ref_l64) <= 1e-4 * max(abs(ref_l64), 1.0)
 
 
-def test_full_size_n16384():
-    """The configuration bench.py times (n = 16384 Gaussian, nb = 128): the
-    first even steps against the oracle run for those steps only (pivots
-    exact, alpha within 1e-10), and the Pfaffian against the full
-    factorization's on the same input."""
-    n, steps = 16384, 4
-    X = synth.skew_gauss(n, 5)
-    ipiv, alpha, logabs, sign, _ = gpu_direct(X, 128)
-    buf = np.ascontiguousarray(X.T)
-    ref_ipiv = oracle.pfaffian_direct_colmajor(buf, n, steps)
-    ref_alpha = np.array([buf[k, k + 1] for k in range(0, 2 * steps, 2)])   # buf[c, r] = A(r, c)
-    assert np.array_equal(ipiv[:2 * steps], ref_ipiv[:2 * steps])
-    assert np.abs(alpha[:steps] - ref_alpha).max() <= 1e-10 * np.abs(ref_alpha).max()
-    flat, A = device_colmajor(X)
-    fip = lt().factor(A, nb=128)
-    fl, fs = lt().pfaffian(A, fip)
-    torch.cuda.synchronize()
-    assert sign == int(fs.item())
-    assert abs(logabs - float(fl.item())) <= 1e-9 * abs(logabs)
-
-
 def test_large_order_default_width_fallback():
     """n = 60000 is past what the default width's pair panel holds on one
     device (256 workgroups x 224 rows): the default call narrows the width.
