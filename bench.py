@@ -9,13 +9,15 @@ device copy (outside the timed events: the factorization works in place).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--nb 128]
                        [--n 16384] [--dtype f64|f32] [--no-cpu-baseline]
-                       [--workload factor|batched|pfaffian|solve|complex] [--nrhs R]
+                       [--workload factor|batched|pfaffian|solve|complex|cpu-oracle] [--nrhs R]
 Prints one JSON line.  `--workload batched` instead times the batched path
 (8192 independent n=64 matrices, factors + Pfaffians) against HBM bandwidth;
 `--workload pfaffian` the Pfaffian by the even column steps alone;
 `--workload solve` the solve X x = b with the factors (R right-hand sides)
 against HBM bandwidth; `--workload complex` the factorization + Pfaffian of a
-complex128 (or, with --dtype f32, complex64) skew-symmetric matrix.
+complex128 (or, with --dtype f32, complex64) skew-symmetric matrix;
+`--workload cpu-oracle` runs the whole CPU oracle at --n on the host's cores
+(no GPU) and prints its rate.
 """
 from __future__ import annotations
 
@@ -44,7 +46,8 @@ def parse():
     ap.add_argument("--seed", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--workload", choices=["factor", "batched", "pfaffian", "solve", "complex"], default="factor")
+    ap.add_argument("--workload", choices=["factor", "batched", "pfaffian", "solve", "complex", "cpu-oracle"],
+                    default="factor")
     ap.add_argument("--nrhs", type=int, default=1)
     ap.add_argument("--batch", type=int, default=8192)
     ap.add_argument("--input", choices=["gauss", "graded", "blockdiag4"], default="gauss",
@@ -53,34 +56,111 @@ def parse():
     return ap.parse_args()
 
 
+def host_info():
+    """The host the CPU baseline ran on: logical CPUs, the CPUs this process
+    may use, the CPU model and OMP_NUM_THREADS."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "cpus_allowed": len(os.sched_getaffinity(0)), "cpu_model": model,
+            "omp_num_threads": os.environ.get("OMP_NUM_THREADS")}
+
+
+def oracle_threads():
+    """Threads for the oracle's OpenMP loop: OMP_NUM_THREADS when set (the
+    share of the host this process is given), else every CPU it may use."""
+    v = os.environ.get("OMP_NUM_THREADS", "")
+    return int(v) if v.isdigit() and int(v) > 0 else len(os.sched_getaffinity(0))
+
+
+def _oracle_prefix_rate(buf, n, target_s, threads):
+    """Run the oracle's first column steps on a copy of ``buf`` with
+    ``threads`` threads, about ``target_s`` seconds; returns (steps, seconds,
+    nominal flops) with step k counting (n-k-2)^2 (the n^3/3 convention)."""
+    import oracle
+    oracle.set_threads(threads)
+    b = buf.copy()
+    t0 = time.perf_counter()
+    oracle.ltlt_colmajor(b, n, 4)                     # calibration: four steps
+    t4 = (time.perf_counter() - t0) / 4
+    steps = int(max(1, min(n - 2, target_s / max(t4, 1e-6))))
+    b[...] = buf
+    t0 = time.perf_counter()
+    oracle.ltlt_colmajor(b, n, steps)
+    dt = time.perf_counter() - t0
+    flops = sum(float(n - k - 2) ** 2 for k in range(steps))
+    return steps, dt, flops
+
+
 def cpu_baseline(X, n, target_s):
-    """Time the CPU oracle (single-threaded scalar C) on the first column steps
-    of the same factorization; report nominal GFLOP/s with the same n^3/3
-    convention: step k counts (n-k-2)^2 flops."""
+    """The CPU oracle (plain scalar C, its rank-2 update split over OpenMP
+    threads) on the first column steps of the same factorization, on every
+    core this process is given, with a single-thread run beside it; nominal
+    GFLOP/s with the n^3/3 convention (step k counts (n-k-2)^2 flops).  The
+    first steps are the heaviest, so the rates are those of the large
+    trailing sizes."""
     import numpy as np
 
     import oracle
     oracle.build()
     buf = np.ascontiguousarray(X.T)            # column-major image
-    # calibrate: one step, then pick a step count near target_s
-    b1 = buf.copy()
-    t0 = time.perf_counter()
-    oracle.ltlt_colmajor(b1, n, 1)
-    t1 = time.perf_counter() - t0
-    del b1
-    steps = int(max(1, min(n - 2, target_s / max(t1, 1e-6))))
-    t0 = time.perf_counter()
-    oracle.ltlt_colmajor(buf, n, steps)
-    dt = time.perf_counter() - t0
-    flops = sum(float(n - k - 2) ** 2 for k in range(steps))
+    threads = oracle_threads()
+    steps, dt, flops = _oracle_prefix_rate(buf, n, target_s, threads)
+    s1, d1, f1 = _oracle_prefix_rate(buf, n, target_s / 2, 1)
     return {
         "value": flops / dt / 1e9,
         "unit": "GFLOP/s",
-        "cores": 1,
+        "cores": threads,
         "kind": "oracle",
-        "sample": f"first {steps} of {n - 2} column steps of the same n={n} input "
+        "sample": f"first {steps} of {n - 2} column steps of the same n={n} input on {threads} threads "
                   f"({dt:.1f} s; nominal flops sum_k (n-k-2)^2 = {flops:.3e})",
+        "single_thread": {"value": f1 / d1 / 1e9, "cores": 1,
+                          "sample": f"first {s1} column steps, one thread ({d1:.1f} s)"},
+        **host_info(),
     }
+
+
+def run_cpu_oracle(args):
+    """The whole oracle factorization + Pfaffian at --n on every core this
+    process is given (no GPU involved): the full-size CPU baseline."""
+    import numpy as np
+
+    import oracle
+    import synth
+    oracle.build()
+    gen = {"gauss": synth.skew_gauss, "graded": synth.skew_graded, "blockdiag4": synth.skew_blockdiag4}[args.input]
+    np_dt = np.float64 if args.dtype == "f64" else np.float32
+    n = args.n
+    X = gen(n, args.seed).astype(np_dt)
+    buf = np.ascontiguousarray(X.T)
+    del X
+    threads = oracle_threads()
+    oracle.set_threads(threads)
+    print(f"[cpu] oracle n={n} {args.dtype} on {threads} threads", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    ipiv = oracle.ltlt_colmajor(buf, n)
+    packed = np.tril(buf.T, -1)
+    logabs, sign = oracle.pfaffian_packed(packed, ipiv)
+    dt = time.perf_counter() - t0
+    out = {
+        "metric": "CPU oracle LTL^T factorization + Pfaffian GFLOP/s (n^3/3)",
+        "value": round(float(n) ** 3 / 3 / dt / 1e9, 3),
+        "unit": "GFLOP/s",
+        "seconds": round(dt, 2),
+        "cores": threads,
+        "dtype": args.dtype,
+        "config": {"workload": f"whole oracle factorization of one n={n} {INPUT_TEXT[args.input]} matrix "
+                               f"(seed {args.seed})", "n": n},
+        "pfaffian": {"logabs": logabs, "sign": sign},
+        **host_info(),
+    }
+    print(json.dumps(out), flush=True)
 
 
 def launch_breakdown(lt, torch, step):
@@ -213,14 +293,17 @@ def run_batched(args):
 
 
 def cpu_baseline_direct(X, n, target_s):
-    """Time the CPU oracle's Pfaffian by the even column steps (single-threaded
-    scalar C) on its first steps; extrapolate by work (step k updates
-    (n-k-2)^2 / 2 entries) to the whole Pfaffian and report the same
-    effective n^3/3 GFLOP/s as the GPU line."""
+    """Time the CPU oracle's Pfaffian by the even column steps (scalar C, its
+    rank-2 update split over the OpenMP threads this process is given) on its
+    first steps; extrapolate by work (step k updates (n-k-2)^2 / 2 entries) to
+    the whole Pfaffian and report the same effective n^3/3 GFLOP/s as the GPU
+    line."""
     import numpy as np
 
     import oracle
     oracle.build()
+    threads = oracle_threads()
+    oracle.set_threads(threads)
     buf = np.ascontiguousarray(X.T)
     b1 = buf.copy()
     t0 = time.perf_counter()
@@ -239,10 +322,11 @@ def cpu_baseline_direct(X, n, target_s):
     return {
         "value": float(n) ** 3 / 3.0 / t_total / 1e9,
         "unit": "GFLOP/s",
-        "cores": 1,
+        "cores": threads,
         "kind": "oracle",
-        "sample": f"first {steps} of {half} even column steps of the same n={n} input ({dt:.1f} s), "
-                  f"extrapolated by work sum_k (n-k-2)^2 to {t_total:.0f} s per Pfaffian",
+        "sample": f"first {steps} of {half} even column steps of the same n={n} input on {threads} threads "
+                  f"({dt:.1f} s), extrapolated by work sum_k (n-k-2)^2 to {t_total:.0f} s per Pfaffian",
+        **host_info(),
     }
 
 
@@ -454,8 +538,10 @@ def cpu_baseline_complex(X, n, target_s):
         "unit": "GFLOP/s",
         "cores": 1,
         "kind": "oracle",
-        "sample": f"first {steps} of {n - 2} column steps of the same complex n={n} input "
-                  f"({dt:.1f} s; nominal flops sum_k 4 (n-k-2)^2 = {flops:.3e})",
+        "sample": f"first {steps} of {n - 2} column steps of the same complex n={n} input, one thread "
+                  f"(the complex oracle is not threaded) ({dt:.1f} s; nominal flops sum_k 4 (n-k-2)^2 = "
+                  f"{flops:.3e})",
+        **host_info(),
     }
 
 
@@ -558,6 +644,9 @@ def main():
         print(f"bench.py: runs on one GPU only (asked for --gpus {args.gpus}); "
               "the single-matrix factorization is not sharded across GPUs", file=sys.stderr)
         sys.exit(2)
+    if args.workload == "cpu-oracle":
+        run_cpu_oracle(args)
+        return
 
     import numpy as np
     import torch
@@ -620,7 +709,7 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     lt.profile_enable(False)
-    lt.device_status()
+    lt.device_status()            # sticky: raises if a wait of any timed step gave up
     prof = lt.profile_read()
     breakdown = launch_breakdown(lt, torch, step_events)
     ms = [a.elapsed_time(b) for a, b, _, _ in evs]

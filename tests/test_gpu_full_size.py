@@ -54,7 +54,8 @@ def golden(name):
 def regenerate(name, g):
     X = make_input(WORKLOADS[name])
     stride = int(g["sample_stride"])
-    assert np.array_equal(X.ravel()[::stride].view(np.uint8), g["input_sample"].view(np.uint8)), \
+    sample = np.ascontiguousarray(X.ravel()[::stride])
+    assert np.array_equal(sample.view(np.uint8), np.ascontiguousarray(g["input_sample"]).view(np.uint8)), \
         "regenerated input differs from the one the oracle factored"
     return X
 
