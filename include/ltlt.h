@@ -69,6 +69,7 @@ extern "C" {
 #define LTLT_ERR_UNSUPPORTED (-2000)
 #define LTLT_ERR_DEVICE_TIMEOUT (-3000) /* a device-side wait exceeded its bound (see ltlt_device_status) */
 #define LTLT_ERR_SINGULAR (-4000)       /* ltlt_solve: odd order, X is singular */
+#define LTLT_ERR_SCRATCH (-5000)        /* ltlt_factor_noalloc: the order needs more than its fixed array */
 
 /* Largest n accepted by ltlt_factor_batched. */
 #define LTLT_BATCHED_MAX_N 64
@@ -124,6 +125,25 @@ int ltlt_factor(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, hipSt
  */
 int ltlt_factor_nb(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, int nb,
                    hipStream_t stream);
+
+/*
+ * ltlt_factor_noalloc -- ltlt_factor for callers that cannot allocate device
+ * memory: code being captured into a HIP graph, tight serving loops, harnesses
+ * that forbid hipMalloc.  Same operation, arguments, outputs and kernels as
+ * ltlt_factor with the default panel width (128), real types only (dtype
+ * LTLT_F64 or LTLT_F32; others return -4).  Its whole workspace is a fixed
+ * 16 MiB device array inside the library (one per GPU, held until the process
+ * ends), so it serves n <= 4928 in fp64 and n <= 8128 in fp32; a larger order
+ * returns LTLT_ERR_SCRATCH with nothing enqueued.  It calls no hipMalloc /
+ * hipFree and allocates no host memory; its first call on a device looks up
+ * the array's address and enqueues one small kernel that clears the status
+ * words kept there.  Every call on one GPU shares that array (and every call
+ * of this library shares its status words): calls that overlap in time on one
+ * GPU -- on two streams, or with another call of this library -- race.  The
+ * array keeps the last call's contents; each call initializes what it reads.
+ * No per-kernel profiling events are recorded for it.
+ */
+int ltlt_factor_noalloc(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, hipStream_t stream);
 
 /*
  * ltlt_pfaffian -- sign and log|Pf(X)| from the output of ltlt_factor.

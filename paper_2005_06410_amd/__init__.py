@@ -75,6 +75,8 @@ _SYMBOLS = {
     "ltlt_pfaffian_direct": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
                               ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "ltlt_test_force_timeout": ([ctypes.c_int], ctypes.c_int),
+    "ltlt_factor_noalloc": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
+                             ctypes.c_void_p], ctypes.c_int),
     "ltlt_solve": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_int64,
                     ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p], ctypes.c_int),
 }
@@ -91,6 +93,8 @@ class LtltError(RuntimeError):
             what = "size not supported on this device"
         elif code == -4000:
             what = "X is singular (odd order)"
+        elif code == -5000:
+            what = "the order needs more than the fixed allocation-free workspace"
         elif code <= -1000:
             what = f"HIP runtime error {-1000 - code}"
         else:

@@ -26,44 +26,82 @@ constexpr size_t kLdsBudget = 160 * 1024 - 2048;   // dynamic LDS a panel workgr
 
 int hip_err(hipError_t e) { return LTLT_ERR_HIP_BASE - (int)e; }
 
-// ---- per-device workspace -------------------------------------------------
+// ---- fixed per-device array: status words and the allocation-free workspace --
+// `scratch` is a file-scope device array: every GPU the library runs on holds
+// its own copy, at its own address, until the process ends.  Its first 256
+// bytes are the two bounded-wait status words of every call on that device
+// (see raise_wait_status); the rest is the whole workspace of
+// ltlt_factor_noalloc, which therefore needs no allocation.  In host code the
+// name `scratch` is only a stand-in for the symbol: its device address on the
+// current device comes from hipGetSymbolAddress, looked up once per device and
+// kept in g_scratch_ptr, and only that address is ever handed to kernels.
+constexpr size_t kScratchBytes = (size_t)16 << 20;
+constexpr size_t kScratchStatusBytes = 256;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[kMaxScratchDevices] = {};   // fixed table: no host allocation either
+
+__global__ void zero_words_kernel(int* p, int count) {
+  const int i = threadIdx.x;
+  if (i < count) p[i] = 0;
+}
+
+// Device address of `scratch` on the current device.  The first call on a
+// device looks it up and clears the status words with a kernel on `s`
+// (stream-ordered before the caller's kernels).
+hipError_t device_scratch(hipStream_t s, char** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(zero_words_kernel, dim3(1), dim3(64), 0, s, static_cast<int*>(p),
+                       (int)(kScratchStatusBytes / sizeof(int)));
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = static_cast<char*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+// The status words of the current device (set up on first use).
+hipError_t status_words(hipStream_t s, int** status) {
+  char* base = nullptr;
+  const hipError_t e = device_scratch(s, &base);
+  if (e == hipSuccess) *status = reinterpret_cast<int*>(base);
+  return e;
+}
+
+// ---- per-device workspace (grown on demand) ---------------------------------
 struct Workspace {
   void* ptr = nullptr;
   size_t bytes = 0;
-  int* status = nullptr;     // device flag for bounded waits (kept separately)
 };
 std::mutex g_ws_mu;
 std::map<int, Workspace> g_ws;
 
-// The two bounded-wait status words (see raise_wait_status) of the current
-// device; caller holds g_ws_mu.
-hipError_t status_locked(Workspace& w) {
-  if (w.status) return hipSuccess;
-  hipError_t e = hipMalloc(&w.status, 256);
-  if (e != hipSuccess) { w.status = nullptr; return e; }
-  e = hipMemset(w.status, 0, 256);
-  if (e != hipSuccess) { (void)hipFree(w.status); w.status = nullptr; }
-  return e;
-}
+// A caller-provided workspace (the allocation-free entry point).
+struct FixedWs {
+  char* ptr;
+  size_t bytes;
+  int* status;
+};
 
-hipError_t status_words(int** status) {
+hipError_t workspace(size_t bytes, hipStream_t s, void** out, int** status) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  std::lock_guard<std::mutex> lk(g_ws_mu);
-  e = status_locked(g_ws[dev]);
-  if (e == hipSuccess) *status = g_ws[dev].status;
-  return e;
-}
-
-hipError_t workspace(size_t bytes, void** out, int** status) {
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
+  e = status_words(s, status);
   if (e != hipSuccess) return e;
   std::lock_guard<std::mutex> lk(g_ws_mu);
   Workspace& w = g_ws[dev];
-  e = status_locked(w);
-  if (e != hipSuccess) return e;
   if (w.bytes < bytes) {
     if (w.ptr) {
       e = hipDeviceSynchronize();       // earlier work may still use it
@@ -79,7 +117,6 @@ hipError_t workspace(size_t bytes, void** out, int** status) {
     w.bytes = want;
   }
   *out = w.ptr;
-  *status = w.status;
   return hipSuccess;
 }
 
@@ -104,17 +141,26 @@ bool cooperative_panels() { return g_cooperative_panels.load(std::memory_order_r
 bool forced_timeout() { return g_forced_timeout.load(std::memory_order_relaxed); }
 
 hipError_t ensure_dynamic_lds(const void* kernel, int bytes) {
+  // a fixed table of (kernel, device) -> bytes allowed: no host allocation, so
+  // the allocation-free entry point may pass through here
+  struct Entry { const void* kernel; int dev; int bytes; };
+  constexpr int kEntries = 256;
+  static Entry table[kEntries];
+  static int used = 0;
   static std::mutex mu;
-  static std::map<std::pair<const void*, int>, int> set_to;   // (kernel, device) -> bytes allowed
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   std::lock_guard<std::mutex> lk(mu);
-  const auto it = set_to.find({kernel, dev});
-  if (it != set_to.end() && it->second >= bytes) return hipSuccess;
+  int at = -1;
+  for (int i = 0; i < used; ++i)
+    if (table[i].kernel == kernel && table[i].dev == dev) { at = i; break; }
+  if (at >= 0 && table[at].bytes >= bytes) return hipSuccess;
   e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-  if (e == hipSuccess) set_to[{kernel, dev}] = bytes;
-  return e;
+  if (e != hipSuccess) return e;
+  if (at < 0 && used < kEntries) at = used++;
+  if (at >= 0) table[at] = Entry{kernel, dev, bytes};   // a full table only means setting it again
+  return hipSuccess;
 }
 }  // namespace ltlt
 
@@ -148,7 +194,9 @@ struct ProfScope {
   ProfRec rec{};
   bool on = false;
   hipStream_t s;
+  // kind < 0: never recorded (the allocation-free path creates no events)
   ProfScope(int kind, double flops, hipStream_t st) : s(st) {
+    if (kind < 0) return;
     std::lock_guard<std::mutex> lk(g_prof_mu);
     if (!g_prof_on || (g_prof_update_only && kind != 1)) return;
     rec.kind = kind;
@@ -185,8 +233,12 @@ int choose_rows(int bw) {
   return panel_lds_bytes<T>(bw, R) <= kLdsBudget ? R : 0;
 }
 
+// fixed == nullptr: the cached, grown-on-demand workspace; otherwise the
+// caller's fixed one (LTLT_ERR_SCRATCH when the order needs more), with no
+// allocation and no profiling events.
 template <typename T>
-int factor_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, hipStream_t s) {
+int factor_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, hipStream_t s,
+                const FixedWs* fixed = nullptr) {
   if (n64 == 0) return 0;
   if (n64 >= kMaxOrder) return LTLT_ERR_UNSUPPORTED;
   const int n = (int)n64;
@@ -220,8 +272,16 @@ int factor_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, hipStream
 
   void* ws = nullptr;
   int* status = nullptr;
-  hipError_t e = workspace(cv.off, &ws, &status);
-  if (e != hipSuccess) return hip_err(e);
+  hipError_t e = hipSuccess;
+  if (fixed) {
+    if (cv.off > fixed->bytes) return LTLT_ERR_SCRATCH;
+    ws = fixed->ptr;
+    status = fixed->status;
+  } else {
+    e = workspace(cv.off, s, &ws, &status);
+    if (e != hipSuccess) return hip_err(e);
+  }
+  const int pk = fixed ? -1 : 0;                 // profiling kinds are offset by this (-1: off)
   char* base = static_cast<char*>(ws);
   T* PO = reinterpret_cast<T*>(base + o_PO);
   T* Bm = reinterpret_cast<T*>(base + o_Bm);
@@ -233,7 +293,7 @@ int factor_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, hipStream
   T* stage = reinterpret_cast<T*>(base + o_st);
 
   {
-    ProfScope ps(3, 0.0, s);
+    ProfScope ps(pk < 0 ? -1 : 3, 0.0, s);
     e = launch_init(ipiv, n, status, s);
     if (e == hipSuccess && nblk > 0) e = launch_rec_init(rec, nrec, s);
   }
@@ -254,7 +314,7 @@ int factor_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, hipStream
     pa.rec = rec;
     pa.status = status;
     {
-      ProfScope ps(0, 0.0, s);
+      ProfScope ps(pk < 0 ? -1 : 0, 0.0, s);
       e = launch_panel<T>(pa, panel_lds_bytes<T>(bw, pa.R), s);
     }
     if (e != hipSuccess) return hip_err(e);
@@ -276,19 +336,19 @@ int factor_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, hipStream
       ua.Bt = Bm;
       ua.ldb = ldw;
       ua.pad_row = 1;      // bw + m2 + 1 <= n <= ldw: row m2 of each column lies inside the workspace
-      ProfScope ps(1, (double)m2 * (double)m2 * (double)bw, s);
+      ProfScope ps(pk < 0 ? -1 : 1, (double)m2 * (double)m2 * (double)bw, s);
       e = launch_update<T>(ua, s);
       if (e != hipSuccess) return hip_err(e);
     }
     {
-      ProfScope ps(2, 0.0, s);
+      ProfScope ps(pk < 0 ? -1 : 2, 0.0, s);
       e = launch_commit<T>(A, lda, n, j, bw, PO, ldw, al, status, s);
     }
     if (e != hipSuccess) return hip_err(e);
   }
 
   if (nblk >= 2) {
-    ProfScope ps(3, 0.0, s);
+    ProfScope ps(pk < 0 ? -1 : 3, 0.0, s);
     e = launch_perm_chain(Tblk, nb, nblk, n, Gc, s);
     if (e == hipSuccess) e = launch_perm_apply<T>(A, lda, n, Gc, nb, c_end, stage, s);
     if (e != hipSuccess) return hip_err(e);
@@ -310,7 +370,7 @@ int pfaffian_direct_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, 
   if (n == 0 || (n & 1)) {                       // Pf = 1 (n = 0) or 0 (odd n): no steps
     void* ws = nullptr;
     int* status = nullptr;
-    e = workspace(256, &ws, &status);
+    e = workspace(256, s, &ws, &status);
     if (e == hipSuccess && n > 0) e = launch_init(ipiv, n, status, s);
     if (e == hipSuccess) e = launch_pfaffian<T>(n, A, lda, ipiv, logabs, sign, status, s);
     return e == hipSuccess ? 0 : hip_err(e);
@@ -333,7 +393,7 @@ int pfaffian_direct_impl(int64_t n64, T* A, int64_t lda, int32_t* ipiv, int nb, 
   const size_t o_rec = cv.take<uint64_t>((size_t)2 * kRecStride * nrec);
   void* ws = nullptr;
   int* status = nullptr;
-  e = workspace(cv.off, &ws, &status);
+  e = workspace(cv.off, s, &ws, &status);
   if (e != hipSuccess) return hip_err(e);
   char* base = static_cast<char*>(ws);
   T* PO = reinterpret_cast<T*>(base + o_PO);
@@ -451,7 +511,7 @@ int factor_complex_impl(int64_t n64, void* A, int64_t lda, int32_t* ipiv, int nb
 
   void* ws = nullptr;
   int* status = nullptr;
-  hipError_t e = workspace(cv.off, &ws, &status);
+  hipError_t e = workspace(cv.off, s, &ws, &status);
   if (e != hipSuccess) return hip_err(e);
   char* base = static_cast<char*>(ws);
   T* Pr = reinterpret_cast<T*>(base + o_Pr);
@@ -578,6 +638,22 @@ int ltlt_factor(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, hipSt
   return r;
 }
 
+int ltlt_factor_noalloc(int64_t n, void* A, int64_t lda, int dtype, int32_t* ipiv, hipStream_t stream) {
+  if (n < 0 || n > (int64_t)INT32_MAX / 2) return -1;
+  if (A == nullptr && n > 0) return -2;
+  if (lda < std::max<int64_t>(1, n)) return -3;
+  if (bad_dtype(dtype)) return -4;              // real types only (complex needs 2 n^2 of planes)
+  if (ipiv == nullptr && n > 0) return -5;
+  if (n == 0) return 0;
+  char* base = nullptr;
+  const hipError_t e = device_scratch(stream, &base);
+  if (e != hipSuccess) return hip_err(e);
+  const FixedWs fw{base + kScratchStatusBytes, kScratchBytes - kScratchStatusBytes, reinterpret_cast<int*>(base)};
+  if (dtype == LTLT_F64)
+    return factor_impl<double>(n, static_cast<double*>(A), lda, ipiv, kDefaultNb, stream, &fw);
+  return factor_impl<float>(n, static_cast<float*>(A), lda, ipiv, kDefaultNb, stream, &fw);
+}
+
 int ltlt_pfaffian_complex(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* ipiv, double* logabs,
                           double* phase, hipStream_t stream) {
   if (n < 0 || n > (int64_t)INT32_MAX / 2) return -1;
@@ -588,7 +664,7 @@ int ltlt_pfaffian_complex(int64_t n, const void* A, int64_t lda, int dtype, cons
   if (logabs == nullptr) return -6;
   if (phase == nullptr) return -7;
   int* status = nullptr;
-  hipError_t e = status_words(&status);
+  hipError_t e = status_words(stream, &status);
   if (e != hipSuccess) return hip_err(e);
   e = dtype == LTLT_C128 ? launch_cpfaffian<double>((int)n, A, lda, ipiv, logabs, phase, status, stream)
                          : launch_cpfaffian<float>((int)n, A, lda, ipiv, logabs, phase, status, stream);
@@ -605,7 +681,7 @@ int ltlt_pfaffian(int64_t n, const void* A, int64_t lda, int dtype, const int32_
   if (logabs == nullptr) return -6;
   if (sign == nullptr) return -7;
   int* status = nullptr;
-  hipError_t e = status_words(&status);
+  hipError_t e = status_words(stream, &status);
   if (e != hipSuccess) return hip_err(e);
   if (dtype == LTLT_F64)
     e = launch_pfaffian<double>((int)n, static_cast<const double*>(A), lda, ipiv, logabs, sign, status, stream);
@@ -669,7 +745,7 @@ int ltlt_solve(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* 
   const size_t o_dinv = cv.take<char>((size_t)(1 + 2 * 2) * nblk * 64 * 64 * esz);
   void* ws = nullptr;
   int* status = nullptr;
-  hipError_t e = workspace(cv.off, &ws, &status);
+  hipError_t e = workspace(cv.off, stream, &ws, &status);
   if (e != hipSuccess) return hip_err(e);
   char* base = static_cast<char*>(ws);
   SolveWork w{};
@@ -748,10 +824,9 @@ int ltlt_device_status(hipStream_t stream) {
   if (e != hipSuccess) return hip_err(e);
   int* st = nullptr;
   {
-    std::lock_guard<std::mutex> lk(g_ws_mu);
-    auto it = g_ws.find(dev);
-    if (it == g_ws.end() || !it->second.status) return 0;
-    st = it->second.status;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (dev < 0 || dev >= kMaxScratchDevices || !g_scratch_ptr[dev]) return 0;   // no call on this device yet
+    st = reinterpret_cast<int*>(g_scratch_ptr[dev]);
   }
   // the sticky word: raised by any wait that gave up since the last read
   int h = 0;
@@ -813,7 +888,6 @@ int ltlt_release_workspace(void) {
     if (hipSetDevice(kv.first) != hipSuccess) continue;
     (void)hipDeviceSynchronize();
     if (kv.second.ptr) (void)hipFree(kv.second.ptr);
-    if (kv.second.status) (void)hipFree(kv.second.status);
   }
   g_ws.clear();
   (void)hipSetDevice(dev0);
