@@ -317,11 +317,13 @@ int ltlt_profile_read(int nkinds, int64_t* launches, double* ms, double* flops);
 int ltlt_release_workspace(void);
 
 /*
- * ltlt_set_cooperative_panels -- how the panel kernels are launched (host
- * call, process-wide; returns 0, or -1 for a value other than 0 or 1).
- * A panel's workgroups (at most one per CU, never more than the device's
- * CUs) wait on each other at every column step, so they must all be
- * resident at once.  on = 0 (the default): ordinary launches.  Issued in
+ * ltlt_set_cooperative_panels -- how the grids whose workgroups wait on
+ * each other are launched: the panels of ltlt_factor and
+ * ltlt_pfaffian_direct and the substitutions of ltlt_solve (host call,
+ * process-wide; returns 0, or -1 for a value other than 0 or 1).  Such a
+ * grid (a panel: at most one workgroup per CU; a substitution: at most what
+ * the device holds at once) must be resident all at once.  on = 0 (the
+ * default): ordinary launches.  Issued in
  * stream order onto a device that runs nothing else, every workgroup is
  * dispatched at once; when other streams or processes hold CUs during a
  * call, the panel waits for them, and if it cannot become resident within

@@ -633,15 +633,16 @@ int solve_tri_max_blocks() {
   return per_cu * cus;
 }
 
+// The substitution's workgroups wait on each other's blocks (bounded waits),
+// so the grid never exceeds what the device holds at once; like the panels it
+// is an ordinary launch unless ltlt_set_cooperative_panels(1) asks for the
+// runtime's cooperative one.
 template <typename T, bool UPPER>
 hipError_t launch_solve_tri(const SolveTriArgs& a, hipStream_t s) {
   const int cap = solve_tri_max_blocks<T, UPPER>();
   if (cap <= 0) return hipErrorInvalidValue;
   const int grid = a.nblk < cap ? a.nblk : cap;
-  SolveTriArgs copy = a;
-  void* args[] = {&copy};
-  const void* k = (const void*)solve_tri_kernel<T, UPPER>;
-  return hipLaunchCooperativeKernel(k, dim3(grid), dim3(kSThreads), args, 0, s);
+  return launch_resident_grid(solve_tri_kernel<T, UPPER>, (unsigned)grid, kSThreads, 0, s, a);
 }
 
 // Stamps of the mailbox words: a process-wide counter that skips 0 (zeroed
