@@ -35,6 +35,9 @@ What it computes (textbook definitions, written out plainly):
 Every floating-point routine runs in the precision of its input (fp64, or fp32
 for fp32 parity); the Pfaffian accumulates in fp64.
 
+The convolution operator of the paper's section 3 (direct loops, im2col) has
+its own module, ``oracle.conv``, with its own C source.
+
 Pins (tests that tie these functions to facts outside themselves) live in
 ``tests/test_oracle_pins*.py``; no function here is unpinned.
 """
@@ -67,6 +70,8 @@ def build(force: bool = False) -> str:
         tmp = _LIB + ".tmp%d" % os.getpid()
         subprocess.check_call(["gcc", *GCC_FLAGS, _SRC, "-o", tmp, "-lm"])
         os.replace(tmp, _LIB)
+    from . import conv
+    conv.build(force)
     return _LIB
 
 
