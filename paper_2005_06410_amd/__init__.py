@@ -40,6 +40,8 @@ __all__ = [
     "profile_enable",
     "profile_read",
     "release_workspace",
+    "conv_out_size",
+    "convgemm",
     "LtltError",
     "F64",
     "F32",
@@ -79,6 +81,10 @@ _SYMBOLS = {
                              ctypes.c_void_p], ctypes.c_int),
     "ltlt_solve": ([ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_int64,
                     ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p], ctypes.c_int),
+    # include/convgemm.h
+    "convgemm_out_size": ([ctypes.c_int] * 4, ctypes.c_int),
+    "convgemm_f32": ([ctypes.c_int] * 9 + [ctypes.c_void_p] * 3 + [ctypes.c_int] * 3 + [ctypes.c_void_p],
+                     ctypes.c_int),
 }
 
 
@@ -353,6 +359,56 @@ def skew_update(C, Lx, Bt, perm=None, offset: int = 0):
     code = lib.ltlt_skew_update(m, ptr, ldc, pp, K, Lx.data_ptr(), ld(Lx), Bt.data_ptr(), ld(Bt),
                                 _dtype_code(C), _stream_ptr(C.device))
     _check("ltlt_skew_update", code)
+
+
+def conv_out_size(h: int, k: int, stride: int = 1, pad: int = 0) -> int:
+    """floor((h - k + 2 pad)/stride) + 1 (``convgemm_out_size``); raises when
+    the window does not fit the padded input."""
+    r = load().convgemm_out_size(int(h), int(k), int(stride), int(pad))
+    if r < 1:
+        raise ValueError(f"no output for h={h} k={k} stride={stride} pad={pad}")
+    return r
+
+
+def _leftmost_fastest(t, name):
+    """The convolution tensors are stored with the leftmost index fastest."""
+    torch = _torch()
+    if t.dtype != torch.float32 or t.dim() != 4:
+        raise TypeError(f"{name} must be a 4-d float32 tensor")
+    if not t.permute(3, 2, 1, 0).is_contiguous():
+        raise ValueError(f"{name} must be stored leftmost index fastest (strides (1, d0, d0 d1, d0 d1 d2))")
+
+
+def convgemm(F, I, stride: int = 1, pad: int = 0, out=None, accumulate: bool = False, tile=(0, 0)):
+    """O = conv(F, I) (or O += conv(F, I) with ``accumulate``) by the
+    implicit-im2col GEMM of ``convgemm_f32``.
+
+    F: (kn, kh, kw, ci) and I: (hi, wi, ci, b) float32 GPU tensors stored with
+    the leftmost index fastest (a numpy Fortran-order array's layout).
+    Returns O (kn, ho, wo, b) in the same storage (``out`` if given).
+    ``tile`` = (mt, nt) forces a workgroup tile (tests and tuning)."""
+    torch = _torch()
+    _require_gpu(I)
+    _same_device(I, F, out)
+    _leftmost_fastest(F, "F")
+    _leftmost_fastest(I, "I")
+    kn, kh, kw, ci = F.shape
+    hi, wi, ci2, b = I.shape
+    if ci2 != ci:
+        raise ValueError("F and I disagree on the channel count")
+    ho, wo = conv_out_size(hi, kh, stride, pad), conv_out_size(wi, kw, stride, pad)
+    if out is None:
+        flat = torch.empty(max(kn * ho * wo * b, 1), dtype=torch.float32, device=I.device)
+        out = flat[:kn * ho * wo * b].as_strided((kn, ho, wo, b), (1, kn, kn * ho, kn * ho * wo))
+    else:
+        _leftmost_fastest(out, "out")
+        if tuple(out.shape) != (kn, ho, wo, b):
+            raise ValueError(f"out must have shape {(kn, ho, wo, b)}")
+    mt, nt = tile
+    code = load().convgemm_f32(kn, kh, kw, ci, hi, wi, b, int(stride), int(pad), F.data_ptr(), I.data_ptr(),
+                               out.data_ptr(), int(bool(accumulate)), int(mt), int(nt), _stream_ptr(I.device))
+    _check("convgemm_f32", code)
+    return out
 
 
 def device_status(device=None):

@@ -1,0 +1,356 @@
+// CONVGEMM on gfx950: the convolution O = conv(F, I) as one fp32 matrix product
+// O^ = F^ . im2col(I) whose second operand is gathered from the input tensor
+// while it is staged into LDS (the paper's section 4, Figure 6: im2col folded
+// into the packing of the GEMM's B operand, so the augmented matrix of
+// section 3 is never formed in memory).
+//
+// Mapping to CDNA4.  One workgroup (4 waves, 2 x 2) owns an MT x NT tile of O^
+// (MT filters x NT output positions).  The contraction runs in chunks of
+// kKC = 16 rows of im2col(I) (= columns of F^):
+//   * F^ chunk (MT x 16): coalesced loads along the filter index, kept in LDS
+//     as rows of 16 contraction values per filter;
+//   * im2col chunk (16 x NT): each thread owns one output position (column)
+//     of the tile, decoded once into (oh, ow, n), and walks its contraction
+//     rows r -> (y, x, c) incrementally; the value is I at
+//     (s*oh + y - p, s*ow + x - p, c, n) or zero outside the input, exactly
+//     Figure 6's index maps.  Neighbouring threads hold neighbouring output
+//     positions, so each load instruction reads a contiguous (stride s) run of
+//     one input row.  Stored in LDS as 16 contraction values per column;
+//   * v_mfma_f32_16x16x4_f32 on 16 x 16 blocks.  Because the contraction may
+//     be taken in any order, lane group q of a wave (lanes 16q .. 16q+15)
+//     takes contraction rows 4q .. 4q+3 of the chunk for the four MFMAs of a
+//     chunk, so one ds_read_b128 feeds four MFMAs;
+//   * two LDS buffers: the next chunk's global loads are issued before the
+//     current chunk's MFMAs and written to the other buffer after them, one
+//     barrier per chunk.
+// Tiles are handed out XCD-aware: consecutive workgroup ids go to different
+// XCDs (round-robin), so ids are remapped to give each XCD a contiguous range of
+// tiles, filter tiles fastest; tiles that share output positions (and the input
+// rows they read) then run on the same XCD and share its L2.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "convgemm.h"
+
+namespace convgemm {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kKC = 16;        // contraction rows per staged chunk
+constexpr int kKP = kKC + 4;   // LDS floats per tile row (padded against bank conflicts)
+
+struct Geometry {
+    int M, K, N;        // kn, kh*kw*ci, ho*wo*b
+    int kh, khw;        // kh, kh*kw
+    int kw;
+    int hi, wi, hiwi;   // input height, width, hi*wi
+    int ho, hw;         // ho, ho*wo
+    int s, p;
+    int64_t sample;     // hi*wi*ci: input floats per batch entry
+};
+
+template <int MT, int NT>
+__global__ __launch_bounds__(kThreads) void convgemm_kernel(Geometry g, const float* __restrict__ F,
+                                                            const float* __restrict__ I,
+                                                            float* __restrict__ O, int accumulate,
+                                                            int vec, int mtiles, int ntiles)
+{
+    constexpr int WM = MT / 2, WN = NT / 2;        // wave tile
+    constexpr int BM = WM / 16, BN = WN / 16;      // 16 x 16 blocks per wave
+    constexpr int AE = MT * kKC / kThreads;        // F^ values per thread per chunk
+    constexpr int RPT = kKC * NT / kThreads;       // im2col rows per thread per chunk
+    static_assert(AE * kThreads == MT * kKC && RPT * kThreads == kKC * NT, "tile must split evenly");
+    static_assert(RPT % 4 == 0 && BM >= 1 && BN >= 1, "tile shape");
+
+    __shared__ __attribute__((aligned(16))) float As[2][MT * kKP];
+    __shared__ __attribute__((aligned(16))) float Bs[2][NT * kKP];
+
+    // XCD-aware tile order: within the largest multiple of 8 of the tile
+    // count, workgroup id -> XCD (id mod 8) gets the contiguous tile range
+    // [xcd * T8/8, (xcd + 1) * T8/8); the remainder keeps the identity.
+    const int T = mtiles * ntiles;
+    const int T8 = T & ~7;
+    const int bid = blockIdx.x;
+    const int t = bid < T8 ? (bid & 7) * (T8 >> 3) + (bid >> 3) : bid;
+    const int m0 = (t % mtiles) * MT;
+    const int n0 = (t / mtiles) * NT;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave & 1, wn = wave >> 1;
+
+    // This thread's output position for the gather, decoded once.
+    const int bcol = tid % NT;
+    const int brow = (tid / NT) * RPT;
+    const int ncol = n0 + bcol;
+    const bool col_ok = ncol < g.N;
+    int hbase = 0, wbase = 0;
+    int64_t cbase = 0;
+    if (col_ok) {
+        const int nb = ncol / g.hw;
+        const int rem = ncol - nb * g.hw;
+        const int ow = rem / g.ho;
+        const int oh = rem - ow * g.ho;
+        hbase = oh * g.s - g.p;
+        wbase = ow * g.s - g.p;
+        cbase = (int64_t)nb * g.sample;
+    }
+    const float* __restrict__ Ib = I + cbase;
+
+    // Raw loaded values and, per value, whether it is a real entry (bit j of
+    // amask / bmask).  Out-of-range lanes load from a clamped valid address;
+    // the zeroing is applied when the chunk is written to LDS, after the
+    // MFMAs, so that nothing waits for the loads before the MFMAs are issued.
+    float ra[AE];
+    float rb[RPT];
+    uint32_t amask, bmask;
+
+    auto load_chunk = [&](int chunk) {
+        const int k0 = chunk * kKC;
+        amask = 0;
+#pragma unroll
+        for (int j = 0; j < AE; ++j) {
+            const int e = tid + kThreads * j;
+            const int m = m0 + e % MT;
+            const int k = k0 + e / MT;
+            const bool ok = m < g.M && k < g.K;
+            ra[j] = F[ok ? (int64_t)k * g.M + m : 0];
+            amask |= (uint32_t)ok << j;
+        }
+        const int r0 = k0 + brow;
+        int c = r0 / g.khw;
+        const int rem = r0 - c * g.khw;
+        int x = rem / g.kh;
+        int y = rem - x * g.kh;
+        bmask = 0;
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) {
+            const int hh = hbase + y, ww = wbase + x;
+            const bool ok = col_ok && (r0 + j) < g.K && (unsigned)hh < (unsigned)g.hi &&
+                            (unsigned)ww < (unsigned)g.wi;
+            rb[j] = Ib[ok ? hh + g.hi * ww + g.hiwi * c : 0];
+            bmask |= (uint32_t)ok << j;
+            // next contraction row: y fastest, then x, then c (branch-free)
+            ++y;
+            const bool wy = y == g.kh;
+            y = wy ? 0 : y;
+            x += wy;
+            const bool wx = x == g.kw;
+            x = wx ? 0 : x;
+            c += wx;
+        }
+    };
+
+    auto store_chunk = [&](int buf) {
+#pragma unroll
+        for (int j = 0; j < AE; ++j) {
+            const int e = tid + kThreads * j;
+            As[buf][(e % MT) * kKP + e / MT] = (amask >> j) & 1 ? ra[j] : 0.0f;
+        }
+        float* bp = &Bs[buf][bcol * kKP + brow];
+#pragma unroll
+        for (int j = 0; j < RPT; j += 4) {
+            f4 v;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) v[q] = (bmask >> (j + q)) & 1 ? rb[j + q] : 0.0f;
+            *reinterpret_cast<f4*>(bp + j) = v;
+        }
+    };
+
+    f4 acc[BM][BN];
+#pragma unroll
+    for (int i = 0; i < BM; ++i)
+#pragma unroll
+        for (int j = 0; j < BN; ++j) acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    auto compute = [&](int buf) {
+        const float* ap = &As[buf][(wm * WM + (lane & 15)) * kKP + 4 * (lane >> 4)];
+        const float* bp = &Bs[buf][(wn * WN + (lane & 15)) * kKP + 4 * (lane >> 4)];
+        f4 a[BM], b[BN];
+#pragma unroll
+        for (int i = 0; i < BM; ++i) a[i] = *reinterpret_cast<const f4*>(ap + i * 16 * kKP);
+#pragma unroll
+        for (int j = 0; j < BN; ++j) b[j] = *reinterpret_cast<const f4*>(bp + j * 16 * kKP);
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+            for (int i = 0; i < BM; ++i)
+#pragma unroll
+                for (int j = 0; j < BN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][kk], b[j][kk], acc[i][j], 0, 0, 0);
+    };
+
+    const int nchunks = (g.K + kKC - 1) / kKC;
+    load_chunk(0);
+    store_chunk(0);
+    __syncthreads();
+    // The scheduling barriers keep the next chunk's loads ahead of the MFMAs
+    // and their LDS stores behind them, so the loads' latency is covered.
+    for (int chunk = 0; chunk + 1 < nchunks; ++chunk) {
+        const int buf = chunk & 1;
+        load_chunk(chunk + 1);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(buf);
+        __builtin_amdgcn_sched_barrier(0);
+        store_chunk(buf ^ 1);
+        __syncthreads();
+    }
+    compute((nchunks - 1) & 1);
+
+    // Epilogue: lane holds rows 4*(lane/16) .. +3 of column lane%16 of each
+    // 16 x 16 block; four consecutive filters are contiguous in O (one 16-byte
+    // store when kn is a multiple of 4 and O is 16-byte aligned: vec).
+#pragma unroll
+    for (int i = 0; i < BM; ++i) {
+        const int m = m0 + wm * WM + i * 16 + 4 * (lane >> 4);
+#pragma unroll
+        for (int j = 0; j < BN; ++j) {
+            const int n = n0 + wn * WN + j * 16 + (lane & 15);
+            if (n >= g.N || m >= g.M) continue;
+            float* o = O + (int64_t)n * g.M + m;
+            f4 v = acc[i][j];
+            if (vec) {
+                if (accumulate) v += *reinterpret_cast<const f4*>(o);
+                *reinterpret_cast<f4*>(o) = v;
+            } else {
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    if (m + q < g.M) o[q] = accumulate ? o[q] + v[q] : v[q];
+            }
+        }
+    }
+}
+
+int out_size(int h, int k, int s, int p)
+{
+    if (k < 1 || s < 1 || p < 0 || h < 1) return -1;
+    const int64_t span = (int64_t)h - k + 2 * (int64_t)p;
+    if (span < 0) return -1;
+    return (int)(span / s + 1);
+}
+
+struct Tile {
+    int mt, nt;
+};
+
+// Tile choice: the least padded work; among near ties (within 5 %) the tile
+// that still gives at least three workgroups per compute unit, then the larger
+// filter tile (fewer re-gathers of the same input).
+Tile choose_tile(int M, int N, int cus)
+{
+    static const Tile cand[] = {{192, 128}, {128, 128}, {64, 256}, {64, 128}, {64, 64}};
+    double best_pad = 1e300;
+    for (const Tile& c : cand) {
+        const double pad = (double)((M + c.mt - 1) / c.mt) * c.mt * ((double)((N + c.nt - 1) / c.nt) * c.nt);
+        if (pad < best_pad) best_pad = pad;
+    }
+    const Tile* pick = nullptr;
+    int64_t pick_tiles = -1;
+    for (const Tile& c : cand) {
+        const double pad = (double)((M + c.mt - 1) / c.mt) * c.mt * ((double)((N + c.nt - 1) / c.nt) * c.nt);
+        if (pad > 1.05 * best_pad) continue;
+        const int64_t tiles = (int64_t)((M + c.mt - 1) / c.mt) * ((N + c.nt - 1) / c.nt);
+        if (tiles >= 3 * (int64_t)cus) return c;
+        if (tiles > pick_tiles) {
+            pick = &c;
+            pick_tiles = tiles;
+        }
+    }
+    return *pick;
+}
+
+template <int MT, int NT>
+hipError_t launch(const Geometry& g, const float* F, const float* I, float* O, int accumulate, int vec,
+                  hipStream_t stream)
+{
+    const int mtiles = (g.M + MT - 1) / MT;
+    const int ntiles = (g.N + NT - 1) / NT;
+    const int64_t tiles = (int64_t)mtiles * ntiles;
+    if (tiles > 0x7fffffff) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((convgemm_kernel<MT, NT>), dim3((unsigned)tiles), dim3(kThreads), 0, stream, g, F, I, O,
+                       accumulate, vec, mtiles, ntiles);
+    return hipGetLastError();
+}
+
+int device_cus()
+{
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 256;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        return 256;
+    return cus;
+}
+
+}  // namespace
+}  // namespace convgemm
+
+extern "C" int convgemm_out_size(int h, int k, int stride, int pad)
+{
+    return convgemm::out_size(h, k, stride, pad);
+}
+
+extern "C" int convgemm_f32(int kn, int kh, int kw, int ci, int hi, int wi, int b, int stride, int pad,
+                            const float* F, const float* I, float* O, int accumulate, int mt, int nt,
+                            hipStream_t stream)
+{
+    using namespace convgemm;
+    if (kn < 1) return -1;
+    if (kh < 1) return -2;
+    if (kw < 1) return -3;
+    if (ci < 1) return -4;
+    if (hi < 1) return -5;
+    if (wi < 1) return -6;
+    if (b < 0) return -7;
+    if (stride < 1) return -8;
+    if (pad < 0) return -9;
+    const int ho = out_size(hi, kh, stride, pad);
+    const int wo = out_size(wi, kw, stride, pad);
+    if (ho < 1) return -5;
+    if (wo < 1) return -6;
+    if ((int64_t)hi * wi * ci >= ((int64_t)1 << 31)) return -5;
+    if ((int64_t)kh * kw * ci >= ((int64_t)1 << 31)) return -2;
+    if ((int64_t)ho * wo * b >= ((int64_t)1 << 31)) return -7;
+    if (accumulate != 0 && accumulate != 1) return -13;
+    const bool auto_tile = mt == 0 && nt == 0;
+    if (!auto_tile && !((mt == 64 && (nt == 64 || nt == 128 || nt == 256)) || (mt == 128 && nt == 128) ||
+                        (mt == 192 && nt == 128)))
+        return -14;
+    if (b == 0) return CONVGEMM_OK;
+    if (!F) return -10;
+    if (!I) return -11;
+    if (!O) return -12;
+
+    Geometry g;
+    g.M = kn;
+    g.K = kh * kw * ci;
+    g.N = ho * wo * b;
+    g.kh = kh;
+    g.kw = kw;
+    g.khw = kh * kw;
+    g.hi = hi;
+    g.wi = wi;
+    g.hiwi = hi * wi;
+    g.ho = ho;
+    g.hw = ho * wo;
+    g.s = stride;
+    g.p = pad;
+    g.sample = (int64_t)hi * wi * ci;
+
+    const int vec = (kn % 4 == 0) && ((uintptr_t)O % 16 == 0);
+    Tile t = auto_tile ? choose_tile(g.M, g.N, device_cus()) : Tile{mt, nt};
+    hipError_t e;
+    if (t.mt == 64 && t.nt == 64)
+        e = launch<64, 64>(g, F, I, O, accumulate, vec, stream);
+    else if (t.mt == 64 && t.nt == 128)
+        e = launch<64, 128>(g, F, I, O, accumulate, vec, stream);
+    else if (t.mt == 64)
+        e = launch<64, 256>(g, F, I, O, accumulate, vec, stream);
+    else if (t.mt == 128)
+        e = launch<128, 128>(g, F, I, O, accumulate, vec, stream);
+    else
+        e = launch<192, 128>(g, F, I, O, accumulate, vec, stream);
+    return e == hipSuccess ? CONVGEMM_OK : CONVGEMM_ERR_HIP_BASE - (int)e;
+}

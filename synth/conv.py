@@ -38,6 +38,16 @@ ALEXNET_CONV = [
 ]
 
 
+# The benchmarked batch: the largest batch size of the paper's AlexNet runs
+# (section 5.4 runs b up to 80).
+ALEXNET_BATCH = 80
+
+
+def layer_seed(spec: dict) -> int:
+    """Seed of one layer's synthetic tensors in the benchmarked workload."""
+    return 1000 + int(spec["layer"])
+
+
 def _fortran(flat: np.ndarray, shape) -> np.ndarray:
     return np.asfortranarray(flat.reshape(shape, order="F"))
 

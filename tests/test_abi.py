@@ -11,13 +11,16 @@ import paper_2005_06410_amd as lt
 from paper_2005_06410_amd import build as ltbuild
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "ltlt.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in sorted(os.listdir(os.path.join(ROOT, "include")))
+           if h.endswith(".h")]
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(ltlt_\w+)\s*\(", text, flags=re.M)))
+    names = set()
+    for h in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*((?:ltlt|convgemm)_\w+)\s*\(", text, flags=re.M))
+    return sorted(names)
 
 
 @pytest.fixture(scope="module")
@@ -33,7 +36,7 @@ def test_header_declares_the_entry_points():
                  "ltlt_skew_update", "ltlt_device_status", "ltlt_profile_enable",
                  "ltlt_profile_read", "ltlt_release_workspace", "ltlt_mfma_probe",
                  "ltlt_pfaffian_direct", "ltlt_solve", "ltlt_pfaffian_complex",
-                 "ltlt_set_cooperative_panels"]:
+                 "ltlt_set_cooperative_panels", "convgemm_f32", "convgemm_out_size"]:
         assert must in names
 
 
@@ -205,3 +208,59 @@ def test_profile_enable_is_host_only(lib):
     assert lib.ltlt_profile_enable(0) == 0
     assert lib.ltlt_profile_enable(3) == -1
     assert lib.ltlt_profile_enable(-1) == -1
+
+
+# convgemm_f32(kn, kh, kw, ci, hi, wi, b, stride, pad, F, I, O, accumulate, mt, nt, stream)
+CG_OK = (8, 3, 3, 2, 9, 9, 2, 1, 1, 1, 1, 1, 0, 0, 0, NULL)
+
+
+def _cg(**kw):
+    names = ["kn", "kh", "kw", "ci", "hi", "wi", "b", "s", "p", "F", "I", "O", "acc", "mt", "nt", "stream"]
+    args = dict(zip(names, CG_OK))
+    args.update(kw)
+    return tuple(args[n] for n in names)
+
+
+@pytest.mark.parametrize("args,code", [
+    (_cg(kn=0), -1),
+    (_cg(kh=0), -2),
+    (_cg(kw=-1), -3),
+    (_cg(ci=0), -4),
+    (_cg(hi=0), -5),
+    (_cg(wi=0), -6),
+    (_cg(b=-1), -7),
+    (_cg(s=0), -8),
+    (_cg(p=-1), -9),
+    (_cg(hi=1, kh=4, p=1), -5),                  # window taller than the padded input
+    (_cg(wi=2, kw=5, p=1), -6),
+    (_cg(hi=50000, wi=50000, ci=1), -5),         # input sample beyond 2^31 floats
+    (_cg(kh=2, kw=1, ci=1 << 30, hi=1, wi=1, p=1), -2),  # kh kw ci = 2^31
+    (_cg(hi=4000, wi=4000, kh=1, kw=1, ci=1, b=200), -7),  # ho wo b beyond 2^31
+    (_cg(acc=2), -13),
+    (_cg(mt=128, nt=64), -14),
+    (_cg(mt=96, nt=128), -14),
+    (_cg(F=NULL), -10),
+    (_cg(I=NULL), -11),
+    (_cg(O=NULL), -12),
+    (_cg(b=0, F=NULL, I=NULL, O=NULL), 0),       # empty batch: nothing to do
+])
+def test_convgemm_argument_checks(lib, args, code):
+    assert lib.convgemm_f32(*args) == code
+
+
+def test_convgemm_out_size_matches_oracle():
+    from oracle import conv as oc
+    for h in range(1, 12):
+        for k in range(1, 6):
+            for s in range(1, 4):
+                for p in range(0, 3):
+                    try:
+                        want = oc.out_size(h, k, s, p)
+                    except ValueError:
+                        want = -1
+                    assert lib_out_size(h, k, s, p) == want
+    assert lib_out_size(5, 0, 1, 0) == -1 and lib_out_size(5, 3, 0, 0) == -1 and lib_out_size(5, 3, 1, -1) == -1
+
+
+def lib_out_size(h, k, s, p):
+    return lt.load().convgemm_out_size(h, k, s, p)

@@ -1,0 +1,196 @@
+"""GPU parity of CONVGEMM (``convgemm_f32`` through the C ABI) against the
+convolution oracle (direct loops of the paper's Figure 4, fp64).
+
+* integer-valued inputs: bit-exact (every partial sum is an integer < 2^24);
+* Gaussian / uniform inputs: within gamma_{K+1} * conv(|F|, |I|) entrywise and
+  1e-5 normwise (see ``conv_util``);
+* every workgroup tile (64x64, 64x128, 64x256, 128x128, 192x128) on the same
+  ragged problem (filter count, contraction length and output count not
+  multiples of any tile), strides 1-4, padding 0-3, non-square inputs and
+  filters, 1x1 filters, a single output position, an empty batch, kn not a
+  multiple of 4 and a misaligned output (scalar epilogue), accumulate mode;
+* the AlexNet layers of the paper's Table 2 at b = 2 in full, and at the
+  benchmarked b = 80 on sampled outputs (each computed one by one by the
+  oracle) plus bit-exact integer runs sampled the same way.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2005_06410_amd as lt
+import synth
+from conv_util import bound, check_close, dev, host
+from oracle import conv as oc
+from synth import conv as sc
+
+pytestmark = pytest.mark.gpu
+
+TILES = [(64, 64), (64, 128), (64, 256), (128, 128), (192, 128)]
+
+
+def run(F, I, s, p, tile=(0, 0), out=None, accumulate=False):
+    Fd, Id = dev(F), dev(I)
+    O = lt.convgemm(Fd, Id, stride=s, pad=p, tile=tile, out=out, accumulate=accumulate)
+    torch.cuda.synchronize()
+    return O
+
+
+def int_case(kn, kh, kw, ci, hi, wi, b, seed, lo=-3, hi_=3):
+    F = sc.int_tensor((kn, kh, kw, ci), seed, lo, hi_, index=5)
+    I = sc.int_tensor((hi, wi, ci, b), seed, lo, hi_, index=6)
+    return F, I
+
+
+def gauss_case(kn, kh, kw, ci, hi, wi, b, seed):
+    return sc.filter_tensor(kn, kh, kw, ci, seed), sc.input_tensor(hi, wi, ci, b, seed)
+
+
+RAGGED = (70, 3, 3, 7, 23, 17, 3)     # kn=70, K=63, N=21*15*3=945 at s=1 p=0
+
+
+@pytest.mark.parametrize("tile", TILES)
+def test_every_tile_integer_exact(tile):
+    kn, kh, kw, ci, hi, wi, b = RAGGED
+    F, I = int_case(kn, kh, kw, ci, hi, wi, b, 40)
+    print(f"[conv] tile {tile} integer ragged", flush=True)
+    got = host(run(F, I, 1, 0, tile))
+    assert np.array_equal(got.astype(np.float64), oc.conv_direct(F, I, 1, 0))
+
+
+@pytest.mark.parametrize("tile", TILES)
+def test_every_tile_gaussian(tile):
+    kn, kh, kw, ci, hi, wi, b = RAGGED
+    F, I = gauss_case(kn, kh, kw, ci, hi, wi, b, 41)
+    print(f"[conv] tile {tile} gaussian ragged, stride 2 pad 1", flush=True)
+    got = host(run(F, I, 2, 1, tile))
+    check_close(got, oc.conv_direct(F, I, 2, 1), bound(F, I, 2, 1, oc), f"tile {tile}")
+
+
+GEOMS = [
+    # kn, kh, kw, ci, hi, wi, b, s, p
+    (5, 3, 2, 3, 11, 9, 3, 2, 1),
+    (16, 1, 1, 9, 7, 5, 4, 1, 0),       # 1x1 filters: a channel product
+    (12, 4, 4, 2, 9, 13, 2, 3, 2),
+    (8, 5, 3, 4, 10, 12, 2, 4, 3),      # stride above the filter: skipped rows
+    (7, 3, 3, 5, 3, 3, 1, 1, 0),        # one output position (kn not a multiple of 4)
+    (3, 2, 2, 1, 4, 4, 1, 2, 3),        # padding wider than the filter: zero borders
+    (33, 7, 7, 3, 30, 28, 2, 2, 3),
+    (130, 3, 3, 17, 12, 12, 5, 1, 1),
+]
+
+
+@pytest.mark.parametrize("g", GEOMS)
+def test_geometries_integer_exact(g):
+    kn, kh, kw, ci, hi, wi, b, s, p = g
+    F, I = int_case(kn, kh, kw, ci, hi, wi, b, 42)
+    print(f"[conv] geometry {g} integer", flush=True)
+    got = host(run(F, I, s, p))
+    assert np.array_equal(got.astype(np.float64), oc.conv_direct(F, I, s, p))
+
+
+@pytest.mark.parametrize("g", GEOMS)
+def test_geometries_gaussian(g):
+    kn, kh, kw, ci, hi, wi, b, s, p = g
+    F, I = gauss_case(kn, kh, kw, ci, hi, wi, b, 43)
+    print(f"[conv] geometry {g} gaussian", flush=True)
+    got = host(run(F, I, s, p))
+    check_close(got, oc.conv_direct(F, I, s, p), bound(F, I, s, p, oc), str(g))
+
+
+def test_accumulate_adds_to_output():
+    kn, kh, kw, ci, hi, wi, b = RAGGED
+    F, I = gauss_case(kn, kh, kw, ci, hi, wi, b, 44)
+    ho, wo = hi - kh + 1, wi - kw + 1
+    O0 = np.asfortranarray(synth.rng_for(45).standard_normal((kn, ho, wo, b)).astype(np.float32))
+    out = dev(O0)
+    got = host(run(F, I, 1, 0, out=out, accumulate=True))
+    ref = oc.conv_direct(F, I, 1, 0) + O0.astype(np.float64)
+    bnd = bound(F, I, 1, 0, oc) + U_ROUND * (np.abs(ref) + np.abs(O0))
+    check_close(got, ref, bnd, "accumulate")
+
+
+U_ROUND = 2.0 ** -24
+
+
+def test_misaligned_output_uses_scalar_stores():
+    kn, kh, kw, ci, hi, wi, b = 8, 3, 3, 4, 10, 9, 2
+    F, I = int_case(kn, kh, kw, ci, hi, wi, b, 46)
+    ho, wo = hi - kh + 1, wi - kw + 1
+    n = kn * ho * wo * b
+    flat = torch.full((n + 1,), 7.0, dtype=torch.float32, device="cuda")
+    out = flat[1:].as_strided((kn, ho, wo, b), (1, kn, kn * ho, kn * ho * wo))
+    assert out.data_ptr() % 16 != 0
+    got = host(run(F, I, 1, 0, out=out))
+    assert np.array_equal(got.astype(np.float64), oc.conv_direct(F, I, 1, 0))
+    assert float(flat[0].item()) == 7.0
+
+
+def test_empty_batch():
+    F = dev(sc.filter_tensor(4, 3, 3, 2, 1))
+    I = torch.empty(0, dtype=torch.float32, device="cuda").as_strided((6, 6, 2, 0), (1, 6, 36, 72))
+    O = lt.convgemm(F, I)
+    torch.cuda.synchronize()
+    assert tuple(O.shape) == (4, 4, 4, 0)
+
+
+@pytest.mark.parametrize("spec", sc.ALEXNET_CONV, ids=lambda s: f"layer{s['layer']}")
+def test_alexnet_layer_b2_full(spec):
+    """Every output of an AlexNet layer (Table 2 shapes) at b = 2."""
+    F, I = sc.layer_tensors(spec, 2, sc.layer_seed(spec))
+    print(f"[conv] AlexNet layer {spec['layer']} b=2", flush=True)
+    got = host(run(F, I, spec["s"], spec["p"]))
+    ref = oc.conv_direct(F, I, spec["s"], spec["p"])
+    check_close(got, ref, bound(F, I, spec["s"], spec["p"], oc), f"layer {spec['layer']}")
+
+
+def sample_points(shape, count, seed):
+    """Random output positions plus every corner and the first/last entries
+    along each dimension (tile edges in both GEMM directions)."""
+    rng = synth.rng_for(seed)
+    pts = np.stack([rng.integers(0, d, count) for d in shape], axis=1)
+    edges = []
+    for k in (0, 1, 63, 64, 127, 128, 191, 192, shape[0] - 1):
+        for b in (0, shape[3] - 1):
+            for oh in (0, shape[1] - 1):
+                for ow in (0, shape[2] - 1):
+                    if k < shape[0]:
+                        edges.append((k, oh, ow, b))
+    return np.concatenate([pts, np.array(edges, dtype=np.int64)])
+
+
+@pytest.mark.parametrize("spec", sc.ALEXNET_CONV, ids=lambda s: f"layer{s['layer']}")
+def test_alexnet_layer_full_batch_sampled(spec):
+    """The benchmarked configuration (b = 80, automatic tile, the benchmark's
+    inputs): 20000 sampled outputs against the oracle's one-by-one sums, and
+    the output checked finite everywhere."""
+    b = sc.ALEXNET_BATCH
+    F, I = sc.layer_tensors(spec, b, sc.layer_seed(spec))
+    print(f"[conv] AlexNet layer {spec['layer']} b={b} sampled", flush=True)
+    O = run(F, I, spec["s"], spec["p"])
+    assert bool(torch.isfinite(O).all())
+    pts = sample_points(tuple(O.shape), 20000, 47 + spec["layer"])
+    idx = torch.from_numpy(pts).cuda()
+    got = O[idx[:, 0], idx[:, 1], idx[:, 2], idx[:, 3]].double().cpu().numpy()
+    ref = oc.conv_points(F, I, pts, spec["s"], spec["p"])
+    absref = oc.conv_points(np.abs(F), np.abs(I), pts, spec["s"], spec["p"])
+    K = spec["kh"] * spec["kw"] * spec["ci"]
+    g = (K + 1) * U_ROUND / (1 - (K + 1) * U_ROUND)
+    err = np.abs(got - ref)
+    assert (err <= g * absref).all(), f"max error {err.max():.3e}"
+    assert err.max() / np.abs(ref).max() <= 1e-5
+
+
+@pytest.mark.parametrize("spec", sc.ALEXNET_CONV, ids=lambda s: f"layer{s['layer']}")
+def test_alexnet_layer_full_batch_integer_sampled(spec):
+    """Integer-valued inputs at the benchmarked size: sampled outputs bit-exact."""
+    b = sc.ALEXNET_BATCH
+    F = sc.int_tensor((spec["kn"], spec["kh"], spec["kw"], spec["ci"]), 48, -3, 3, index=7)
+    I = sc.int_tensor((spec["hi"], spec["wi"], spec["ci"], b), 48, 0, 3, index=8)
+    print(f"[conv] AlexNet layer {spec['layer']} b={b} integer sampled", flush=True)
+    O = run(F, I, spec["s"], spec["p"])
+    pts = sample_points(tuple(O.shape), 20000, 49 + spec["layer"])
+    idx = torch.from_numpy(pts).cuda()
+    got = O[idx[:, 0], idx[:, 1], idx[:, 2], idx[:, 3]].double().cpu().numpy()
+    assert np.array_equal(got, oc.conv_points(F, I, pts, spec["s"], spec["p"]))
