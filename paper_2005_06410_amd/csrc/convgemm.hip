@@ -51,7 +51,7 @@ struct Geometry {
     int64_t sample;     // hi*wi*ci: input floats per batch entry
 };
 
-template <int MT, int NT>
+template <int MT, int NT, bool PAD>
 __global__ __launch_bounds__(kThreads) void convgemm_kernel(Geometry g, const float* __restrict__ F,
                                                             const float* __restrict__ I,
                                                             float* __restrict__ O, int accumulate,
@@ -59,10 +59,12 @@ __global__ __launch_bounds__(kThreads) void convgemm_kernel(Geometry g, const fl
 {
     constexpr int WM = MT / 2, WN = NT / 2;        // wave tile
     constexpr int BM = WM / 16, BN = WN / 16;      // 16 x 16 blocks per wave
-    constexpr int AE = MT * kKC / kThreads;        // F^ values per thread per chunk
+    constexpr int AK = MT == 64 ? 4 : (MT == 128 ? 8 : 16);   // contraction rows per F^-loading thread
+    constexpr int ATHREADS = MT * kKC / AK;        // threads that load F^ (whole waves)
     constexpr int RPT = kKC * NT / kThreads;       // im2col rows per thread per chunk
-    static_assert(AE * kThreads == MT * kKC && RPT * kThreads == kKC * NT, "tile must split evenly");
-    static_assert(RPT % 4 == 0 && BM >= 1 && BN >= 1, "tile shape");
+    static_assert(ATHREADS <= kThreads && ATHREADS % 64 == 0 && ATHREADS * AK == MT * kKC && AK % 4 == 0,
+                  "F^ loader split");
+    static_assert(RPT * kThreads == kKC * NT && RPT % 4 == 0 && BM >= 1 && BN >= 1, "tile shape");
 
     __shared__ __attribute__((aligned(16))) float As[2][MT * kKP];
     __shared__ __attribute__((aligned(16))) float Bs[2][NT * kKP];
@@ -82,43 +84,58 @@ __global__ __launch_bounds__(kThreads) void convgemm_kernel(Geometry g, const fl
     const int wave = tid >> 6;
     const int wm = wave & 1, wn = wave >> 1;
 
-    // This thread's output position for the gather, decoded once.
-    const int bcol = tid % NT;
-    const int brow = (tid / NT) * RPT;
-    const int ncol = n0 + bcol;
-    const bool col_ok = ncol < g.N;
-    int hbase = 0, wbase = 0;
-    int64_t cbase = 0;
-    if (col_ok) {
-        const int nb = ncol / g.hw;
-        const int rem = ncol - nb * g.hw;
-        const int ow = rem / g.ho;
-        const int oh = rem - ow * g.ho;
-        hbase = oh * g.s - g.p;
-        wbase = ow * g.s - g.p;
-        cbase = (int64_t)nb * g.sample;
-    }
-    const float* __restrict__ Ib = I + cbase;
+    // F^ loader: filter am (clamped: rows past kn only feed outputs that are
+    // never stored), contraction rows akg .. akg+AK-1 of each chunk.
+    const bool a_loader = tid < ATHREADS;            // whole waves
+    const int am = tid % MT;
+    const int akg = (tid / MT) * AK;
+    const int am_c = min(m0 + am, g.M - 1);
+    const uint32_t aoff = (uint32_t)(akg * g.M + am_c) * 4u;   // bytes from row k0 of F^
 
-    // Raw loaded values and, per value, whether it is a real entry (bit j of
-    // amask / bmask).  Out-of-range lanes load from a clamped valid address;
-    // the zeroing is applied when the chunk is written to LDS, after the
-    // MFMAs, so that nothing waits for the loads before the MFMAs are issued.
-    float ra[AE];
+    // im2col gatherer: output position bcol of the tile (clamped to the last
+    // one: columns past N only feed outputs that are never stored), decoded
+    // once into (oh, ow, n); contraction rows brow .. brow+RPT-1 of each chunk.
+    // brow is the same for a whole wave, so the row -> (y, x, c) walk and the
+    // row's offset y + hi*x + hi*wi*c live in scalar registers.
+    const int bcol = tid % NT;
+    const int brow = __builtin_amdgcn_readfirstlane((tid / NT) * RPT);
+    const int ncol = min(n0 + bcol, g.N - 1);
+    const int nb = ncol / g.hw;
+    const int prem = ncol - nb * g.hw;
+    const int ow = prem / g.ho;
+    const int oh = prem - ow * g.ho;
+    const int hbase = oh * g.s - g.p;
+    const int wbase = ow * g.s - g.p;
+    // without padding every tap of a valid column is inside the input: the
+    // element is I[colpos + row offset], colpos < 2^30 (checked on the host)
+    const uint32_t colbyte = PAD ? 0u : (uint32_t)(nb * g.sample + hbase + g.hi * wbase) * 4u;
+    const float* __restrict__ Ib = I + (int64_t)nb * g.sample;
+
+    float ra[AK];
     float rb[RPT];
-    uint32_t amask, bmask;
+    uint32_t amask = ~0u, bmask = ~0u;   // bit j: value j is a real entry (else stored as 0)
 
     auto load_chunk = [&](int chunk) {
         const int k0 = chunk * kKC;
-        amask = 0;
+        const bool tail = k0 + kKC > g.K;            // uniform: only the last chunk can be partial
+        if (a_loader) {
+            if (!tail) {
 #pragma unroll
-        for (int j = 0; j < AE; ++j) {
-            const int e = tid + kThreads * j;
-            const int m = m0 + e % MT;
-            const int k = k0 + e / MT;
-            const bool ok = m < g.M && k < g.K;
-            ra[j] = F[ok ? (int64_t)k * g.M + m : 0];
-            amask |= (uint32_t)ok << j;
+                for (int i = 0; i < AK; ++i) {
+                    const char* base = reinterpret_cast<const char*>(F + (int64_t)(k0 + i) * g.M);
+                    ra[i] = *reinterpret_cast<const float*>(base + aoff);
+                }
+                amask = ~0u;
+            } else {
+                amask = 0;
+#pragma unroll
+                for (int i = 0; i < AK; ++i) {
+                    const int k = k0 + akg + i;
+                    const bool ok = k < g.K;
+                    ra[i] = F[(int64_t)(ok ? k : g.K - 1) * g.M + am_c];
+                    amask |= (uint32_t)ok << i;
+                }
+            }
         }
         const int r0 = k0 + brow;
         int c = r0 / g.khw;
@@ -128,12 +145,20 @@ __global__ __launch_bounds__(kThreads) void convgemm_kernel(Geometry g, const fl
         bmask = 0;
 #pragma unroll
         for (int j = 0; j < RPT; ++j) {
-            const int hh = hbase + y, ww = wbase + x;
-            const bool ok = col_ok && (r0 + j) < g.K && (unsigned)hh < (unsigned)g.hi &&
-                            (unsigned)ww < (unsigned)g.wi;
-            rb[j] = Ib[ok ? hh + g.hi * ww + g.hiwi * c : 0];
-            bmask |= (uint32_t)ok << j;
-            // next contraction row: y fastest, then x, then c (branch-free)
+            const bool rok = r0 + j < g.K;           // uniform
+            if (!PAD) {
+                const int roff = rok ? y + g.hi * x + g.hiwi * c : 0;
+                const char* base = reinterpret_cast<const char*>(I + roff);
+                rb[j] = *reinterpret_cast<const float*>(base + colbyte);
+                bmask |= (uint32_t)rok << j;
+            } else {
+                const int hh = hbase + y, ww = wbase + x;
+                const bool ok = rok && (unsigned)hh < (unsigned)g.hi && (unsigned)ww < (unsigned)g.wi;
+                const float v = Ib[ok ? hh + g.hi * ww + g.hiwi * c : 0];
+                rb[j] = v;
+                bmask |= (uint32_t)ok << j;
+            }
+            // next contraction row: y fastest, then x, then c
             ++y;
             const bool wy = y == g.kh;
             y = wy ? 0 : y;
@@ -144,18 +169,30 @@ __global__ __launch_bounds__(kThreads) void convgemm_kernel(Geometry g, const fl
         }
     };
 
-    auto store_chunk = [&](int buf) {
+    // The zeroing is applied here, after the MFMAs, so that nothing waits for
+    // the loads before the MFMAs are issued; full chunks without padding store
+    // the loaded values as they are.
+    auto store_chunk = [&](int buf, bool tail) {
+        if (a_loader) {
+            float* ap = &As[buf][am * kKP + akg];
 #pragma unroll
-        for (int j = 0; j < AE; ++j) {
-            const int e = tid + kThreads * j;
-            As[buf][(e % MT) * kKP + e / MT] = (amask >> j) & 1 ? ra[j] : 0.0f;
+            for (int i = 0; i < AK; i += 4) {
+                f4 v = f4{ra[i], ra[i + 1], ra[i + 2], ra[i + 3]};
+                if (tail) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) v[q] = (amask >> (i + q)) & 1 ? v[q] : 0.0f;
+                }
+                *reinterpret_cast<f4*>(ap + i) = v;
+            }
         }
         float* bp = &Bs[buf][bcol * kKP + brow];
 #pragma unroll
         for (int j = 0; j < RPT; j += 4) {
-            f4 v;
+            f4 v = f4{rb[j], rb[j + 1], rb[j + 2], rb[j + 3]};
+            if (PAD || tail) {
 #pragma unroll
-            for (int q = 0; q < 4; ++q) v[q] = (bmask >> (j + q)) & 1 ? rb[j + q] : 0.0f;
+                for (int q = 0; q < 4; ++q) v[q] = (bmask >> (j + q)) & 1 ? v[q] : 0.0f;
+            }
             *reinterpret_cast<f4*>(bp + j) = v;
         }
     };
@@ -185,7 +222,7 @@ __global__ __launch_bounds__(kThreads) void convgemm_kernel(Geometry g, const fl
 
     const int nchunks = (g.K + kKC - 1) / kKC;
     load_chunk(0);
-    store_chunk(0);
+    store_chunk(0, kKC > g.K);
     __syncthreads();
     // The scheduling barriers keep the next chunk's loads ahead of the MFMAs
     // and their LDS stores behind them, so the loads' latency is covered.
@@ -195,7 +232,7 @@ __global__ __launch_bounds__(kThreads) void convgemm_kernel(Geometry g, const fl
         __builtin_amdgcn_sched_barrier(0);
         compute(buf);
         __builtin_amdgcn_sched_barrier(0);
-        store_chunk(buf ^ 1);
+        store_chunk(buf ^ 1, (chunk + 2) * kKC > g.K);
         __syncthreads();
     }
     compute((nchunks - 1) & 1);
@@ -270,8 +307,12 @@ hipError_t launch(const Geometry& g, const float* F, const float* I, float* O, i
     const int ntiles = (g.N + NT - 1) / NT;
     const int64_t tiles = (int64_t)mtiles * ntiles;
     if (tiles > 0x7fffffff) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((convgemm_kernel<MT, NT>), dim3((unsigned)tiles), dim3(kThreads), 0, stream, g, F, I, O,
-                       accumulate, vec, mtiles, ntiles);
+    if (g.p == 0)
+        hipLaunchKernelGGL((convgemm_kernel<MT, NT, false>), dim3((unsigned)tiles), dim3(kThreads), 0, stream, g, F,
+                           I, O, accumulate, vec, mtiles, ntiles);
+    else
+        hipLaunchKernelGGL((convgemm_kernel<MT, NT, true>), dim3((unsigned)tiles), dim3(kThreads), 0, stream, g, F,
+                           I, O, accumulate, vec, mtiles, ntiles);
     return hipGetLastError();
 }
 
@@ -313,6 +354,8 @@ extern "C" int convgemm_f32(int kn, int kh, int kw, int ci, int hi, int wi, int 
     if ((int64_t)hi * wi * ci >= ((int64_t)1 << 31)) return -5;
     if ((int64_t)kh * kw * ci >= ((int64_t)1 << 31)) return -2;
     if ((int64_t)ho * wo * b >= ((int64_t)1 << 31)) return -7;
+    if ((int64_t)hi * wi * ci * b >= ((int64_t)1 << 30)) return -7;
+    if (kn >= (1 << 24) || (int64_t)kn * kh * kw * ci >= ((int64_t)1 << 31)) return -1;
     if (accumulate != 0 && accumulate != 1) return -13;
     const bool auto_tile = mt == 0 && nt == 0;
     if (!auto_tile && !((mt == 64 && (nt == 64 || nt == 128 || nt == 256)) || (mt == 128 && nt == 128) ||
