@@ -68,7 +68,7 @@ int convgemm_out_size(int h, int k, int stride, int pad);
  * Limits (else the argument named is reported invalid): hi*wi*ci and
  * kh*kw*ci below 2^31 (hi, kh); ho*wo*b below 2^31 and the whole input
  * hi*wi*ci*b below 2^30 elements, 4 GiB (b); kn below 2^24 and the filter
- * tensor kn*kh*kw*ci below 2^31 elements (kn). */
+ * tensor kn*kh*kw*ci below 2^30 elements (kn). */
 int convgemm_f32(int kn, int kh, int kw, int ci, int hi, int wi, int b, int stride, int pad,
                  const float* F, const float* I, float* O, int accumulate, int mt, int nt,
                  hipStream_t stream);

@@ -49,7 +49,23 @@ struct Geometry {
     int ho, hw;         // ho, ho*wo
     int s, p;
     int64_t sample;     // hi*wi*ci: input floats per batch entry
+    uint32_t ibytes;    // bytes of I (< 2^32)
+    uint32_t fbytes;    // bytes of F (< 2^32)
 };
+
+// Raw buffer resource over a whole tensor: base address, no stride, the
+// tensor's size in bytes as the range, 32-bit data format.  A buffer load
+// then takes a per-lane byte offset (vector) plus a wave-uniform byte offset
+// (scalar), so the gather needs no per-element address arithmetic.
+__device__ inline __amdgpu_buffer_rsrc_t tensor_rsrc(const float* p, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+__device__ inline float buffer_load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0));
+}
 
 template <int MT, int NT, bool PAD>
 __global__ __launch_bounds__(kThreads) void convgemm_kernel(Geometry g, const float* __restrict__ F,
@@ -110,6 +126,8 @@ __global__ __launch_bounds__(kThreads) void convgemm_kernel(Geometry g, const fl
     // element is I[colpos + row offset], colpos < 2^30 (checked on the host)
     const uint32_t colbyte = PAD ? 0u : (uint32_t)(nb * g.sample + hbase + g.hi * wbase) * 4u;
     const float* __restrict__ Ib = I + (int64_t)nb * g.sample;
+    const __amdgpu_buffer_rsrc_t irs = tensor_rsrc(I, g.ibytes);
+    const __amdgpu_buffer_rsrc_t frs = tensor_rsrc(F, g.fbytes);
 
     float ra[AK];
     float rb[RPT];
@@ -121,10 +139,7 @@ __global__ __launch_bounds__(kThreads) void convgemm_kernel(Geometry g, const fl
         if (a_loader) {
             if (!tail) {
 #pragma unroll
-                for (int i = 0; i < AK; ++i) {
-                    const char* base = reinterpret_cast<const char*>(F + (int64_t)(k0 + i) * g.M);
-                    ra[i] = *reinterpret_cast<const float*>(base + aoff);
-                }
+                for (int i = 0; i < AK; ++i) ra[i] = buffer_load(frs, aoff, (uint32_t)(k0 + i) * g.M * 4u);
                 amask = ~0u;
             } else {
                 amask = 0;
@@ -148,8 +163,7 @@ __global__ __launch_bounds__(kThreads) void convgemm_kernel(Geometry g, const fl
             const bool rok = r0 + j < g.K;           // uniform
             if (!PAD) {
                 const int roff = rok ? y + g.hi * x + g.hiwi * c : 0;
-                const char* base = reinterpret_cast<const char*>(I + roff);
-                rb[j] = *reinterpret_cast<const float*>(base + colbyte);
+                rb[j] = buffer_load(irs, colbyte, (uint32_t)roff * 4u);
                 bmask |= (uint32_t)rok << j;
             } else {
                 const int hh = hbase + y, ww = wbase + x;
@@ -273,30 +287,15 @@ struct Tile {
     int mt, nt;
 };
 
-// Tile choice: the least padded work; among near ties (within 5 %) the tile
-// that still gives at least three workgroups per compute unit, then the larger
-// filter tile (fewer re-gathers of the same input).
+// Tile choice (measured on the AlexNet layers): 128 x 128 tiles when the
+// filter count is a multiple of 128 and they still give at least four
+// workgroups per compute unit; otherwise 64 x 64 tiles, whose small register
+// and LDS footprint keeps four or more workgroups resident per compute unit.
 Tile choose_tile(int M, int N, int cus)
 {
-    static const Tile cand[] = {{192, 128}, {128, 128}, {64, 256}, {64, 128}, {64, 64}};
-    double best_pad = 1e300;
-    for (const Tile& c : cand) {
-        const double pad = (double)((M + c.mt - 1) / c.mt) * c.mt * ((double)((N + c.nt - 1) / c.nt) * c.nt);
-        if (pad < best_pad) best_pad = pad;
-    }
-    const Tile* pick = nullptr;
-    int64_t pick_tiles = -1;
-    for (const Tile& c : cand) {
-        const double pad = (double)((M + c.mt - 1) / c.mt) * c.mt * ((double)((N + c.nt - 1) / c.nt) * c.nt);
-        if (pad > 1.05 * best_pad) continue;
-        const int64_t tiles = (int64_t)((M + c.mt - 1) / c.mt) * ((N + c.nt - 1) / c.nt);
-        if (tiles >= 3 * (int64_t)cus) return c;
-        if (tiles > pick_tiles) {
-            pick = &c;
-            pick_tiles = tiles;
-        }
-    }
-    return *pick;
+    const int64_t t128 = (int64_t)((M + 127) / 128) * ((N + 127) / 128);
+    if (M % 128 == 0 && t128 >= 4 * (int64_t)cus) return Tile{128, 128};
+    return Tile{64, 64};
 }
 
 template <int MT, int NT>
@@ -355,7 +354,7 @@ extern "C" int convgemm_f32(int kn, int kh, int kw, int ci, int hi, int wi, int 
     if ((int64_t)kh * kw * ci >= ((int64_t)1 << 31)) return -2;
     if ((int64_t)ho * wo * b >= ((int64_t)1 << 31)) return -7;
     if ((int64_t)hi * wi * ci * b >= ((int64_t)1 << 30)) return -7;
-    if (kn >= (1 << 24) || (int64_t)kn * kh * kw * ci >= ((int64_t)1 << 31)) return -1;
+    if (kn >= (1 << 24) || (int64_t)kn * kh * kw * ci >= ((int64_t)1 << 30)) return -1;
     if (accumulate != 0 && accumulate != 1) return -13;
     const bool auto_tile = mt == 0 && nt == 0;
     if (!auto_tile && !((mt == 64 && (nt == 64 || nt == 128 || nt == 256)) || (mt == 128 && nt == 128) ||
@@ -381,6 +380,8 @@ extern "C" int convgemm_f32(int kn, int kh, int kw, int ci, int hi, int wi, int 
     g.s = stride;
     g.p = pad;
     g.sample = (int64_t)hi * wi * ci;
+    g.ibytes = (uint32_t)(g.sample * b * 4);
+    g.fbytes = (uint32_t)((int64_t)kn * g.K * 4);
 
     const int vec = (kn % 4 == 0) && ((uintptr_t)O % 16 == 0);
     Tile t = auto_tile ? choose_tile(g.M, g.N, device_cus()) : Tile{mt, nt};

@@ -236,6 +236,7 @@ def _cg(**kw):
     (_cg(hi=50000, wi=50000, ci=1), -5),         # input sample beyond 2^31 floats
     (_cg(kh=2, kw=1, ci=1 << 30, hi=1, wi=1, p=1), -2),  # kh kw ci = 2^31
     (_cg(hi=4000, wi=4000, kh=1, kw=1, ci=1, b=200), -7),  # ho wo b beyond 2^31
+    (_cg(kn=2, kh=1, kw=1, ci=1 << 29, hi=1, wi=1, b=1, p=0), -1),  # filter tensor 2^30 elements
     (_cg(acc=2), -13),
     (_cg(mt=128, nt=64), -14),
     (_cg(mt=96, nt=128), -14),
