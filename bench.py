@@ -17,7 +17,10 @@ Prints one JSON line.  `--workload batched` instead times the batched path
 against HBM bandwidth; `--workload complex` the factorization + Pfaffian of a
 complex128 (or, with --dtype f32, complex64) skew-symmetric matrix;
 `--workload cpu-oracle` runs the whole CPU oracle at --n on the host's cores
-(no GPU) and prints its rate.
+(no GPU) and prints its rate; `--workload convgemm` times the paper's own
+operator, CONVGEMM (convolution as one GEMM with im2col folded into operand
+staging), over the five AlexNet convolution layers of the paper's Table 2 at
+batch --conv-batch (default 80), in fp32 TFLOP/s.
 """
 from __future__ import annotations
 
@@ -46,8 +49,11 @@ def parse():
     ap.add_argument("--seed", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--workload", choices=["factor", "batched", "pfaffian", "solve", "complex", "cpu-oracle"],
+    ap.add_argument("--workload", choices=["factor", "batched", "pfaffian", "solve", "complex", "cpu-oracle",
+                                           "convgemm"],
                     default="factor")
+    ap.add_argument("--conv-batch", type=int, default=80, help="convgemm workload: batch size b")
+    ap.add_argument("--tile", default="0,0", help="convgemm workload: workgroup tile mt,nt (0,0 = automatic)")
     ap.add_argument("--nrhs", type=int, default=1)
     ap.add_argument("--batch", type=int, default=8192)
     ap.add_argument("--input", choices=["gauss", "graded", "blockdiag4"], default="gauss",
@@ -186,17 +192,17 @@ INPUT_TEXT = {
 KERNEL_HEADERS = ("ltlt_device.h", "ltlt_internal.h")
 
 
-def kernel_source_hash(source):
+def kernel_source_hash(source, headers=KERNEL_HEADERS):
     """sha256 of a kernel source followed by the shared headers it includes."""
     import hashlib
     h = hashlib.sha256()
-    for name in (source, *KERNEL_HEADERS):
+    for name in (source, *headers):
         with open(os.path.join(ROOT, "paper_2005_06410_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
 
 
-def measured_traffic(summary, source):
+def measured_traffic(summary, source, headers=KERNEL_HEADERS):
     """HBM bytes per launch from a committed counter summary under profiles/
     (two rocprofv3 --pmc passes, FETCH_SIZE and WRITE_SIZE, scaled by a copy of
     known size), or None when the kernel's code (its source or the headers it
@@ -208,12 +214,162 @@ def measured_traffic(summary, source):
             if ":" in line and not line.startswith(("|", "#", " ", "-", "`")):
                 k, v = line.split(":", 1)
                 fields[k.strip()] = v.strip()
-        h = kernel_source_hash(source)
+        h = kernel_source_hash(source, headers)
         if not h.startswith(fields.get("source_sha256_prefix", "-")):
             return None
         return float(fields["traffic_bytes_per_launch"])
     except (OSError, KeyError, ValueError):
         return None
+
+
+def conv_tensor_dev(a, torch):
+    """numpy array (stored leftmost index fastest) -> GPU tensor, same layout."""
+    import numpy as np
+    a = np.asfortranarray(a)
+    strides, acc = [], 1
+    for d in a.shape:
+        strides.append(acc)
+        acc *= d
+    flat = torch.from_numpy(np.ravel(a, order="F").copy()).to("cuda:0")
+    return flat.as_strided(a.shape, tuple(strides))
+
+
+def cpu_baseline_conv(specs, target_s):
+    """The convolution oracle (direct loops of the paper's Figure 4 in scalar C,
+    OpenMP over the batch index) on the same five layers at a batch of one
+    entry per thread, repeated to about ``target_s`` seconds."""
+    from oracle import conv as oc
+    from synth import conv as sc
+    threads = oracle_threads()
+    oc.set_threads(threads)
+    b = threads
+    tensors = [sc.layer_tensors(sp, b, sc.layer_seed(sp)) for sp in specs]
+    flops = 0.0
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        for sp, (F, I) in zip(specs, tensors):
+            O = oc.conv_direct(F, I, sp["s"], sp["p"])
+            flops += 2.0 * O.size * sp["kh"] * sp["kw"] * sp["ci"]
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= target_s or reps >= 50:
+            break
+    return {
+        "value": flops / dt / 1e12,
+        "unit": "TFLOP/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"the five layers at batch {b} (one entry per thread), {reps} pass(es), {dt:.1f} s, "
+                  f"fp64 sums of fp32 products",
+        **host_info(),
+    }
+
+
+def run_convgemm(args):
+    """The paper's own operator on MI355X: the five AlexNet convolution layers
+    (Table 2) at batch b, each as one CONVGEMM launch on resident inputs.
+
+    One step = the five layers in sequence.  The roofline is that of the
+    dominant launch (layer 4, about half of the flops): algorithmic flops
+    2 kn ho wo b kh kw ci per launch over its average HIP-event duration in
+    the timed steps, against the fp32 matrix-core peak."""
+    import torch
+
+    import paper_2005_06410_amd as lt
+    from synth import conv as sc
+    b = args.conv_batch
+    mt, nt = (int(v) for v in args.tile.split(","))
+    stream = torch.cuda.current_stream(torch.device("cuda:0"))
+    layers = []
+    for sp in sc.ALEXNET_CONV:
+        F, I = sc.layer_tensors(sp, b, sc.layer_seed(sp))
+        ho = lt.conv_out_size(sp["hi"], sp["kh"], sp["s"], sp["p"])
+        wo = lt.conv_out_size(sp["wi"], sp["kw"], sp["s"], sp["p"])
+        kn = sp["kn"]
+        O = torch.empty(kn * ho * wo * b, dtype=torch.float32, device="cuda:0").as_strided(
+            (kn, ho, wo, b), (1, kn, kn * ho, kn * ho * wo))
+        layers.append(dict(spec=sp, F=conv_tensor_dev(F, torch), I=conv_tensor_dev(I, torch), O=O,
+                           flops=2.0 * kn * ho * wo * b * sp["kh"] * sp["kw"] * sp["ci"],
+                           gemm=(kn, ho * wo * b, sp["kh"] * sp["kw"] * sp["ci"])))
+        del F, I
+
+    # a plain copy of known size (256 MiB read + 256 MiB written), untimed: the
+    # calibration that the HBM counter passes of this workload are scaled by
+    calib_src = torch.ones(64 << 20, dtype=torch.float32, device="cuda:0")
+    calib_dst = torch.empty_like(calib_src)
+    calib_dst.copy_(calib_src)
+    del calib_src, calib_dst
+
+    def step():
+        evs = []
+        for L in layers:
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            lt.convgemm(L["F"], L["I"], L["spec"]["s"], L["spec"]["p"], out=L["O"], tile=(mt, nt))
+            e1.record(stream)
+            evs.append((e0, e1))
+        return evs
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    all_evs = [step() for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    per_layer = [[a.elapsed_time(e) for a, e in (evs[i] for evs in all_evs)] for i in range(len(layers))]
+    step_ms = [evs[0][0].elapsed_time(evs[-1][1]) for evs in all_evs]
+    ms_step = sum(step_ms) / len(step_ms)
+    total_flops = sum(L["flops"] for L in layers)
+    value = total_flops / (ms_step * 1e-3) / 1e12
+    dom = max(range(len(layers)), key=lambda i: layers[i]["flops"])
+    dom_ms = sum(per_layer[dom]) / len(per_layer[dom])
+    achieved = layers[dom]["flops"] / (dom_ms * 1e-3) / 1e12
+    out = {
+        "metric": f"CONVGEMM, AlexNet convolution layers (paper Table 2) at b={b}: fp32 TFLOP/s",
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"the five AlexNet convolution layers of the paper's Table 2 (inputs 224x224x3 .. "
+                        f"13x13x384, stride 4 then 1, no padding) at batch {b}, inputs U[0,1), He-Gaussian "
+                        f"filters, each layer one implicit-im2col GEMM launch",
+            "batch": b,
+            "tile": "automatic" if (mt, nt) == (0, 0) else f"{mt}x{nt}",
+            "parallelism": "single GPU",
+        },
+        "pct_of_peak": round(100.0 * value / FP32_PEAK_TF, 2),
+        "roofline": {
+            "kernel": f"convgemm_kernel, layer {layers[dom]['spec']['layer']} "
+                      f"(GEMM {layers[dom]['gemm'][0]} x {layers[dom]['gemm'][1]} x {layers[dom]['gemm'][2]})",
+            "bound": "mfma",
+            "achieved": round(achieved, 3),
+            "peak": FP32_PEAK_TF,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / FP32_PEAK_TF, 4),
+            "traffic": (measured_traffic("convgemm_alexnet_b80_f32.md", "convgemm.hip", headers=())
+                        if (b, mt, nt) == (80, 0, 0) else None),
+            "avg_launch_ms": round(dom_ms, 5),
+        },
+        "layers": [{"layer": L["spec"]["layer"], "gemm_mnk": L["gemm"],
+                    "ms": round(sum(t) / len(t), 4),
+                    "tflops": round(L["flops"] / (sum(t) / len(t) * 1e-3) / 1e12, 3)}
+                   for L, t in zip(layers, per_layer)],
+        "wall_s_timed_region": round(wall, 3),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_conv(sc.ALEXNET_CONV, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
 
 
 def run_batched(args):
@@ -669,6 +825,9 @@ def main():
         return
     if args.workload == "complex":
         run_complex(args)
+        return
+    if args.workload == "convgemm":
+        run_convgemm(args)
         return
     dev = torch.device("cuda:0")
     n, nb = args.n, args.nb

@@ -6,20 +6,20 @@
 //
 // Mapping to CDNA4.  One workgroup (4 waves, 2 x 2) owns an MT x NT tile of O^
 // (MT filters x NT output positions).  The contraction runs in chunks of
-// kKC = 16 rows of im2col(I) (= columns of F^):
-//   * F^ chunk (MT x 16): coalesced loads along the filter index, kept in LDS
-//     as rows of 16 contraction values per filter;
-//   * im2col chunk (16 x NT): each thread owns one output position (column)
+// KC = 16 or 32 rows of im2col(I) (= columns of F^):
+//   * F^ chunk (MT x KC): coalesced loads along the filter index, kept in LDS
+//     as rows of KC contraction values per filter;
+//   * im2col chunk (KC x NT): each thread owns one output position (column)
 //     of the tile, decoded once into (oh, ow, n), and walks its contraction
 //     rows r -> (y, x, c) incrementally; the value is I at
 //     (s*oh + y - p, s*ow + x - p, c, n) or zero outside the input, exactly
 //     Figure 6's index maps.  Neighbouring threads hold neighbouring output
 //     positions, so each load instruction reads a contiguous (stride s) run of
-//     one input row.  Stored in LDS as 16 contraction values per column;
+//     one input row.  Stored in LDS as KC contraction values per column;
 //   * v_mfma_f32_16x16x4_f32 on 16 x 16 blocks.  Because the contraction may
 //     be taken in any order, lane group q of a wave (lanes 16q .. 16q+15)
-//     takes contraction rows 4q .. 4q+3 of the chunk for the four MFMAs of a
-//     chunk, so one ds_read_b128 feeds four MFMAs;
+//     takes contraction rows 4q .. 4q+3 of each group of 16 for that group's
+//     four MFMAs, so one ds_read_b128 feeds four MFMAs;
 //   * two LDS buffers: the next chunk's global loads are issued before the
 //     current chunk's MFMAs and written to the other buffer after them, one
 //     barrier per chunk.
@@ -38,8 +38,6 @@ namespace {
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
-constexpr int kKC = 16;        // contraction rows per staged chunk
-constexpr int kKP = kKC + 4;   // LDS floats per tile row (padded against bank conflicts)
 
 struct Geometry {
     int M, K, N;        // kn, kh*kw*ci, ho*wo*b
@@ -67,20 +65,23 @@ __device__ inline float buffer_load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uin
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0));
 }
 
-template <int MT, int NT, bool PAD>
+template <int MT, int NT, bool PAD, int KC>
 __global__ __launch_bounds__(kThreads) void convgemm_kernel(Geometry g, const float* __restrict__ F,
                                                             const float* __restrict__ I,
                                                             float* __restrict__ O, int accumulate,
                                                             int vec, int mtiles, int ntiles)
 {
+    constexpr int kKC = KC;                        // contraction rows per staged chunk
+    constexpr int kKP = KC + 4;                    // LDS floats per tile row (padded against bank conflicts)
     constexpr int WM = MT / 2, WN = NT / 2;        // wave tile
     constexpr int BM = WM / 16, BN = WN / 16;      // 16 x 16 blocks per wave
-    constexpr int AK = MT == 64 ? 4 : (MT == 128 ? 8 : 16);   // contraction rows per F^-loading thread
+    constexpr int AK = MT == 192 ? kKC : MT * kKC / kThreads; // contraction rows per F^-loading thread
     constexpr int ATHREADS = MT * kKC / AK;        // threads that load F^ (whole waves)
     constexpr int RPT = kKC * NT / kThreads;       // im2col rows per thread per chunk
     static_assert(ATHREADS <= kThreads && ATHREADS % 64 == 0 && ATHREADS * AK == MT * kKC && AK % 4 == 0,
                   "F^ loader split");
-    static_assert(RPT * kThreads == kKC * NT && RPT % 4 == 0 && BM >= 1 && BN >= 1, "tile shape");
+    static_assert(RPT * kThreads == kKC * NT && RPT % 4 == 0 && BM >= 1 && BN >= 1 && kKC % 16 == 0,
+                  "tile shape");
 
     __shared__ __attribute__((aligned(16))) float As[2][MT * kKP];
     __shared__ __attribute__((aligned(16))) float Bs[2][NT * kKP];
@@ -217,21 +218,26 @@ __global__ __launch_bounds__(kThreads) void convgemm_kernel(Geometry g, const fl
 #pragma unroll
         for (int j = 0; j < BN; ++j) acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
 
+    // Each group of 16 contraction rows: lane group q = lane/16 takes rows
+    // 4q .. 4q+3 of the group, one per MFMA of the group's four.
     auto compute = [&](int buf) {
         const float* ap = &As[buf][(wm * WM + (lane & 15)) * kKP + 4 * (lane >> 4)];
         const float* bp = &Bs[buf][(wn * WN + (lane & 15)) * kKP + 4 * (lane >> 4)];
-        f4 a[BM], b[BN];
 #pragma unroll
-        for (int i = 0; i < BM; ++i) a[i] = *reinterpret_cast<const f4*>(ap + i * 16 * kKP);
+        for (int g16 = 0; g16 < kKC; g16 += 16) {
+            f4 a[BM], b[BN];
 #pragma unroll
-        for (int j = 0; j < BN; ++j) b[j] = *reinterpret_cast<const f4*>(bp + j * 16 * kKP);
+            for (int i = 0; i < BM; ++i) a[i] = *reinterpret_cast<const f4*>(ap + i * 16 * kKP + g16);
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk)
+            for (int j = 0; j < BN; ++j) b[j] = *reinterpret_cast<const f4*>(bp + j * 16 * kKP + g16);
 #pragma unroll
-            for (int i = 0; i < BM; ++i)
+            for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
-                for (int j = 0; j < BN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][kk], b[j][kk], acc[i][j], 0, 0, 0);
+                for (int i = 0; i < BM; ++i)
+#pragma unroll
+                    for (int j = 0; j < BN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][kk], b[j][kk], acc[i][j], 0, 0, 0);
+        }
     };
 
     const int nchunks = (g.K + kKC - 1) / kKC;
@@ -298,20 +304,32 @@ Tile choose_tile(int M, int N, int cus)
     return Tile{64, 64};
 }
 
+// KC: 32-row chunks when the grid is short (fewer than four tiles per compute
+// unit: long contractions over few output positions, where fewer and larger
+// chunks pay), else 16-row chunks (smaller LDS footprint, more resident
+// workgroups).
 template <int MT, int NT>
 hipError_t launch(const Geometry& g, const float* F, const float* I, float* O, int accumulate, int vec,
-                  hipStream_t stream)
+                  int cus, hipStream_t stream)
 {
     const int mtiles = (g.M + MT - 1) / MT;
     const int ntiles = (g.N + NT - 1) / NT;
     const int64_t tiles = (int64_t)mtiles * ntiles;
     if (tiles > 0x7fffffff) return hipErrorInvalidConfiguration;
-    if (g.p == 0)
-        hipLaunchKernelGGL((convgemm_kernel<MT, NT, false>), dim3((unsigned)tiles), dim3(kThreads), 0, stream, g, F,
-                           I, O, accumulate, vec, mtiles, ntiles);
+    const bool long_k = tiles < 4 * (int64_t)cus;
+    const dim3 grid((unsigned)tiles), block(kThreads);
+    if (g.p == 0 && !long_k)
+        hipLaunchKernelGGL((convgemm_kernel<MT, NT, false, 16>), grid, block, 0, stream, g, F, I, O, accumulate, vec,
+                           mtiles, ntiles);
+    else if (g.p == 0)
+        hipLaunchKernelGGL((convgemm_kernel<MT, NT, false, 32>), grid, block, 0, stream, g, F, I, O, accumulate, vec,
+                           mtiles, ntiles);
+    else if (!long_k)
+        hipLaunchKernelGGL((convgemm_kernel<MT, NT, true, 16>), grid, block, 0, stream, g, F, I, O, accumulate, vec,
+                           mtiles, ntiles);
     else
-        hipLaunchKernelGGL((convgemm_kernel<MT, NT, true>), dim3((unsigned)tiles), dim3(kThreads), 0, stream, g, F,
-                           I, O, accumulate, vec, mtiles, ntiles);
+        hipLaunchKernelGGL((convgemm_kernel<MT, NT, true, 32>), grid, block, 0, stream, g, F, I, O, accumulate, vec,
+                           mtiles, ntiles);
     return hipGetLastError();
 }
 
@@ -384,17 +402,18 @@ extern "C" int convgemm_f32(int kn, int kh, int kw, int ci, int hi, int wi, int 
     g.fbytes = (uint32_t)((int64_t)kn * g.K * 4);
 
     const int vec = (kn % 4 == 0) && ((uintptr_t)O % 16 == 0);
-    Tile t = auto_tile ? choose_tile(g.M, g.N, device_cus()) : Tile{mt, nt};
+    const int cus = device_cus();
+    Tile t = auto_tile ? choose_tile(g.M, g.N, cus) : Tile{mt, nt};
     hipError_t e;
     if (t.mt == 64 && t.nt == 64)
-        e = launch<64, 64>(g, F, I, O, accumulate, vec, stream);
+        e = launch<64, 64>(g, F, I, O, accumulate, vec, cus, stream);
     else if (t.mt == 64 && t.nt == 128)
-        e = launch<64, 128>(g, F, I, O, accumulate, vec, stream);
+        e = launch<64, 128>(g, F, I, O, accumulate, vec, cus, stream);
     else if (t.mt == 64)
-        e = launch<64, 256>(g, F, I, O, accumulate, vec, stream);
+        e = launch<64, 256>(g, F, I, O, accumulate, vec, cus, stream);
     else if (t.mt == 128)
-        e = launch<128, 128>(g, F, I, O, accumulate, vec, stream);
+        e = launch<128, 128>(g, F, I, O, accumulate, vec, cus, stream);
     else
-        e = launch<192, 128>(g, F, I, O, accumulate, vec, stream);
+        e = launch<192, 128>(g, F, I, O, accumulate, vec, cus, stream);
     return e == hipSuccess ? CONVGEMM_OK : CONVGEMM_ERR_HIP_BASE - (int)e;
 }

@@ -6,8 +6,9 @@ convolution oracle (direct loops of the paper's Figure 4, fp64).
   1e-5 normwise (see ``conv_util``);
 * every workgroup tile (64x64, 64x128, 64x256, 128x128, 192x128) on the same
   ragged problem (filter count, contraction length and output count not
-  multiples of any tile), strides 1-4, padding 0-3, non-square inputs and
-  filters, 1x1 filters, a single output position, an empty batch, kn not a
+  multiples of any tile), both with few tiles (32-row contraction chunks) and
+  with many (16-row chunks), with and without padding; strides 1-4, padding
+  0-3, non-square inputs and filters, 1x1 filters, a single output position, an empty batch, kn not a
   multiple of 4 and a misaligned output (scalar epilogue), accumulate mode;
 * the AlexNet layers of the paper's Table 2 at b = 2 in full, and at the
   benchmarked b = 80 on sampled outputs (each computed one by one by the
@@ -66,6 +67,30 @@ def test_every_tile_gaussian(tile):
     print(f"[conv] tile {tile} gaussian ragged, stride 2 pad 1", flush=True)
     got = host(run(F, I, 2, 1, tile))
     check_close(got, oc.conv_direct(F, I, 2, 1), bound(F, I, 2, 1, oc), f"tile {tile}")
+
+
+# kn=70, K=63, N = 58*58*40 = 134560 (stride 1, no padding) or 60*60*40 with
+# padding 1: at least 1052 tiles for every tile shape, so the 16-row chunk
+# kernels run.
+LONG = (70, 3, 3, 7, 60, 60, 40)
+
+
+@pytest.mark.parametrize("tile", TILES)
+def test_every_tile_many_tiles_integer_exact(tile):
+    kn, kh, kw, ci, hi, wi, b = LONG
+    F, I = int_case(kn, kh, kw, ci, hi, wi, b, 50)
+    print(f"[conv] tile {tile} integer, many tiles", flush=True)
+    got = host(run(F, I, 1, 0, tile))
+    assert np.array_equal(got.astype(np.float64), oc.conv_direct(F, I, 1, 0))
+
+
+@pytest.mark.parametrize("tile", TILES)
+def test_every_tile_many_tiles_padded_gaussian(tile):
+    kn, kh, kw, ci, hi, wi, b = LONG
+    F, I = gauss_case(kn, kh, kw, ci, hi, wi, b, 51)
+    print(f"[conv] tile {tile} gaussian, many tiles, pad 1", flush=True)
+    got = host(run(F, I, 1, 1, tile))
+    check_close(got, oc.conv_direct(F, I, 1, 1), bound(F, I, 1, 1, oc), f"tile {tile} padded")
 
 
 GEOMS = [
