@@ -54,6 +54,8 @@ def parse():
                     default="factor")
     ap.add_argument("--conv-batch", type=int, default=80, help="convgemm workload: batch size b")
     ap.add_argument("--tile", default="0,0", help="convgemm workload: workgroup tile mt,nt (0,0 = automatic)")
+    ap.add_argument("--conv-path", type=int, default=0,
+                    help="convgemm workload: 0 automatic, 1 LDS-staged gather, 2 register-direct")
     ap.add_argument("--nrhs", type=int, default=1)
     ap.add_argument("--batch", type=int, default=8192)
     ap.add_argument("--input", choices=["gauss", "graded", "blockdiag4"], default="gauss",
@@ -307,7 +309,8 @@ def run_convgemm(args):
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record(stream)
-            lt.convgemm(L["F"], L["I"], L["spec"]["s"], L["spec"]["p"], out=L["O"], tile=(mt, nt))
+            lt.convgemm(L["F"], L["I"], L["spec"]["s"], L["spec"]["p"], out=L["O"], tile=(mt, nt),
+                        path=args.conv_path)
             e1.record(stream)
             evs.append((e0, e1))
         return evs
@@ -345,6 +348,7 @@ def run_convgemm(args):
                         f"13x13x384, stride 4 then 1, no padding) at batch {b}, inputs U[0,1), He-Gaussian "
                         f"filters, each layer one implicit-im2col GEMM launch",
             "batch": b,
+            "kernel": {0: "automatic", 1: "LDS-staged gather", 2: "register-direct"}[args.conv_path],
             "tile": "automatic" if (mt, nt) == (0, 0) else f"{mt}x{nt}",
             "parallelism": "single GPU",
         },
@@ -358,7 +362,7 @@ def run_convgemm(args):
             "unit": "TFLOP/s",
             "frac": round(achieved / FP32_PEAK_TF, 4),
             "traffic": (measured_traffic("convgemm_alexnet_b80_f32.md", "convgemm.hip", headers=())
-                        if (b, mt, nt) == (80, 0, 0) else None),
+                        if (b, mt, nt, args.conv_path) == (80, 0, 0, 0) else None),
             "avg_launch_ms": round(dom_ms, 5),
         },
         "layers": [{"layer": L["spec"]["layer"], "gemm_mnk": L["gemm"],

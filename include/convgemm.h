@@ -61,16 +61,23 @@ int convgemm_out_size(int h, int k, int stride, int pad);
  *   b              : batch size (>= 0);
  *   stride >= 1, pad >= 0;
  *   F, I, O        : tensors in the storage above (O: kn*ho*wo*b floats);
- *   mt, nt         : output tile of one workgroup, (0, 0) = chosen from the
- *                    sizes; otherwise one of (64, 64), (64, 128), (64, 256),
- *                    (128, 128), (192, 128) (for tests and tuning; any choice
- *                    gives results within the bound above).
+ *   path           : 0 = chosen from the sizes (then mt = nt = 0);
+ *                    1 = LDS-staged gather (any stride and padding), tile
+ *                        (mt, nt) one of (64, 64), (64, 128), (64, 256),
+ *                        (128, 128), (192, 128), or (0, 0) = chosen;
+ *                    2 = register-direct (no LDS staging; pad must be 0 and
+ *                        kh*kw*ci <= 16384), tile one of (64, 64), (64, 128),
+ *                        (128, 64), (128, 128), or (0, 0) = chosen.
+ *                    Paths and tiles are for tests and tuning: every choice
+ *                    gives results within the bound above.  An invalid path
+ *                    or path/padding/size combination is argument 14, an
+ *                    invalid tile argument 15.
  * Limits (else the argument named is reported invalid): hi*wi*ci and
  * kh*kw*ci below 2^31 (hi, kh); ho*wo*b below 2^31 and the whole input
  * hi*wi*ci*b below 2^30 elements, 4 GiB (b); kn below 2^24 and the filter
  * tensor kn*kh*kw*ci below 2^30 elements (kn). */
 int convgemm_f32(int kn, int kh, int kw, int ci, int hi, int wi, int b, int stride, int pad,
-                 const float* F, const float* I, float* O, int accumulate, int mt, int nt,
+                 const float* F, const float* I, float* O, int accumulate, int path, int mt, int nt,
                  hipStream_t stream);
 
 #ifdef __cplusplus

@@ -83,7 +83,7 @@ _SYMBOLS = {
                     ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p], ctypes.c_int),
     # include/convgemm.h
     "convgemm_out_size": ([ctypes.c_int] * 4, ctypes.c_int),
-    "convgemm_f32": ([ctypes.c_int] * 9 + [ctypes.c_void_p] * 3 + [ctypes.c_int] * 3 + [ctypes.c_void_p],
+    "convgemm_f32": ([ctypes.c_int] * 9 + [ctypes.c_void_p] * 3 + [ctypes.c_int] * 4 + [ctypes.c_void_p],
                      ctypes.c_int),
 }
 
@@ -379,14 +379,16 @@ def _leftmost_fastest(t, name):
         raise ValueError(f"{name} must be stored leftmost index fastest (strides (1, d0, d0 d1, d0 d1 d2))")
 
 
-def convgemm(F, I, stride: int = 1, pad: int = 0, out=None, accumulate: bool = False, tile=(0, 0)):
+def convgemm(F, I, stride: int = 1, pad: int = 0, out=None, accumulate: bool = False, path: int = 0,
+             tile=(0, 0)):
     """O = conv(F, I) (or O += conv(F, I) with ``accumulate``) by the
     implicit-im2col GEMM of ``convgemm_f32``.
 
     F: (kn, kh, kw, ci) and I: (hi, wi, ci, b) float32 GPU tensors stored with
     the leftmost index fastest (a numpy Fortran-order array's layout).
     Returns O (kn, ho, wo, b) in the same storage (``out`` if given).
-    ``tile`` = (mt, nt) forces a workgroup tile (tests and tuning)."""
+    ``path`` (1 LDS-staged, 2 register-direct) and ``tile`` = (mt, nt) force a
+    kernel and workgroup tile (tests and tuning); 0 / (0, 0) choose them."""
     torch = _torch()
     _require_gpu(I)
     _same_device(I, F, out)
@@ -406,7 +408,8 @@ def convgemm(F, I, stride: int = 1, pad: int = 0, out=None, accumulate: bool = F
             raise ValueError(f"out must have shape {(kn, ho, wo, b)}")
     mt, nt = tile
     code = load().convgemm_f32(kn, kh, kw, ci, hi, wi, b, int(stride), int(pad), F.data_ptr(), I.data_ptr(),
-                               out.data_ptr(), int(bool(accumulate)), int(mt), int(nt), _stream_ptr(I.device))
+                               out.data_ptr(), int(bool(accumulate)), int(path), int(mt), int(nt),
+                               _stream_ptr(I.device))
     _check("convgemm_f32", code)
     return out
 

@@ -38,6 +38,7 @@ namespace {
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
+constexpr int kDirectMaxK = 16384;   // register-direct kernel: its row table (4 bytes a row) fits 64 KiB of LDS
 
 struct Geometry {
     int M, K, N;        // kn, kh*kw*ci, ho*wo*b
@@ -63,6 +64,24 @@ __device__ inline __amdgpu_buffer_rsrc_t tensor_rsrc(const float* p, uint32_t by
 __device__ inline float buffer_load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff)
 {
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0));
+}
+
+// One lane's share of a 16 x 16 output block: filters m .. m+3 of output
+// position n (the v_mfma_f32_16x16x4_f32 result layout), contiguous in O;
+// one 16-byte store when kn is a multiple of 4 and O is 16-byte aligned (vec).
+__device__ inline void store_block(float* __restrict__ O, const Geometry& g, int m, int n, f4 v, int accumulate,
+                                   int vec)
+{
+    if (n >= g.N || m >= g.M) return;
+    float* o = O + (int64_t)n * g.M + m;
+    if (vec) {
+        if (accumulate) v += *reinterpret_cast<const f4*>(o);
+        *reinterpret_cast<f4*>(o) = v;
+    } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (m + q < g.M) o[q] = accumulate ? o[q] + v[q] : v[q];
+    }
 }
 
 template <int MT, int NT, bool PAD, int KC>
@@ -258,27 +277,150 @@ __global__ __launch_bounds__(kThreads) void convgemm_kernel(Geometry g, const fl
     compute((nchunks - 1) & 1);
 
     // Epilogue: lane holds rows 4*(lane/16) .. +3 of column lane%16 of each
-    // 16 x 16 block; four consecutive filters are contiguous in O (one 16-byte
-    // store when kn is a multiple of 4 and O is 16-byte aligned: vec).
+    // 16 x 16 block.
+#pragma unroll
+    for (int i = 0; i < BM; ++i)
+#pragma unroll
+        for (int j = 0; j < BN; ++j)
+            store_block(O, g, m0 + wm * WM + i * 16 + 4 * (lane >> 4), n0 + wn * WN + j * 16 + (lane & 15),
+                        acc[i][j], accumulate, vec);
+}
+
+// Register-direct CONVGEMM (no padding): every wave loads the operand values
+// its own MFMAs consume straight into registers, so there is no LDS staging
+// and no barrier in the contraction loop; waves run independently and the
+// operands they share (F^ rows between the two waves of a tile row, input
+// positions between the two of a tile column, and the im2col duplication of
+// the input) are served by the L1 and L2 caches.
+//
+// Tile: 4 waves (2 x 2), wave tile 16BM x 16BN, workgroup tile 32BM x 32BN.
+// Contraction in groups of 16 rows; lane group q = lane/16 takes rows
+// 4q .. 4q+3 of a group, one per MFMA, so that:
+//   * F^ value (filter m, row k0 + 4q + kk): byte (k0 + kk)*4kn [wave-uniform,
+//     the scalar offset] + (4q kn + m)*4 [per lane, fixed];
+//   * im2col value (row k0 + 4q + kk, position n): byte colpos(n) [per lane,
+//     fixed] + rowoff(k0 + 4q + kk) [per lane group], where rowoff(r) =
+//     4 (y + hi x + hi wi c) comes from a table of all rows built in LDS when
+//     the workgroup starts (one ds_read_b128 gives a lane its four rows of a
+//     group).  Without padding every tap of a valid position is inside the
+//     input, so no element needs a check.
+// Two register sets pipeline the groups: the next group's loads are issued
+// before the current group's MFMAs.
+template <int BM, int BN>
+__global__ __launch_bounds__(kThreads) void convgemm_direct_kernel(Geometry g, const float* __restrict__ F,
+                                                                   const float* __restrict__ I,
+                                                                   float* __restrict__ O, int accumulate,
+                                                                   int vec, int mtiles, int ntiles, int kpad)
+{
+    constexpr int WM = 16 * BM, WN = 16 * BN;
+    constexpr int MT = 2 * WM, NT = 2 * WN;
+    extern __shared__ int rowoff[];                // kpad entries; rows past K read offset 0
+    for (int r = threadIdx.x; r < kpad; r += kThreads) {
+        int v = 0;
+        if (r < g.K) {
+            const int c = r / g.khw, rem = r - c * g.khw, x = rem / g.kh, y = rem - x * g.kh;
+            v = (y + g.hi * x + g.hiwi * c) * 4;
+        }
+        rowoff[r] = v;
+    }
+    __syncthreads();
+
+    // XCD-aware tile order, as in the LDS-staged kernel
+    const int T = mtiles * ntiles;
+    const int T8 = T & ~7;
+    const int bid = blockIdx.x;
+    const int t = bid < T8 ? (bid & 7) * (T8 >> 3) + (bid >> 3) : bid;
+    const int m0 = (t % mtiles) * MT;
+    const int n0 = (t / mtiles) * NT;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = wave & 1, wn = wave >> 1;
+    const int q = lane >> 4, l16 = lane & 15;
+    const __amdgpu_buffer_rsrc_t irs = tensor_rsrc(I, g.ibytes);
+    const __amdgpu_buffer_rsrc_t frs = tensor_rsrc(F, g.fbytes);
+
+    // per-lane fixed offsets; filters and positions past the edge are clamped
+    // (they only feed outputs that are never stored)
+    int am[BM];
+    uint32_t aoff[BM], coff[BN];
 #pragma unroll
     for (int i = 0; i < BM; ++i) {
-        const int m = m0 + wm * WM + i * 16 + 4 * (lane >> 4);
+        am[i] = min(m0 + wm * WM + 16 * i + l16, g.M - 1);
+        aoff[i] = (uint32_t)(4 * q * g.M + am[i]) * 4u;
+    }
 #pragma unroll
-        for (int j = 0; j < BN; ++j) {
-            const int n = n0 + wn * WN + j * 16 + (lane & 15);
-            if (n >= g.N || m >= g.M) continue;
-            float* o = O + (int64_t)n * g.M + m;
-            f4 v = acc[i][j];
-            if (vec) {
-                if (accumulate) v += *reinterpret_cast<const f4*>(o);
-                *reinterpret_cast<f4*>(o) = v;
-            } else {
+    for (int j = 0; j < BN; ++j) {
+        const int n = min(n0 + wn * WN + 16 * j + l16, g.N - 1);
+        const int nb = n / g.hw, rem = n - nb * g.hw, ow = rem / g.ho, oh = rem - ow * g.ho;
+        coff[j] = (uint32_t)(nb * g.sample + oh * g.s + g.hi * (ow * g.s)) * 4u;
+    }
+
+    f4 acc[BM][BN];
 #pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    if (m + q < g.M) o[q] = accumulate ? o[q] + v[q] : v[q];
+    for (int i = 0; i < BM; ++i)
+#pragma unroll
+        for (int j = 0; j < BN; ++j) acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    float a[2][BM][4], b[2][BN][4];
+    auto load = [&](int grp, int set) {
+        const int k0 = grp * 16;
+        const int4 r4 = *reinterpret_cast<const int4*>(&rowoff[k0 + 4 * q]);
+        const uint32_t rr[4] = {(uint32_t)r4.x, (uint32_t)r4.y, (uint32_t)r4.z, (uint32_t)r4.w};
+        if (k0 + 16 <= g.K) {
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+#pragma unroll
+                for (int i = 0; i < BM; ++i) a[set][i][kk] = buffer_load(frs, aoff[i], (uint32_t)(k0 + kk) * g.M * 4u);
+#pragma unroll
+                for (int j = 0; j < BN; ++j) b[set][j][kk] = buffer_load(irs, coff[j] + rr[kk], 0u);
+            }
+        } else {
+            // last, partial group: F^ rows past K are loaded clamped and zeroed
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+                const int row = k0 + 4 * q + kk;
+                const bool ok = row < g.K;
+                const int rc = ok ? row : g.K - 1;
+#pragma unroll
+                for (int i = 0; i < BM; ++i) {
+                    const float v = buffer_load(frs, (uint32_t)(rc * g.M + am[i]) * 4u, 0u);
+                    a[set][i][kk] = ok ? v : 0.0f;
+                }
+#pragma unroll
+                for (int j = 0; j < BN; ++j) b[set][j][kk] = buffer_load(irs, coff[j] + rr[kk], 0u);
             }
         }
+    };
+    auto compute = [&](int set) {
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+            for (int i = 0; i < BM; ++i)
+#pragma unroll
+                for (int j = 0; j < BN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[set][i][kk], b[set][j][kk], acc[i][j], 0, 0, 0);
+    };
+
+    const int ngroups = (g.K + 15) / 16;
+    load(0, 0);
+    int grp = 0;
+    for (; grp + 2 <= ngroups; grp += 2) {
+        load(grp + 1, 1);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(0);
+        __builtin_amdgcn_sched_barrier(0);
+        if (grp + 2 < ngroups) load(grp + 2, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(1);
+        __builtin_amdgcn_sched_barrier(0);
     }
+    if (grp < ngroups) compute(0);
+
+#pragma unroll
+    for (int i = 0; i < BM; ++i)
+#pragma unroll
+        for (int j = 0; j < BN; ++j)
+            store_block(O, g, m0 + wm * WM + 16 * i + 4 * q, n0 + wn * WN + 16 * j + l16, acc[i][j], accumulate,
+                        vec);
 }
 
 int out_size(int h, int k, int s, int p)
@@ -333,6 +475,20 @@ hipError_t launch(const Geometry& g, const float* F, const float* I, float* O, i
     return hipGetLastError();
 }
 
+template <int BM, int BN>
+hipError_t launch_direct(const Geometry& g, const float* F, const float* I, float* O, int accumulate, int vec,
+                         hipStream_t stream)
+{
+    const int mtiles = (g.M + 32 * BM - 1) / (32 * BM);
+    const int ntiles = (g.N + 32 * BN - 1) / (32 * BN);
+    const int64_t tiles = (int64_t)mtiles * ntiles;
+    if (tiles > 0x7fffffff) return hipErrorInvalidConfiguration;
+    const int kpad = (g.K + 15) / 16 * 16;
+    hipLaunchKernelGGL((convgemm_direct_kernel<BM, BN>), dim3((unsigned)tiles), dim3(kThreads),
+                       (size_t)kpad * sizeof(int), stream, g, F, I, O, accumulate, vec, mtiles, ntiles, kpad);
+    return hipGetLastError();
+}
+
 int device_cus()
 {
     int dev = 0, cus = 0;
@@ -351,7 +507,7 @@ extern "C" int convgemm_out_size(int h, int k, int stride, int pad)
 }
 
 extern "C" int convgemm_f32(int kn, int kh, int kw, int ci, int hi, int wi, int b, int stride, int pad,
-                            const float* F, const float* I, float* O, int accumulate, int mt, int nt,
+                            const float* F, const float* I, float* O, int accumulate, int path, int mt, int nt,
                             hipStream_t stream)
 {
     using namespace convgemm;
@@ -374,10 +530,16 @@ extern "C" int convgemm_f32(int kn, int kh, int kw, int ci, int hi, int wi, int 
     if ((int64_t)hi * wi * ci * b >= ((int64_t)1 << 30)) return -7;
     if (kn >= (1 << 24) || (int64_t)kn * kh * kw * ci >= ((int64_t)1 << 30)) return -1;
     if (accumulate != 0 && accumulate != 1) return -13;
-    const bool auto_tile = mt == 0 && nt == 0;
-    if (!auto_tile && !((mt == 64 && (nt == 64 || nt == 128 || nt == 256)) || (mt == 128 && nt == 128) ||
-                        (mt == 192 && nt == 128)))
+    // path: 0 automatic, 1 LDS-staged gather, 2 register-direct (no padding,
+    // contraction up to kDirectMaxK rows: its row table lives in LDS)
+    const int64_t kk = (int64_t)kh * kw * ci;
+    if (path < 0 || path > 2 || (path == 2 && (pad != 0 || kk > kDirectMaxK)) || (path == 0 && (mt || nt)))
         return -14;
+    const bool lds_tile = (mt == 64 && (nt == 64 || nt == 128 || nt == 256)) || (mt == 128 && nt == 128) ||
+                          (mt == 192 && nt == 128);
+    const bool direct_tile = (mt == 64 || mt == 128) && (nt == 64 || nt == 128);
+    if (path == 1 && !(lds_tile || (mt == 0 && nt == 0))) return -15;
+    if (path == 2 && !(direct_tile || (mt == 0 && nt == 0))) return -15;
     if (b == 0) return CONVGEMM_OK;
     if (!F) return -10;
     if (!I) return -11;
@@ -403,8 +565,39 @@ extern "C" int convgemm_f32(int kn, int kh, int kw, int ci, int hi, int wi, int 
 
     const int vec = (kn % 4 == 0) && ((uintptr_t)O % 16 == 0);
     const int cus = device_cus();
-    Tile t = auto_tile ? choose_tile(g.M, g.N, cus) : Tile{mt, nt};
     hipError_t e;
+    // automatic: the register-direct kernel for unit-stride
+    // convolutions without padding (the im2col columns of neighbouring
+    // positions are then contiguous input runs that the caches serve well);
+    // the LDS-staged gather otherwise (measured: the direct kernel is slower
+    // at stride 4, where each load instruction spans four times the lines)
+    if (path == 0) path = (pad == 0 && stride == 1 && kk <= kDirectMaxK) ? 2 : 1;
+    if (path == 2) {
+        int dm = mt, dn = nt;
+        if (dm == 0) {
+            // measured on the AlexNet layers: 64 x 128 while that still gives
+            // four tiles per CU; 128 x 64 for filter counts divisible by 128
+            // with at least 1.5 tiles per CU; 64 x 64 otherwise
+            const int64_t t64x128 = (int64_t)((g.M + 63) / 64) * ((g.N + 127) / 128);
+            const int64_t t128x64 = (int64_t)((g.M + 127) / 128) * ((g.N + 63) / 64);
+            if (t64x128 >= 4 * (int64_t)cus)
+                dm = 64, dn = 128;
+            else if (g.M % 128 == 0 && 2 * t128x64 >= 3 * (int64_t)cus)
+                dm = 128, dn = 64;
+            else
+                dm = 64, dn = 64;
+        }
+        if (dm == 64 && dn == 64)
+            e = launch_direct<2, 2>(g, F, I, O, accumulate, vec, stream);
+        else if (dm == 64)
+            e = launch_direct<2, 4>(g, F, I, O, accumulate, vec, stream);
+        else if (dn == 64)
+            e = launch_direct<4, 2>(g, F, I, O, accumulate, vec, stream);
+        else
+            e = launch_direct<4, 4>(g, F, I, O, accumulate, vec, stream);
+        return e == hipSuccess ? CONVGEMM_OK : CONVGEMM_ERR_HIP_BASE - (int)e;
+    }
+    Tile t = (mt == 0 && nt == 0) ? choose_tile(g.M, g.N, cus) : Tile{mt, nt};
     if (t.mt == 64 && t.nt == 64)
         e = launch<64, 64>(g, F, I, O, accumulate, vec, cus, stream);
     else if (t.mt == 64 && t.nt == 128)

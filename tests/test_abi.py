@@ -210,12 +210,13 @@ def test_profile_enable_is_host_only(lib):
     assert lib.ltlt_profile_enable(-1) == -1
 
 
-# convgemm_f32(kn, kh, kw, ci, hi, wi, b, stride, pad, F, I, O, accumulate, mt, nt, stream)
-CG_OK = (8, 3, 3, 2, 9, 9, 2, 1, 1, 1, 1, 1, 0, 0, 0, NULL)
+# convgemm_f32(kn, kh, kw, ci, hi, wi, b, stride, pad, F, I, O, accumulate, path, mt, nt, stream)
+CG_OK = (8, 3, 3, 2, 9, 9, 2, 1, 1, 1, 1, 1, 0, 0, 0, 0, NULL)
 
 
 def _cg(**kw):
-    names = ["kn", "kh", "kw", "ci", "hi", "wi", "b", "s", "p", "F", "I", "O", "acc", "mt", "nt", "stream"]
+    names = ["kn", "kh", "kw", "ci", "hi", "wi", "b", "s", "p", "F", "I", "O", "acc", "path", "mt", "nt",
+             "stream"]
     args = dict(zip(names, CG_OK))
     args.update(kw)
     return tuple(args[n] for n in names)
@@ -238,8 +239,15 @@ def _cg(**kw):
     (_cg(hi=4000, wi=4000, kh=1, kw=1, ci=1, b=200), -7),  # ho wo b beyond 2^31
     (_cg(kn=2, kh=1, kw=1, ci=1 << 29, hi=1, wi=1, b=1, p=0), -1),  # filter tensor 2^30 elements
     (_cg(acc=2), -13),
-    (_cg(mt=128, nt=64), -14),
-    (_cg(mt=96, nt=128), -14),
+    (_cg(path=3), -14),
+    (_cg(path=-1), -14),
+    (_cg(path=0, mt=64, nt=64), -14),           # automatic path takes no tile
+    (_cg(path=2, p=1), -14),                    # register-direct: no padding
+    (_cg(path=2, p=0, kh=3, kw=3, ci=1821, hi=9, wi=9), -14),   # register-direct: K <= 16384
+    (_cg(path=1, mt=128, nt=64), -15),
+    (_cg(path=1, mt=96, nt=128), -15),
+    (_cg(path=2, p=0, mt=64, nt=256), -15),
+    (_cg(path=2, p=0, mt=192, nt=128), -15),
     (_cg(F=NULL), -10),
     (_cg(I=NULL), -11),
     (_cg(O=NULL), -12),

@@ -4,7 +4,9 @@ convolution oracle (direct loops of the paper's Figure 4, fp64).
 * integer-valued inputs: bit-exact (every partial sum is an integer < 2^24);
 * Gaussian / uniform inputs: within gamma_{K+1} * conv(|F|, |I|) entrywise and
   1e-5 normwise (see ``conv_util``);
-* every workgroup tile (64x64, 64x128, 64x256, 128x128, 192x128) on the same
+* both kernels: the LDS-staged gather (path 1) in every workgroup tile (64x64,
+  64x128, 64x256, 128x128, 192x128) and the register-direct one (path 2, no
+  padding) in every tile (64x64, 64x128, 128x64, 128x128), on the same
   ragged problem (filter count, contraction length and output count not
   multiples of any tile), both with few tiles (32-row contraction chunks) and
   with many (16-row chunks), with and without padding; strides 1-4, padding
@@ -29,11 +31,14 @@ from synth import conv as sc
 pytestmark = pytest.mark.gpu
 
 TILES = [(64, 64), (64, 128), (64, 256), (128, 128), (192, 128)]
+DIRECT_TILES = [(64, 64), (64, 128), (128, 64), (128, 128)]
 
 
-def run(F, I, s, p, tile=(0, 0), out=None, accumulate=False):
+def run(F, I, s, p, tile=(0, 0), out=None, accumulate=False, path=None):
     Fd, Id = dev(F), dev(I)
-    O = lt.convgemm(Fd, Id, stride=s, pad=p, tile=tile, out=out, accumulate=accumulate)
+    if path is None:
+        path = 0 if tile == (0, 0) else 1
+    O = lt.convgemm(Fd, Id, stride=s, pad=p, tile=tile, out=out, accumulate=accumulate, path=path)
     torch.cuda.synchronize()
     return O
 
@@ -93,6 +98,25 @@ def test_every_tile_many_tiles_padded_gaussian(tile):
     check_close(got, oc.conv_direct(F, I, 1, 1), bound(F, I, 1, 1, oc), f"tile {tile} padded")
 
 
+@pytest.mark.parametrize("tile", DIRECT_TILES)
+@pytest.mark.parametrize("shape", ["ragged", "long"])
+def test_direct_every_tile_integer_exact(tile, shape):
+    kn, kh, kw, ci, hi, wi, b = RAGGED if shape == "ragged" else LONG
+    F, I = int_case(kn, kh, kw, ci, hi, wi, b, 52)
+    print(f"[conv] register-direct tile {tile} integer {shape}", flush=True)
+    got = host(run(F, I, 1, 0, tile, path=2))
+    assert np.array_equal(got.astype(np.float64), oc.conv_direct(F, I, 1, 0))
+
+
+@pytest.mark.parametrize("tile", DIRECT_TILES)
+def test_direct_every_tile_gaussian_strided(tile):
+    kn, kh, kw, ci, hi, wi, b = RAGGED
+    F, I = gauss_case(kn, kh, kw, ci, hi, wi, b, 53)
+    print(f"[conv] register-direct tile {tile} gaussian stride 2", flush=True)
+    got = host(run(F, I, 2, 0, tile, path=2))
+    check_close(got, oc.conv_direct(F, I, 2, 0), bound(F, I, 2, 0, oc), f"direct tile {tile}")
+
+
 GEOMS = [
     # kn, kh, kw, ci, hi, wi, b, s, p
     (5, 3, 2, 3, 11, 9, 3, 2, 1),
@@ -103,6 +127,8 @@ GEOMS = [
     (3, 2, 2, 1, 4, 4, 1, 2, 3),        # padding wider than the filter: zero borders
     (33, 7, 7, 3, 30, 28, 2, 2, 3),
     (130, 3, 3, 17, 12, 12, 5, 1, 1),
+    (9, 4, 3, 3, 17, 14, 2, 3, 0),
+    (66, 5, 5, 6, 20, 19, 3, 2, 0),
 ]
 
 
@@ -115,6 +141,16 @@ def test_geometries_integer_exact(g):
     assert np.array_equal(got.astype(np.float64), oc.conv_direct(F, I, s, p))
 
 
+@pytest.mark.parametrize("g", [g for g in GEOMS if g[8] == 0])
+@pytest.mark.parametrize("path", [1, 2])
+def test_unpadded_geometries_both_paths_integer_exact(g, path):
+    kn, kh, kw, ci, hi, wi, b, s, p = g
+    F, I = int_case(kn, kh, kw, ci, hi, wi, b, 54)
+    print(f"[conv] geometry {g} path {path} integer", flush=True)
+    got = host(run(F, I, s, p, path=path))
+    assert np.array_equal(got.astype(np.float64), oc.conv_direct(F, I, s, p))
+
+
 @pytest.mark.parametrize("g", GEOMS)
 def test_geometries_gaussian(g):
     kn, kh, kw, ci, hi, wi, b, s, p = g
@@ -124,13 +160,14 @@ def test_geometries_gaussian(g):
     check_close(got, oc.conv_direct(F, I, s, p), bound(F, I, s, p, oc), str(g))
 
 
-def test_accumulate_adds_to_output():
+@pytest.mark.parametrize("path", [1, 2])
+def test_accumulate_adds_to_output(path):
     kn, kh, kw, ci, hi, wi, b = RAGGED
     F, I = gauss_case(kn, kh, kw, ci, hi, wi, b, 44)
     ho, wo = hi - kh + 1, wi - kw + 1
     O0 = np.asfortranarray(synth.rng_for(45).standard_normal((kn, ho, wo, b)).astype(np.float32))
     out = dev(O0)
-    got = host(run(F, I, 1, 0, out=out, accumulate=True))
+    got = host(run(F, I, 1, 0, out=out, accumulate=True, path=path))
     ref = oc.conv_direct(F, I, 1, 0) + O0.astype(np.float64)
     bnd = bound(F, I, 1, 0, oc) + U_ROUND * (np.abs(ref) + np.abs(O0))
     check_close(got, ref, bnd, "accumulate")
@@ -139,7 +176,8 @@ def test_accumulate_adds_to_output():
 U_ROUND = 2.0 ** -24
 
 
-def test_misaligned_output_uses_scalar_stores():
+@pytest.mark.parametrize("path", [1, 2])
+def test_misaligned_output_uses_scalar_stores(path):
     kn, kh, kw, ci, hi, wi, b = 8, 3, 3, 4, 10, 9, 2
     F, I = int_case(kn, kh, kw, ci, hi, wi, b, 46)
     ho, wo = hi - kh + 1, wi - kw + 1
@@ -147,7 +185,7 @@ def test_misaligned_output_uses_scalar_stores():
     flat = torch.full((n + 1,), 7.0, dtype=torch.float32, device="cuda")
     out = flat[1:].as_strided((kn, ho, wo, b), (1, kn, kn * ho, kn * ho * wo))
     assert out.data_ptr() % 16 != 0
-    got = host(run(F, I, 1, 0, out=out))
+    got = host(run(F, I, 1, 0, out=out, path=path))
     assert np.array_equal(got.astype(np.float64), oc.conv_direct(F, I, 1, 0))
     assert float(flat[0].item()) == 7.0
 
