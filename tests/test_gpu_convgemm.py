@@ -190,6 +190,29 @@ def test_misaligned_output_uses_scalar_stores(path):
     assert float(flat[0].item()) == 7.0
 
 
+@pytest.mark.parametrize("path", [1, 2])
+@pytest.mark.parametrize("kn,kh,kw,ci", [(1, 1, 1, 1), (3, 1, 1, 15), (5, 2, 2, 4), (4, 1, 1, 17),
+                                         (2, 31, 1, 1), (6, 3, 11, 1)])
+def test_short_contractions_integer_exact(path, kn, kh, kw, ci):
+    """K = 1, 15, 16, 17, 31, 33: a single partial group, exact multiples of
+    the 16-row group, and one row past it; kn = 1 (one filter)."""
+    hi, wi, b = kh + 4, kw + 3, 2
+    F, I = int_case(kn, kh, kw, ci, hi, wi, b, 55)
+    print(f"[conv] short contraction K={kh * kw * ci} kn={kn} path {path}", flush=True)
+    got = host(run(F, I, 1, 0, path=path))
+    assert np.array_equal(got.astype(np.float64), oc.conv_direct(F, I, 1, 0))
+
+
+def test_long_contraction_falls_back_to_lds_staging():
+    """K = 3*3*2000 = 18000 rows exceeds the register-direct kernel's row table:
+    the automatic choice takes the LDS-staged kernel."""
+    kn, kh, kw, ci, hi, wi, b = 8, 3, 3, 2000, 5, 6, 2
+    F, I = int_case(kn, kh, kw, ci, hi, wi, b, 56, -2, 2)
+    print("[conv] long contraction K=18000", flush=True)
+    got = host(run(F, I, 1, 0))
+    assert np.array_equal(got.astype(np.float64), oc.conv_direct(F, I, 1, 0))
+
+
 def test_empty_batch():
     F = dev(sc.filter_tensor(4, 3, 3, 2, 1))
     I = torch.empty(0, dtype=torch.float32, device="cuda").as_strided((6, 6, 2, 0), (1, 6, 36, 72))
