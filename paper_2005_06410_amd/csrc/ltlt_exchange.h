@@ -59,6 +59,29 @@ __device__ __forceinline__ void wave_lds_sync() { asm volatile("s_waitcnt lgkmcn
     _Pragma("unroll") for (int i = 0; i < 16; ++i) L[(G0) + i] = (on && c == (G0) + i) ? v : L[(G0) + i]; \
   }
 
+// L[c] = v where `on`, for a wave-uniform slot c < KC: a uniform jump to the
+// one slot (register indices stay static and only that slot is written),
+// instead of LTLT_SET_GROUP's selects over a whole group of 16.  Measured
+// faster in the two- and four-lane-per-row panels; with one lane per row the
+// jump table's control flow pushed the kernel past its register budget, so
+// that panel keeps the group form.
+#define LTLT_SLOT_CASE(i) \
+  case (i): L[(i)] = on ? v : L[(i)]; break;
+#define LTLT_SLOT_CASE4(i) LTLT_SLOT_CASE(i) LTLT_SLOT_CASE((i) + 1) LTLT_SLOT_CASE((i) + 2) LTLT_SLOT_CASE((i) + 3)
+#define LTLT_SLOT_CASE16(i) \
+  LTLT_SLOT_CASE4(i) LTLT_SLOT_CASE4((i) + 4) LTLT_SLOT_CASE4((i) + 8) LTLT_SLOT_CASE4((i) + 12)
+template <typename T>
+__device__ __forceinline__ void set_slot(T (&L)[KC], int c, bool on, T v) {
+  static_assert(KC == 64, "64 slots");
+  switch (c) {
+    LTLT_SLOT_CASE16(0) LTLT_SLOT_CASE16(16) LTLT_SLOT_CASE16(32) LTLT_SLOT_CASE16(48)
+    default: break;
+  }
+}
+#undef LTLT_SLOT_CASE16
+#undef LTLT_SLOT_CASE4
+#undef LTLT_SLOT_CASE
+
 // Sum of v over the S parts of a row (lanes lane ^ 16, lane ^ 32).
 template <int S, typename T>
 __device__ __forceinline__ T part_sum(T v) {

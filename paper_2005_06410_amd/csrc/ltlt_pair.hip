@@ -302,7 +302,11 @@ __global__ void __launch_bounds__(kPanelThreads, 1) pair_panel_kernel(PanelArgs 
       const int c = ns / S;
       const bool on = next2 && part == ns % S;
       const T v = l;
-      LTLT_SET_GROUP(0) LTLT_SET_GROUP(16) LTLT_SET_GROUP(32) LTLT_SET_GROUP(48)
+      if constexpr (S >= 2) {
+        set_slot<T>(L, c, on, v);
+      } else {
+        LTLT_SET_GROUP(0) LTLT_SET_GROUP(16) LTLT_SET_GROUP(32) LTLT_SET_GROUP(48)
+      }
     }
 #pragma unroll
     for (int u = 0; u < NLQ; ++u) {
@@ -351,7 +355,11 @@ __global__ void __launch_bounds__(kPanelThreads, 1) pair_panel_kernel(PanelArgs 
         const int c = (ns + 1) / S;
         const bool on = next2 && part == (ns + 1) % S;
         const T v = wv;
-        LTLT_SET_GROUP(0) LTLT_SET_GROUP(16) LTLT_SET_GROUP(32) LTLT_SET_GROUP(48)
+        if constexpr (S >= 2) {
+          set_slot<T>(L, c, on, v);
+        } else {
+          LTLT_SET_GROUP(0) LTLT_SET_GROUP(16) LTLT_SET_GROUP(32) LTLT_SET_GROUP(48)
+        }
       }
       int ro = pos - (j + 1);
       asm volatile("" : "+v"(ro));

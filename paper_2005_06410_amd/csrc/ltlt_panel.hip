@@ -201,7 +201,11 @@ __global__ void __launch_bounds__(kPanelThreads, 1) panel_kernel(PanelArgs a) {
       const bool on = next && part == t % S;
       const T v = l;
       static_assert(KC == 64, "four groups of 16 slots");
-      LTLT_SET_GROUP(0) LTLT_SET_GROUP(16) LTLT_SET_GROUP(32) LTLT_SET_GROUP(48)
+      if constexpr (S >= 2) {
+        set_slot<T>(L, c, on, v);
+      } else {
+        LTLT_SET_GROUP(0) LTLT_SET_GROUP(16) LTLT_SET_GROUP(32) LTLT_SET_GROUP(48)
+      }
     }
 
     // ---- g coefficients for step k+1 (t+1 terms), row broadcast layout ----
