@@ -55,7 +55,9 @@ __device__ __forceinline__ void cdiv(T xr, T xi, T yr, T yi, T& zr, T& zi) {
 }
 
 // Lr[c] = vr, Li[c] = vi where `on`, for a wave-uniform slot c (static
-// register indices: uniform branch on the group of 16, selects inside).
+// register indices: uniform branch on the group of 16, selects inside).  The
+// two- and four-lane-per-row panels use cset_slot instead: a uniform jump to
+// the one slot.
 #define LTLT_CSET_GROUP(G0)                                                         \
   if ((c >> 4) == (G0) / 16) {                                                     \
     _Pragma("unroll") for (int i = 0; i < 16; ++i) {                               \
@@ -63,6 +65,22 @@ __device__ __forceinline__ void cdiv(T xr, T xi, T yr, T yi, T& zr, T& zi) {
       Li[(G0) + i] = (on && c == (G0) + i) ? vi : Li[(G0) + i];                    \
     }                                                                              \
   }
+
+#define LTLT_CSLOT_CASE(i) \
+  case (i): Lr[(i)] = on ? vr : Lr[(i)]; Li[(i)] = on ? vi : Li[(i)]; break;
+#define LTLT_CSLOT_CASE4(i) \
+  LTLT_CSLOT_CASE(i) LTLT_CSLOT_CASE((i) + 1) LTLT_CSLOT_CASE((i) + 2) LTLT_CSLOT_CASE((i) + 3)
+template <typename T>
+__device__ __forceinline__ void cset_slot(T (&Lr)[KCC], T (&Li)[KCC], int c, bool on, T vr, T vi) {
+  static_assert(KCC == 32, "32 slots");
+  switch (c) {
+    LTLT_CSLOT_CASE4(0) LTLT_CSLOT_CASE4(4) LTLT_CSLOT_CASE4(8) LTLT_CSLOT_CASE4(12)
+    LTLT_CSLOT_CASE4(16) LTLT_CSLOT_CASE4(20) LTLT_CSLOT_CASE4(24) LTLT_CSLOT_CASE4(28)
+    default: break;
+  }
+}
+#undef LTLT_CSLOT_CASE4
+#undef LTLT_CSLOT_CASE
 
 template <typename T, int S>
 __global__ void __launch_bounds__(kPanelThreads, 1) cpanel_kernel(CPanelArgs ca) {
@@ -215,7 +233,11 @@ __global__ void __launch_bounds__(kPanelThreads, 1) cpanel_kernel(CPanelArgs ca)
       const bool on = next && part == t % S;
       const T vr = lr, vi = li;
       static_assert(KCC == 32, "two groups of 16 slots");
-      LTLT_CSET_GROUP(0) LTLT_CSET_GROUP(16)
+      if constexpr (S >= 2) {
+        cset_slot<T>(Lr, Li, c, on, vr, vi);
+      } else {
+        LTLT_CSET_GROUP(0) LTLT_CSET_GROUP(16)
+      }
     }
 
     // ---- g coefficients for step k+1, row broadcast layout:
