@@ -212,7 +212,7 @@ __global__ void __launch_bounds__(kPanelThreads, 1) cpanel_kernel(CPanelArgs ca)
       const int umax = t > 0 ? t - 1 : 0;
 #pragma unroll
       for (int q = 0; q < NLQ; ++q) {
-        const int64_t at = ro + (int64_t)min(q * kWave + lane, umax) * ldw;
+        const int64_t at = ro * bw + min(q * kWave + lane, umax);
         lrr[q] = ld_coh_t(&Gr[at]);
         lri[q] = ld_coh_t(&Gi[at]);
       }
@@ -273,8 +273,8 @@ __global__ void __launch_bounds__(kPanelThreads, 1) cpanel_kernel(CPanelArgs ca)
       int ro = pos - (j + 1);
       asm volatile("" : "+v"(ro));
       if (next && part == t % S) {
-        st_coh_t(&Gr[(int64_t)ro + (int64_t)t * ldw], lr);
-        st_coh_t(&Gi[(int64_t)ro + (int64_t)t * ldw], li);
+        st_coh_t(&Gr[(int64_t)ro * bw + t], lr);
+        st_coh_t(&Gi[(int64_t)ro * bw + t], li);
       }
     }
     if (tid == 0 && w == 0) a.ipiv[k + 1] = p;

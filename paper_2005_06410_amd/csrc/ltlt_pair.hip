@@ -213,9 +213,9 @@ __global__ void __launch_bounds__(kPanelThreads, 1) pair_panel_kernel(PanelArgs 
         lsgA = pos > qq ? T(1) : T(-1);
       }
       T lrQ[NLQ];
-      const T* growQ = G + (int64_t)(qq - (j + 1));
+      const T* growQ = G + (int64_t)(qq - (j + 1)) * bw;
 #pragma unroll
-      for (int u = 0; u < NLQ; ++u) lrQ[u] = ld_coh_t(&growQ[(int64_t)min(u * kWave + lane, uo) * ldw]);
+      for (int u = 0; u < NLQ; ++u) lrQ[u] = ld_coh_t(&growQ[min(u * kWave + lane, uo)]);
       T sA = A[(int64_t)max(qq, qk) + (int64_t)min(qq, qk) * lda];
       if (qq < qk) sA = -sA;
 #pragma unroll
@@ -266,16 +266,16 @@ __global__ void __launch_bounds__(kPanelThreads, 1) pair_panel_kernel(PanelArgs 
         lvB = A[(int64_t)max(pos, posw) + (int64_t)min(pos, posw) * lda];
         lsgB = pos > posw ? T(1) : T(-1);
       }
-      const T* growB = G + (int64_t)(posw - (j + 1));
+      const T* growB = G + (int64_t)(posw - (j + 1)) * bw;
 #pragma unroll
-      for (int u = 0; u < NLQ; ++u) lrB[u] = ld_coh_t(&growB[(int64_t)min(u * kWave + lane, umax) * ldw]);
+      for (int u = 0; u < NLQ; ++u) lrB[u] = ld_coh_t(&growB[min(u * kWave + lane, umax)]);
       if (!last) {
         sB = A[(int64_t)max(q, posw) + (int64_t)min(q, posw) * lda];
         if (q < posw) sB = -sB;
         if (ns >= 2) {
-          const T* growQ = G + (int64_t)(q - (j + 1));
-          qn0 = ld_coh_t(&growQ[(int64_t)(ns - 2) * ldw]);
-          qn1 = ld_coh_t(&growQ[(int64_t)(ns - 1) * ldw]);
+          const T* growQ = G + (int64_t)(q - (j + 1)) * bw;
+          qn0 = ld_coh_t(&growQ[ns - 2]);
+          qn1 = ld_coh_t(&growQ[ns - 1]);
         }
       }
     }
@@ -363,8 +363,8 @@ __global__ void __launch_bounds__(kPanelThreads, 1) pair_panel_kernel(PanelArgs 
       }
       int ro = pos - (j + 1);
       asm volatile("" : "+v"(ro));
-      if (next2 && part == ns % S) st_coh_t(&G[(int64_t)ro + (int64_t)ns * ldw], l);
-      if (next2 && part == (ns + 1) % S) st_coh_t(&G[(int64_t)ro + (int64_t)(ns + 1) * ldw], wv);
+      if (next2 && part == ns % S) st_coh_t(&G[(int64_t)ro * bw + ns], l);
+      if (next2 && part == (ns + 1) % S) st_coh_t(&G[(int64_t)ro * bw + ns + 1], wv);
     }
     // g of column k+2 by slot, for the next step's cA
     if (!last) {

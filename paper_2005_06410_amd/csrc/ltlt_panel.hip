@@ -16,9 +16,10 @@
 // keeps its multipliers and column value where they are.
 //
 // A copy of the multipliers also lives in global memory, indexed by the
-// block-start index, G[pos - (j+1)][u]: every lane needs the pivot row's
-// multipliers of the earlier steps, and it is the only data that crosses
-// workgroups besides the exchange records.
+// block-start index, G[pos - (j+1)][u], row by row (stride bw) so that the
+// pivot row's multipliers of the earlier steps, which every lane needs after
+// each agreement, are one contiguous run of a few cache lines; it is the only
+// data that crosses workgroups besides the exchange records.
 //
 // Column refresh.  The trailing matrix is stored as it was at block start
 // (strict lower triangle), so the current column k is the stored column of
@@ -187,10 +188,10 @@ __global__ void __launch_bounds__(kPanelThreads, 1) panel_kernel(PanelArgs a) {
     constexpr int NLQ = TOT / kWave;              // multiplier loads per lane
     T lr[NLQ];
     {
-      const T* grow = G + (int64_t)(posw - (j + 1));
+      const T* grow = G + (int64_t)(posw - (j + 1)) * bw;
       const int umax = t > 0 ? t - 1 : 0;
 #pragma unroll
-      for (int q = 0; q < NLQ; ++q) lr[q] = ld_coh_t(&grow[(int64_t)min(q * kWave + lane, umax) * ldw]);
+      for (int q = 0; q < NLQ; ++q) lr[q] = ld_coh_t(&grow[min(q * kWave + lane, umax)]);
     }
 
     // ---- multipliers of step k (registers now, G after the loads are used) ----
@@ -236,7 +237,7 @@ __global__ void __launch_bounds__(kPanelThreads, 1) panel_kernel(PanelArgs a) {
       // live across the step loop (the kernel runs at the register limit)
       int ro = pos - (j + 1);
       asm volatile("" : "+v"(ro));
-      if (next && part == t % S) st_coh_t(&G[(int64_t)ro + (int64_t)t * ldw], l);
+      if (next && part == t % S) st_coh_t(&G[(int64_t)ro * bw + t], l);
     }
     if (tid == 0 && w == 0) a.ipiv[k + 1] = p;
     wave_lds_sync();
