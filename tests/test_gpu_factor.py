@@ -203,6 +203,13 @@ def test_panel_widths(nb):
 # --------------------------------------------------------------------------
 @pytest.mark.parametrize("m,K,off,dtype", [(2, 1, 0, np.float64), (100, 5, 0, np.float64),
                                            (129, 129, 7, np.float64), (300, 33, 20, np.float64),
+                                           # fp64 halves of 128 x 128 tiles: one, two, three
+                                           # and more operand chunks (K = 8, 9, 16, 17, 25),
+                                           # an empty second half (m = 64, 130), every wave
+                                           # of a diagonal half above the diagonal (m = 193)
+                                           (64, 8, 3, np.float64), (130, 9, 5, np.float64),
+                                           (193, 16, 9, np.float64), (256, 17, 0, np.float64),
+                                           (385, 25, 12, np.float64), (700, 257, 33, np.float64),
                                            (257, 17, 11, np.float32), (128, 4, 3, np.float32)])
 def test_skew_update_parity(m, K, off, dtype):
     rng = synth.rng_for(m * 1000 + K)
