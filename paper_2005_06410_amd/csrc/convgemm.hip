@@ -30,6 +30,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "convgemm.h"
 
 namespace convgemm {
@@ -306,11 +308,29 @@ __global__ __launch_bounds__(kThreads) void convgemm_kernel(Geometry g, const fl
 //     input, so no element needs a check.
 // Two register sets pipeline the groups: the next group's loads are issued
 // before the current group's MFMAs.
+// O += v with one atomic add per element: the contraction of a tile split
+// over several workgroups (O cleared first unless accumulating).
+__device__ inline void add_block(float* __restrict__ O, const Geometry& g, int m, int n, f4 v)
+{
+    if (n >= g.N || m >= g.M) return;
+    float* o = O + (int64_t)n * g.M + m;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+        if (m + q < g.M) unsafeAtomicAdd(o + q, v[q]);
+}
+
+__global__ void zero_kernel(float* __restrict__ O, int64_t count)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += (int64_t)gridDim.x * blockDim.x)
+        O[i] = 0.0f;
+}
+
 template <int BM, int BN>
 __global__ __launch_bounds__(kThreads) void convgemm_direct_kernel(Geometry g, const float* __restrict__ F,
                                                                    const float* __restrict__ I,
                                                                    float* __restrict__ O, int accumulate,
-                                                                   int vec, int mtiles, int ntiles, int kpad)
+                                                                   int vec, int mtiles, int ntiles, int kpad,
+                                                                   int kparts)
 {
     constexpr int WM = 16 * BM, WN = 16 * BN;
     constexpr int MT = 2 * WM, NT = 2 * WN;
@@ -325,10 +345,13 @@ __global__ __launch_bounds__(kThreads) void convgemm_direct_kernel(Geometry g, c
     }
     __syncthreads();
 
-    // XCD-aware tile order, as in the LDS-staged kernel
+    // XCD-aware tile order, as in the LDS-staged kernel; with kparts > 1,
+    // workgroup T * part + b takes groups [part * G / kparts, (part + 1) * G /
+    // kparts) of the contraction of tile b
     const int T = mtiles * ntiles;
     const int T8 = T & ~7;
-    const int bid = blockIdx.x;
+    const int part = blockIdx.x / T;
+    const int bid = blockIdx.x - part * T;
     const int t = bid < T8 ? (bid & 7) * (T8 >> 3) + (bid >> 3) : bid;
     const int m0 = (t % mtiles) * MT;
     const int n0 = (t / mtiles) * NT;
@@ -401,19 +424,29 @@ __global__ __launch_bounds__(kThreads) void convgemm_direct_kernel(Geometry g, c
     };
 
     const int ngroups = (g.K + 15) / 16;
-    load(0, 0);
-    int grp = 0;
-    for (; grp + 2 <= ngroups; grp += 2) {
+    const int glo = (int)((int64_t)part * ngroups / kparts), ghi = (int)((int64_t)(part + 1) * ngroups / kparts);
+    int grp = glo;
+    if (grp < ghi) load(grp, 0);
+    for (; grp + 2 <= ghi; grp += 2) {
         load(grp + 1, 1);
         __builtin_amdgcn_sched_barrier(0);
         compute(0);
         __builtin_amdgcn_sched_barrier(0);
-        if (grp + 2 < ngroups) load(grp + 2, 0);
+        if (grp + 2 < ghi) load(grp + 2, 0);
         __builtin_amdgcn_sched_barrier(0);
         compute(1);
         __builtin_amdgcn_sched_barrier(0);
     }
-    if (grp < ngroups) compute(0);
+    if (grp < ghi) compute(0);
+
+    if (kparts > 1) {
+#pragma unroll
+        for (int i = 0; i < BM; ++i)
+#pragma unroll
+            for (int j = 0; j < BN; ++j)
+                add_block(O, g, m0 + wm * WM + 16 * i + 4 * q, n0 + wn * WN + 16 * j + l16, acc[i][j]);
+        return;
+    }
 
 #pragma unroll
     for (int i = 0; i < BM; ++i)
@@ -475,17 +508,23 @@ hipError_t launch(const Geometry& g, const float* F, const float* I, float* O, i
     return hipGetLastError();
 }
 
+// kparts: workgroups sharing one tile's contraction (atomic adds into O)
 template <int BM, int BN>
 hipError_t launch_direct(const Geometry& g, const float* F, const float* I, float* O, int accumulate, int vec,
-                         hipStream_t stream)
+                         int kparts, hipStream_t stream)
 {
     const int mtiles = (g.M + 32 * BM - 1) / (32 * BM);
     const int ntiles = (g.N + 32 * BN - 1) / (32 * BN);
     const int64_t tiles = (int64_t)mtiles * ntiles;
-    if (tiles > 0x7fffffff) return hipErrorInvalidConfiguration;
+    if (tiles * kparts > 0x7fffffff) return hipErrorInvalidConfiguration;
     const int kpad = (g.K + 15) / 16 * 16;
-    hipLaunchKernelGGL((convgemm_direct_kernel<BM, BN>), dim3((unsigned)tiles), dim3(kThreads),
-                       (size_t)kpad * sizeof(int), stream, g, F, I, O, accumulate, vec, mtiles, ntiles, kpad);
+    if (kparts > 1 && !accumulate) {
+        const int64_t count = (int64_t)g.M * g.N;
+        const int64_t blocks = std::min<int64_t>((count + 255) / 256, 4096);
+        hipLaunchKernelGGL(zero_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, O, count);
+    }
+    hipLaunchKernelGGL((convgemm_direct_kernel<BM, BN>), dim3((unsigned)(tiles * kparts)), dim3(kThreads),
+                       (size_t)kpad * sizeof(int), stream, g, F, I, O, accumulate, vec, mtiles, ntiles, kpad, kparts);
     return hipGetLastError();
 }
 
@@ -587,14 +626,25 @@ extern "C" int convgemm_f32(int kn, int kh, int kw, int ci, int hi, int wi, int 
             else
                 dm = 64, dn = 64;
         }
+        // grids short even with the smallest tile, and long contractions: the
+        // contraction of each tile is split over several workgroups (atomic
+        // adds into O) so that every CU holds about three, each part keeping
+        // at least 64 groups of 16 (measured on AlexNet layer 8, 608 tiles:
+        // 0.227 -> 0.209 ms; layer 7's 456 larger tiles were slower split)
+        int kparts = 1;
+        if (mt == 0 && dm == 64 && dn == 64) {
+            const int64_t tl = (int64_t)((g.M + 63) / 64) * ((g.N + 63) / 64);
+            const int ngroups = (g.K + 15) / 16;
+            while (kparts < 4 && tl * kparts < 3 * (int64_t)cus && ngroups / (2 * kparts) >= 64) kparts *= 2;
+        }
         if (dm == 64 && dn == 64)
-            e = launch_direct<2, 2>(g, F, I, O, accumulate, vec, stream);
+            e = launch_direct<2, 2>(g, F, I, O, accumulate, vec, kparts, stream);
         else if (dm == 64)
-            e = launch_direct<2, 4>(g, F, I, O, accumulate, vec, stream);
+            e = launch_direct<2, 4>(g, F, I, O, accumulate, vec, kparts, stream);
         else if (dn == 64)
-            e = launch_direct<4, 2>(g, F, I, O, accumulate, vec, stream);
+            e = launch_direct<4, 2>(g, F, I, O, accumulate, vec, kparts, stream);
         else
-            e = launch_direct<4, 4>(g, F, I, O, accumulate, vec, stream);
+            e = launch_direct<4, 4>(g, F, I, O, accumulate, vec, kparts, stream);
         return e == hipSuccess ? CONVGEMM_OK : CONVGEMM_ERR_HIP_BASE - (int)e;
     }
     Tile t = (mt == 0 && nt == 0) ? choose_tile(g.M, g.N, cus) : Tile{mt, nt};

@@ -12,6 +12,9 @@ convolution oracle (direct loops of the paper's Figure 4, fp64).
   with many (16-row chunks), with and without padding; strides 1-4, padding
   0-3, non-square inputs and filters, 1x1 filters, a single output position, an empty batch, kn not a
   multiple of 4 and a misaligned output (scalar epilogue), accumulate mode;
+* short grids with long contractions, whose tiles' contractions the
+  automatic choice splits over several workgroups (atomic adds), exact and
+  accumulating;
 * the AlexNet layers of the paper's Table 2 at b = 2 in full, and at the
   benchmarked b = 80 on sampled outputs (each computed one by one by the
   oracle) plus bit-exact integer runs sampled the same way.
@@ -201,6 +204,38 @@ def test_short_contractions_integer_exact(path, kn, kh, kw, ci):
     print(f"[conv] short contraction K={kh * kw * ci} kn={kn} path {path}", flush=True)
     got = host(run(F, I, 1, 0, path=path))
     assert np.array_equal(got.astype(np.float64), oc.conv_direct(F, I, 1, 0))
+
+
+# Short grid, long contraction: the automatic register-direct choice (64 x 64
+# tiles, fewer than three per CU) splits each tile's contraction over two or
+# four workgroups that add into O atomically (O cleared first unless
+# accumulating).  K = 3*3*300 = 2700 (169 groups of 16: two parts), and
+# 3*3*600 = 5400 (338 groups: four parts); kn = 70 is not a multiple of 4.
+SPLITS = [(70, 3, 3, 300, 9, 8, 2), (36, 3, 3, 600, 7, 9, 3)]
+
+
+@pytest.mark.parametrize("g", SPLITS)
+def test_split_contraction_integer_exact(g):
+    kn, kh, kw, ci, hi, wi, b = g
+    F, I = int_case(kn, kh, kw, ci, hi, wi, b, 57, -2, 2)
+    ho, wo = hi - kh + 1, wi - kw + 1
+    print(f"[conv] split contraction K={kh * kw * ci} kn={kn} N={ho * wo * b}", flush=True)
+    # a stale output must not leak into the result
+    out = dev(np.asfortranarray(np.full((kn, ho, wo, b), 9.0, dtype=np.float32)))
+    got = host(run(F, I, 1, 0, out=out))
+    assert np.array_equal(got.astype(np.float64), oc.conv_direct(F, I, 1, 0))
+    # accumulate: O += conv(F, I), exact for integers
+    O0 = sc.int_tensor((kn, ho, wo, b), 58, -5, 5, index=7)
+    got = host(run(F, I, 1, 0, out=dev(O0), accumulate=True))
+    assert np.array_equal(got.astype(np.float64), oc.conv_direct(F, I, 1, 0) + O0.astype(np.float64))
+
+
+@pytest.mark.parametrize("g", SPLITS)
+def test_split_contraction_gaussian(g):
+    kn, kh, kw, ci, hi, wi, b = g
+    F, I = gauss_case(kn, kh, kw, ci, hi, wi, b, 59)
+    got = host(run(F, I, 1, 0))
+    check_close(got, oc.conv_direct(F, I, 1, 0), bound(F, I, 1, 0, oc), f"split {g}")
 
 
 def test_long_contraction_falls_back_to_lds_staging():
