@@ -32,7 +32,10 @@
  * single precision), products and sums on the fp32 matrix cores; the order of
  * the sums is unspecified, so results agree with an exact evaluation within
  * the usual fp32 bound |error| <= gamma_K * sum |F| |I| (K = kh kw ci), and are
- * exact whenever every partial sum is an integer below 2^24.  O may not
+ * exact whenever every partial sum is an integer below 2^24.  For short
+ * grids with long contractions the automatic choice splits a tile's
+ * contraction over several workgroups that add into O atomically, so the
+ * last bits of such a call may differ from one run to the next.  O may not
  * overlap F or I.
  */
 #ifndef CONVGEMM_H
