@@ -335,7 +335,13 @@ __global__ __launch_bounds__(kThreads) void convgemm_direct_kernel(Geometry g, c
     constexpr int WM = 16 * BM, WN = 16 * BN;
     constexpr int MT = 2 * WM, NT = 2 * WN;
     extern __shared__ int rowoff[];                // kpad entries; rows past K read offset 0
-    for (int r = threadIdx.x; r < kpad; r += kThreads) {
+    // workgroup T * part + b takes groups [part * G / kparts, (part + 1) * G /
+    // kparts) of the contraction of tile b; only its rows' offsets are formed
+    const int T = mtiles * ntiles;
+    const int part = blockIdx.x / T;
+    const int ngroups = (g.K + 15) / 16;
+    const int glo = (int)((int64_t)part * ngroups / kparts), ghi = (int)((int64_t)(part + 1) * ngroups / kparts);
+    for (int r = glo * 16 + threadIdx.x; r < ghi * 16; r += kThreads) {
         int v = 0;
         if (r < g.K) {
             const int c = r / g.khw, rem = r - c * g.khw, x = rem / g.kh, y = rem - x * g.kh;
@@ -345,12 +351,8 @@ __global__ __launch_bounds__(kThreads) void convgemm_direct_kernel(Geometry g, c
     }
     __syncthreads();
 
-    // XCD-aware tile order, as in the LDS-staged kernel; with kparts > 1,
-    // workgroup T * part + b takes groups [part * G / kparts, (part + 1) * G /
-    // kparts) of the contraction of tile b
-    const int T = mtiles * ntiles;
+    // XCD-aware tile order, as in the LDS-staged kernel
     const int T8 = T & ~7;
-    const int part = blockIdx.x / T;
     const int bid = blockIdx.x - part * T;
     const int t = bid < T8 ? (bid & 7) * (T8 >> 3) + (bid >> 3) : bid;
     const int m0 = (t % mtiles) * MT;
@@ -423,8 +425,6 @@ __global__ __launch_bounds__(kThreads) void convgemm_direct_kernel(Geometry g, c
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[set][i][kk], b[set][j][kk], acc[i][j], 0, 0, 0);
     };
 
-    const int ngroups = (g.K + 15) / 16;
-    const int glo = (int)((int64_t)part * ngroups / kparts), ghi = (int)((int64_t)(part + 1) * ngroups / kparts);
     int grp = glo;
     if (grp < ghi) load(grp, 0);
     for (; grp + 2 <= ghi; grp += 2) {
