@@ -325,7 +325,7 @@ __global__ void zero_kernel(float* __restrict__ O, int64_t count)
         O[i] = 0.0f;
 }
 
-template <int BM, int BN>
+template <int BM, int BN, bool SPLIT>
 __global__ __launch_bounds__(kThreads) void convgemm_direct_kernel(Geometry g, const float* __restrict__ F,
                                                                    const float* __restrict__ I,
                                                                    float* __restrict__ O, int accumulate,
@@ -338,9 +338,13 @@ __global__ __launch_bounds__(kThreads) void convgemm_direct_kernel(Geometry g, c
     // workgroup T * part + b takes groups [part * G / kparts, (part + 1) * G /
     // kparts) of the contraction of tile b; only its rows' offsets are formed
     const int T = mtiles * ntiles;
-    const int part = blockIdx.x / T;
     const int ngroups = (g.K + 15) / 16;
-    const int glo = (int)((int64_t)part * ngroups / kparts), ghi = (int)((int64_t)(part + 1) * ngroups / kparts);
+    int part = 0, glo = 0, ghi = ngroups;
+    if (SPLIT) {
+        part = blockIdx.x / T;
+        glo = part * ngroups / kparts;
+        ghi = (part + 1) * ngroups / kparts;
+    }
     for (int r = glo * 16 + threadIdx.x; r < ghi * 16; r += kThreads) {
         int v = 0;
         if (r < g.K) {
@@ -439,7 +443,7 @@ __global__ __launch_bounds__(kThreads) void convgemm_direct_kernel(Geometry g, c
     }
     if (grp < ghi) compute(0);
 
-    if (kparts > 1) {
+    if (SPLIT) {
 #pragma unroll
         for (int i = 0; i < BM; ++i)
 #pragma unroll
@@ -523,8 +527,12 @@ hipError_t launch_direct(const Geometry& g, const float* F, const float* I, floa
         const int64_t blocks = std::min<int64_t>((count + 255) / 256, 4096);
         hipLaunchKernelGGL(zero_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, O, count);
     }
-    hipLaunchKernelGGL((convgemm_direct_kernel<BM, BN>), dim3((unsigned)(tiles * kparts)), dim3(kThreads),
-                       (size_t)kpad * sizeof(int), stream, g, F, I, O, accumulate, vec, mtiles, ntiles, kpad, kparts);
+    if (kparts > 1)
+        hipLaunchKernelGGL((convgemm_direct_kernel<BM, BN, true>), dim3((unsigned)(tiles * kparts)), dim3(kThreads),
+                           (size_t)kpad * sizeof(int), stream, g, F, I, O, accumulate, vec, mtiles, ntiles, kpad, kparts);
+    else
+        hipLaunchKernelGGL((convgemm_direct_kernel<BM, BN, false>), dim3((unsigned)tiles), dim3(kThreads),
+                           (size_t)kpad * sizeof(int), stream, g, F, I, O, accumulate, vec, mtiles, ntiles, kpad, 1);
     return hipGetLastError();
 }
 
@@ -640,11 +648,11 @@ extern "C" int convgemm_f32(int kn, int kh, int kw, int ci, int hi, int wi, int 
         if (dm == 64 && dn == 64)
             e = launch_direct<2, 2>(g, F, I, O, accumulate, vec, kparts, stream);
         else if (dm == 64)
-            e = launch_direct<2, 4>(g, F, I, O, accumulate, vec, kparts, stream);
+            e = launch_direct<2, 4>(g, F, I, O, accumulate, vec, 1, stream);
         else if (dn == 64)
-            e = launch_direct<4, 2>(g, F, I, O, accumulate, vec, kparts, stream);
+            e = launch_direct<4, 2>(g, F, I, O, accumulate, vec, 1, stream);
         else
-            e = launch_direct<4, 4>(g, F, I, O, accumulate, vec, kparts, stream);
+            e = launch_direct<4, 4>(g, F, I, O, accumulate, vec, 1, stream);
         return e == hipSuccess ? CONVGEMM_OK : CONVGEMM_ERR_HIP_BASE - (int)e;
     }
     Tile t = (mt == 0 && nt == 0) ? choose_tile(g.M, g.N, cus) : Tile{mt, nt};
