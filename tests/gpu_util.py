@@ -11,7 +11,13 @@ Comparison rules (the reading of "parity" used throughout the GPU tests):
   from the fp64 oracle on the same (fp32-rounded) input when that is larger:
   two fp32 computations cannot be asked to agree more closely than either
   agrees with the exact factors (that distance grows with n and passes 1e-4
-  near n = 1000 for Gaussian input).
+  near n = 1000 for Gaussian input).  Two fp32 results with different
+  rounding orders can still fall on opposite sides of the exact factors, so
+  when the pivots of both oracles and the GPU agree, a GPU result that fails
+  that bar is accepted if it is as accurate as the fp32 oracle itself: its
+  normwise distance from the fp64 oracle at most 4 max(d, n eps32), d the
+  fp32 oracle's own distance (measured over 36 random fp32 / complex64
+  cases: the GPU's distance is 0.2-1.7 times the oracle's, median 0.8-1.0).
 * log|Pf|: |diff| <= 1e-9 |ref| (fp64); sign equal.
 * residual ||P X P^T - L T L^T||_F / (n eps ||X||_F) <= 10.
 * complex128 / complex64 factors follow the same rules with complex
@@ -85,6 +91,7 @@ def compare_factors(X: np.ndarray, packed_gpu: np.ndarray, ipiv_gpu, dtype, ref=
     if ref is None:
         ref = oracle.ltlt(Xd)
     packed_ref, ipiv_ref = ref
+    exact = None                                   # fp64 factors and the fp32 oracle's distances to them
     if np.dtype(dtype) in (np.float32, np.complex64) and n >= 3:
         p64, i64 = oracle.ltlt(Xd.astype(W))
         if np.array_equal(i64, ipiv_ref):
@@ -94,6 +101,8 @@ def compare_factors(X: np.ndarray, packed_gpu: np.ndarray, ipiv_gpu, dtype, ref=
             d_a = np.abs(packed_ref[sub].astype(W) - p64[sub]).max() / np.abs(p64[sub]).max()
             tol = max(tol, 2.0 * d_l)
             tol_a = max(tol_a, 2.0 * d_a)
+            ne = n * float(np.finfo(dtype).eps)
+            exact = (p64, 4.0 * max(d_l, ne), 4.0 * max(d_a, ne))
     ipiv_gpu = np.asarray(ipiv_gpu)
     ks = first_mismatch(ipiv_gpu, ipiv_ref)
     info = {"first_pivot_mismatch": ks}
@@ -120,13 +129,26 @@ def compare_factors(X: np.ndarray, packed_gpu: np.ndarray, ipiv_gpu, dtype, ref=
         a_gpu = g[sub]
         ea = np.abs(a_gpu - a_ref).max() / max(np.abs(a_ref).max(), np.finfo(float).tiny)
         info["alpha_err"] = float(ea)
-        assert ea <= tol_a, f"alpha normwise error {ea:.3e} > {tol_a}"
+        # same accuracy as the fp32 oracle (see the module notes), when all pivots agree
+        use_exact = exact is not None and ks >= n
+        if ea > tol_a and use_exact:
+            e64 = np.abs(a_gpu - exact[0][:, :ncols][sub]).max() / np.abs(exact[0][:, :ncols][sub]).max()
+            info["alpha_err_exact"] = float(e64)
+            assert e64 <= exact[2], f"alpha normwise error {ea:.3e} > {tol_a}, and {e64:.3e} > {exact[2]:.3e} from fp64"
+        else:
+            assert ea <= tol_a, f"alpha normwise error {ea:.3e} > {tol_a}"
         if lmask.any():
             l_ref = cols_ref[lmask]
             l_gpu = g[lmask]
             el = np.abs(l_gpu - l_ref).max() / max(np.abs(l_ref).max(), np.finfo(float).tiny)
             info["L_err"] = float(el)
-            assert el <= tol, f"L normwise error {el:.3e} > {tol}"
+            if el > tol and use_exact:
+                l64 = exact[0][:, :ncols][lmask]
+                e64 = np.abs(l_gpu - l64).max() / max(np.abs(l64).max(), np.finfo(float).tiny)
+                info["L_err_exact"] = float(e64)
+                assert e64 <= exact[1], f"L normwise error {el:.3e} > {tol}, and {e64:.3e} > {exact[1]:.3e} from fp64"
+            else:
+                assert el <= tol, f"L normwise error {el:.3e} > {tol}"
     if ks >= n and n >= 2:
         e_last = abs(complex(packed_gpu[n - 1, n - 2]) - complex(packed_ref[n - 1, n - 2]))
         scale = max(np.abs(np.diag(packed_ref.astype(W), -1)).max(), np.finfo(float).tiny)
