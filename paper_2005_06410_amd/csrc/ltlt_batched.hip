@@ -2,20 +2,31 @@
 // four matrices per 256-thread workgroup, with no workgroup barrier.
 //
 // Lane l holds row l+1 of its matrix (positions 1..n-1; row 0 is never
-// eliminated, L(:,0) = e_0) and keeps that row's multipliers in registers,
-// L[u] = multiplier of step u.  As in the blocked panel, rows never move: an
-// exchange of positions k+1 and p swaps the logical positions of two lanes.
-// The matrix itself is never updated: the original strict lower triangle
-// stays in LDS (packed by column) and column k is refreshed as
-//   cv[i] = S(pos[i], pos[k]) + sum_{u<k} g_u L_u[i],
-//   g_u = alpha_{u+1} Lrow[u+1] [u <= k-2] - alpha_u Lrow[u-1] [u >= 1],
-// Lrow = the multipliers of the row now at position k (Lrow[k-1] = 1), the
-// Lx Tx Lx^T form of the accumulated skew rank-2 updates.  g reaches the
-// FMAs through DPP row broadcasts (row-broadcast layout, 4 registers).
-// Per step: refresh, wave first-maximum, logical exchange, multipliers, the
-// pivot row's multipliers staged through LDS, g for the next step.  Global
-// traffic is one read and one write of each strict lower triangle, plus
-// ipiv and the Pfaffian, which is what bounds this path (HBM).
+// eliminated, L(:,0) = e_0) and keeps that row's multipliers in registers.
+// As in the blocked panel, rows never move: an exchange of positions k+1 and
+// p swaps the logical positions of two lanes.  The skew matrix S stays in LDS
+// as its strict lower triangle (packed by column, indexed by original row),
+// and the column steps run in blocks of 16:
+//  * inside a block starting at step k0, column k is refreshed from S and the
+//    block's own steps only,
+//      cv[i] = S(pos[i], pos[k]) + sum_{k0<=u<k} g_u Lb_u[i],
+//      g_u = alpha_{u+1} Lrow[u+1] [u <= k-2] - alpha_u Lrow[u-1] [u >= k0+1],
+//    Lrow = the in-block multipliers of the row now at position k
+//    (Lrow[k-1] = 1), the Lx Tx Lx^T form of the block's skew rank-2
+//    updates; g reaches the FMAs through DPP row broadcasts, and only the
+//    pivot row's in-block multipliers (at most 15) are staged through LDS;
+//  * at the end of a block, the next column (the carry) is refreshed the same
+//    way, and the block's update S += Lx Tx Lx^T, Lx = [block multipliers,
+//    carry], Tx skew tridiagonal (Tx[u,u+1] = alpha_{k0+u+1}, Tx[15,16] = 1),
+//    is applied to the pairs of rows still to be eliminated: each lane forms
+//    its row of Bt = Lx Tx^T, the rows of 16 lanes at a time are spread over
+//    the wave with ds_bpermute, and lane a adds sum_u Lx(a,u) Bt(b,u) to
+//    S(a,b) for every b < a (17 DPP-broadcast FMAs per entry).
+// This is the right-looking skew rank-2k update of the method applied every
+// 16 steps inside the wave, with the left-looking refresh confined to the
+// block, so a step's refresh, staging and g formation stay short.
+// Global traffic is one read and one write of each strict lower triangle,
+// plus ipiv and the Pfaffian, which is what bounds this path (HBM).
 
 #include "ltlt_device.h"
 #include "ltlt_internal.h"
@@ -24,12 +35,124 @@ namespace ltlt {
 
 constexpr int kBN = 64;                          // largest order handled
 constexpr int kBSlots = 64;                      // multiplier slots per lane (steps 0..61)
+constexpr int kBBlk = 16;                        // column steps per block
 constexpr int kBPack = kBN * (kBN - 1) / 2;      // packed strict lower triangle
-constexpr int kBWaveLds = kBPack + (kBSlots + 1) + (kBSlots + 2) + kBN;   // + alpha history + pivot row + ipiv (kBN ints fit in kBN elements)
+constexpr int kBAlpha = kBSlots + 2;             // alpha history (even length keeps the next array 16-byte aligned)
+constexpr int kBRow = kBBlk + 2;                 // pivot row's in-block multipliers and its unit
+constexpr int kBWaveLds = kBPack + kBAlpha + kBRow + kBN;   // + ipiv (kBN ints fit in kBN elements)
 constexpr int kBWaves = 4;                       // matrices per workgroup
 
 // Offset of X(i, c), i > c, in the column-packed strict lower triangle.
 __device__ __forceinline__ int pack_idx(int n, int i, int c) { return c * (2 * n - c - 1) / 2 + (i - c - 1); }
+
+// One value from lane addr/4 (ds_bpermute: a cross-lane read, no LDS storage).
+__device__ __forceinline__ double bperm(int addr, double v) {
+  const int lo = __builtin_amdgcn_ds_bpermute(addr, __double2loint(v));
+  const int hi = __builtin_amdgcn_ds_bpermute(addr, __double2hiint(v));
+  return __hiloint2double(hi, lo);
+}
+__device__ __forceinline__ float bperm(int addr, float v) {
+  return __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(v)));
+}
+
+// In-block refresh, eight slots at a time: acc[c % 4] += g(lane (lane & ~15) + c) * Lb[c]
+// for c = 8H .. 8H+7, v_fmac with a DPP row broadcast.  Each asm block starts
+// with the two wait states a DPP read needs after a VALU write of its source.
+#define LTLT_BF(OP, A, C, X) OP " %" #A ", %4, %" #X " row_newbcast:" #C " row_mask:0xf bank_mask:0xf\n"
+#define LTLT_REFRESH8(OP, C0, C1, C2, C3, C4, C5, C6, C7, B)                                                  \
+  asm volatile("s_nop 1\n" LTLT_BF(OP, 0, C0, 5) LTLT_BF(OP, 1, C1, 6) LTLT_BF(OP, 2, C2, 7)                 \
+                   LTLT_BF(OP, 3, C3, 8) LTLT_BF(OP, 0, C4, 9) LTLT_BF(OP, 1, C5, 10) LTLT_BF(OP, 2, C6, 11) \
+                       LTLT_BF(OP, 3, C7, 12)                                                                 \
+               : "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3])                                      \
+               : "v"(g), "v"(Lb[B + 0]), "v"(Lb[B + 1]), "v"(Lb[B + 2]), "v"(Lb[B + 3]), "v"(Lb[B + 4]),     \
+                 "v"(Lb[B + 5]), "v"(Lb[B + 6]), "v"(Lb[B + 7]))
+#define LTLT_REFRESH_FNS(TY, OP)                                                                              \
+  template <int H>                                                                                            \
+  __device__ __forceinline__ void refresh8(TY (&acc)[4], TY g, const TY (&Lb)[kBBlk]);                        \
+  template <>                                                                                                 \
+  __device__ __forceinline__ void refresh8<0>(TY (&acc)[4], TY g, const TY (&Lb)[kBBlk]) {                    \
+    LTLT_REFRESH8(OP, 0, 1, 2, 3, 4, 5, 6, 7, 0);                                                             \
+  }                                                                                                           \
+  template <>                                                                                                 \
+  __device__ __forceinline__ void refresh8<1>(TY (&acc)[4], TY g, const TY (&Lb)[kBBlk]) {                    \
+    LTLT_REFRESH8(OP, 8, 9, 10, 11, 12, 13, 14, 15, 8);                                                       \
+  }
+LTLT_REFRESH_FNS(double, "v_fmac_f64_dpp")
+LTLT_REFRESH_FNS(float, "v_fmac_f32_dpp")
+#undef LTLT_REFRESH_FNS
+#undef LTLT_REFRESH8
+#undef LTLT_BF
+
+// Block update of four columns b = 16q + C0..C0+3 (lanes of one 16-lane row):
+// a[j] += sum_u R_u(lane C0+j of each row) * X_u, u = U0..U0+8, where R_u holds
+// row 16q + (lane & 15) of Bt and X the lane's own row of Lx.
+#define LTLT_BU1(OP, C0, C1, C2, C3, R, X)                                     \
+  OP " %0, %" #R ", %" #X " row_newbcast:" #C0 " row_mask:0xf bank_mask:0xf\n" \
+  OP " %1, %" #R ", %" #X " row_newbcast:" #C1 " row_mask:0xf bank_mask:0xf\n" \
+  OP " %2, %" #R ", %" #X " row_newbcast:" #C2 " row_mask:0xf bank_mask:0xf\n" \
+  OP " %3, %" #R ", %" #X " row_newbcast:" #C3 " row_mask:0xf bank_mask:0xf\n"
+#define LTLT_BU9(OP, C0, C1, C2, C3, U0)                                                                         \
+  asm volatile("s_nop 1\n" LTLT_BU1(OP, C0, C1, C2, C3, 4, 13) LTLT_BU1(OP, C0, C1, C2, C3, 5, 14)              \
+                   LTLT_BU1(OP, C0, C1, C2, C3, 6, 15) LTLT_BU1(OP, C0, C1, C2, C3, 7, 16)                       \
+                       LTLT_BU1(OP, C0, C1, C2, C3, 8, 17) LTLT_BU1(OP, C0, C1, C2, C3, 9, 18)                   \
+                           LTLT_BU1(OP, C0, C1, C2, C3, 10, 19) LTLT_BU1(OP, C0, C1, C2, C3, 11, 20)             \
+                               LTLT_BU1(OP, C0, C1, C2, C3, 12, 21)                                              \
+               : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3])                                                  \
+               : "v"(R[U0 + 0]), "v"(R[U0 + 1]), "v"(R[U0 + 2]), "v"(R[U0 + 3]), "v"(R[U0 + 4]),                 \
+                 "v"(R[U0 + 5]), "v"(R[U0 + 6]), "v"(R[U0 + 7]), "v"(R[U0 + 8]), "v"(X[U0 + 0]),                 \
+                 "v"(X[U0 + 1]), "v"(X[U0 + 2]), "v"(X[U0 + 3]), "v"(X[U0 + 4]), "v"(X[U0 + 5]),                 \
+                 "v"(X[U0 + 6]), "v"(X[U0 + 7]), "v"(X[U0 + 8]))
+#define LTLT_UPD_FNS(TY, OP)                                                                              \
+  template <int G>                                                                                        \
+  __device__ __forceinline__ void upd4(TY (&a)[4], const TY (&R)[18], const TY (&X)[18]);                 \
+  template <>                                                                                             \
+  __device__ __forceinline__ void upd4<0>(TY (&a)[4], const TY (&R)[18], const TY (&X)[18]) {            \
+    LTLT_BU9(OP, 0, 1, 2, 3, 0);                                                                          \
+    LTLT_BU9(OP, 0, 1, 2, 3, 9);                                                                          \
+  }                                                                                                       \
+  template <>                                                                                             \
+  __device__ __forceinline__ void upd4<1>(TY (&a)[4], const TY (&R)[18], const TY (&X)[18]) {            \
+    LTLT_BU9(OP, 4, 5, 6, 7, 0);                                                                          \
+    LTLT_BU9(OP, 4, 5, 6, 7, 9);                                                                          \
+  }                                                                                                       \
+  template <>                                                                                             \
+  __device__ __forceinline__ void upd4<2>(TY (&a)[4], const TY (&R)[18], const TY (&X)[18]) {            \
+    LTLT_BU9(OP, 8, 9, 10, 11, 0);                                                                        \
+    LTLT_BU9(OP, 8, 9, 10, 11, 9);                                                                        \
+  }                                                                                                       \
+  template <>                                                                                             \
+  __device__ __forceinline__ void upd4<3>(TY (&a)[4], const TY (&R)[18], const TY (&X)[18]) {            \
+    LTLT_BU9(OP, 12, 13, 14, 15, 0);                                                                      \
+    LTLT_BU9(OP, 12, 13, 14, 15, 9);                                                                      \
+  }
+LTLT_UPD_FNS(double, "v_fmac_f64_dpp")
+LTLT_UPD_FNS(float, "v_fmac_f32_dpp")
+#undef LTLT_UPD_FNS
+#undef LTLT_BU9
+#undef LTLT_BU1
+
+// Columns b = 16q + 4G .. 16q + 4G + 3 of the block update (see upd4):
+// entries S(pos, b+1) of this lane's row for b+1 < pos, both rows trailing.
+template <int G, typename T>
+__device__ __forceinline__ void update_group(T* orig, int n, int lane, int pos, bool ta, unsigned qm, int q,
+                                             const T (&R)[18], const T (&X)[18]) {
+  if (((qm >> (4 * G)) & 0xFu) == 0) return;     // none of the four rows is still trailing
+  T a[4];
+  int idx[4];
+  bool ok[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int c = 4 * G + j;
+    const int bl = 16 * q + c;                   // lane of row b+1
+    ok[j] = ta && lane > bl && ((qm >> c) & 1u);
+    idx[j] = ok[j] ? pack_idx(n, pos, bl + 1) : 0;
+    a[j] = orig[idx[j]];
+  }
+  upd4<G>(a, R, X);
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    if (ok[j]) orig[idx[j]] = a[j];
+}
 
 template <typename T>
 __global__ void __launch_bounds__(256, 2) batched_kernel(int n, int batch, T* Aall, int64_t lda, int64_t strideA,
@@ -44,13 +167,13 @@ __global__ void __launch_bounds__(256, 2) batched_kernel(int n, int batch, T* Aa
   int* ipiv = ipiv_all + b * strideIpiv;
   T* orig = reinterpret_cast<T*>(smem) + (size_t)wave * kBWaveLds;
   T* my_alpha = orig + kBPack;
-  T* my_lrowp = my_alpha + (kBSlots + 1);        // my_lrowp[u + 1] = Lrow[u]
-  int* my_piv = reinterpret_cast<int*>(my_lrowp + (kBSlots + 2));   // ipiv, written out at the end
+  T* my_lrow = my_alpha + kBAlpha;                 // my_lrow[u] = Lrow[k0 + u]
+  int* my_piv = reinterpret_cast<int*>(my_lrow + kBRow);   // ipiv, written out at the end
 
-  // original strict lower triangle into LDS.  Column c holds n-1-c < 64
-  // entries, one per lane (coalesced); the loads of 16 columns are issued
-  // before any of them is written, so a matrix costs four memory round trips
-  // instead of one per column.
+  // strict lower triangle into LDS.  Column c holds n-1-c < 64 entries, one
+  // per lane (coalesced); the loads of 16 columns are issued before any of
+  // them is written, so a matrix costs four memory round trips instead of one
+  // per column.
   constexpr int kBFill = 16;
   for (int c0 = 0; c0 + 1 < n; c0 += kBFill) {
     T v[kBFill];
@@ -65,114 +188,148 @@ __global__ void __launch_bounds__(256, 2) batched_kernel(int n, int batch, T* Aa
       if (c + 1 < n && lane < n - 1 - c) orig[pack_idx(n, c + 1, c) + lane] = v[cc];
     }
   }
-  if (lane == 0) my_lrowp[0] = T(0);
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 
   const bool my_row = lane + 1 < n;
   const int pos = lane + 1;                        // original index of this lane's row
   int lp = pos;                                    // its current position
-  T L[kBSlots], gr[4];
+  T L[kBSlots], Lb[kBBlk];                         // finished blocks' multipliers; the current block's
 #pragma unroll
   for (int c = 0; c < kBSlots; ++c) L[c] = T(0);
 #pragma unroll
-  for (int k4 = 0; k4 < 4; ++k4) gr[k4] = T(0);
+  for (int c = 0; c < kBBlk; ++c) Lb[c] = T(0);
+  T gr = T(0);                                     // g of the current block, row-broadcast layout
   T cv = T(0);
   T lv = my_row ? orig[pack_idx(n, pos, 0)] : T(0), lsg = T(1);   // column 0: S(pos, 0)
   int npiv = 0;                                    // exchanges made (Pfaffian sign)
 
-  for (int t = 0; t + 1 < n; ++t) {               // t = k; t = n-2 only forms alpha_{n-2}
-    const int k = t;
-    const bool active = my_row && lp >= k + 1;
+  int k0 = 0;
+  bool done = n < 2;
+  while (!done) {
+#pragma unroll
+    for (int tt = 0; tt < kBBlk; ++tt) {          // step k = k0 + tt; k = n-2 only forms alpha_{n-2}
+      const int k = k0 + tt;
+      if (done || k + 1 >= n) { done = true; continue; }
+      const bool active = my_row && lp >= k + 1;
+      if (tt > 0 || k0 == 0) {                    // a block's first column is the carry of the block before
+        T acc[4] = {T(0), T(0), T(0), T(0)};
+        if (tt > 0) refresh8<0>(acc, gr, Lb);
+        if (tt > 8) refresh8<1>(acc, gr, Lb);
+        const T sum = fma(lsg, lv, (acc[0] + acc[1]) + (acc[2] + acc[3]));
+        if (active) cv = sum;
+      }
+      // pivot: first maximum of |cv| by position (NaN never a candidate)
+      double av = -1.0;
+      if (active) {
+        const double mag = (double)fabs(cv);
+        if (mag == mag) av = mag;
+      }
+      double vmax;
+      int p;
+      const int wl = wave_first_max(av, active ? lp : INT32_MAX, vmax, p);
+      T alph;
+      int posw;
+      if (wl < 0) {                                // no finite candidate: no exchange
+        p = k + 1;
+        alph = T(NAN);
+        posw = k + 1;
+      } else {
+        posw = __builtin_amdgcn_readlane(pos, wl);
+        alph = (T)vmax;
+        if (__builtin_amdgcn_readlane(cv < T(0) ? 1 : 0, wl)) alph = -alph;
+      }
+      if (lane == 0) my_alpha[k] = alph;
+      if (k + 2 == n) { done = true; continue; }   // alpha_{n-2}: last entry of T
+      if (lane == 0) my_piv[k + 1] = p;
+      if (p != k + 1) {
+        ++npiv;
+        if (my_row) {
+          if (lp == p) lp = k + 1;
+          else if (lp == k + 1) lp = p;
+        }
+      }
+      const bool next = my_row && lp >= k + 2;
+
+      // stored column of the pivot row for the next step: S(pos, posw)
+      if (next) {
+        const int hi = max(pos, posw), lo = min(pos, posw);
+        lv = orig[pack_idx(n, hi, lo)];
+        lsg = pos > posw ? T(1) : T(-1);
+      }
+      // the pivot row's in-block multipliers (steps k0 .. k-1) into LDS
+      if (wl >= 0 && lane == wl) {
+#pragma unroll
+        for (int u = 0; u < tt; ++u) my_lrow[u] = Lb[u];
+      }
+      // multiplier of step k
+      Lb[tt] = next ? ((alph != T(0)) ? cv / alph : T(0)) : T(0);
+      if (lane == 0) my_lrow[tt] = T(1);           // Lrow[k] = 1 (unit diagonal)
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      // g for step k+1: in-block terms u = k0 .. k, row-broadcast layout
+      {
+        const int u = lane & 15;
+        const T a0 = my_alpha[k0 + u], a1 = my_alpha[k0 + u + 1];
+        const T lm = my_lrow[u > 0 ? u - 1 : 0], l1 = my_lrow[u + 1];
+        const T up = (u <= tt - 1) ? a1 * l1 : T(0);
+        const T g = (u >= 1) ? up - a0 * lm : up;
+        gr = (u <= tt) ? g : T(0);
+      }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    }
+    if (done) break;
+    const int kn = k0 + kBBlk;                     // first step of the next block
+    if (kn + 1 >= n) break;
+    // the carry: column kn refreshed with all of this block's steps
+    const bool ta = my_row && lp >= kn + 1;        // rows still to be eliminated
     {
       T acc[4] = {T(0), T(0), T(0), T(0)};
-      if (0 < t) refresh16<0>(acc, gr[0], L);
-      if (16 < t) refresh16<1>(acc, gr[1], L);
-      if (32 < t) refresh16<2>(acc, gr[2], L);
-      if (48 < t) refresh16<3>(acc, gr[3], L);
+      refresh8<0>(acc, gr, Lb);
+      refresh8<1>(acc, gr, Lb);
       const T sum = fma(lsg, lv, (acc[0] + acc[1]) + (acc[2] + acc[3]));
-      if (active) cv = sum;
+      if (ta) cv = sum;
     }
-    // pivot: first maximum of |cv| by position (NaN never a candidate)
-    double av = -1.0;
-    if (active) {
-      const double mag = (double)fabs(cv);
-      if (mag == mag) av = mag;
-    }
-    double vmax;
-    int p;
-    const int wl = wave_first_max(av, active ? lp : INT32_MAX, vmax, p);
-    T alph;
-    int posw;
-    if (wl < 0) {                                  // no finite candidate: no exchange
-      p = k + 1;
-      alph = T(NAN);
-      posw = k + 1;
-    } else {
-      posw = __builtin_amdgcn_readlane(pos, wl);
-      alph = (T)vmax;
-      if (__builtin_amdgcn_readlane(cv < T(0) ? 1 : 0, wl)) alph = -alph;
-    }
-    if (lane == 0) my_alpha[t] = alph;
-    if (t + 2 == n) break;                         // alpha_{n-2}: last entry of T
-    if (lane == 0) my_piv[k + 1] = p;
-    if (p != k + 1) {
-      ++npiv;
-      if (my_row) {
-        if (lp == p) lp = k + 1;
-        else if (lp == k + 1) lp = p;
-      }
-    }
-    const bool next = my_row && lp >= k + 2;
-
-    // stored column of the pivot row for the next step: S(pos, posw)
-    if (next) {
-      const int hi = max(pos, posw), lo = min(pos, posw);
-      lv = orig[pack_idx(n, hi, lo)];
-      lsg = pos > posw ? T(1) : T(-1);
-    }
-    // the pivot row's multipliers (steps < t) into LDS, from its lane, in
-    // groups of 16 slots (entries past t-1 are unused)
-    if (wl >= 0 && lane == wl) {
-#pragma unroll
-      for (int g0 = 0; g0 < kBSlots; g0 += 16) {
-        if (g0 < t) {
-#pragma unroll
-          for (int c = g0; c < g0 + 16; ++c) my_lrowp[c + 1] = L[c];
-        }
-      }
-    }
-    // multiplier of step k into slot t
+    // S += Lx Tx Lx^T on the trailing rows: Lx = [Lb, carry], Bt = Lx Tx^T,
+    // each entry of this lane's Bt row formed just before it is spread
     {
-      const T l = next ? ((alph != T(0)) ? cv / alph : T(0)) : T(0);
-      const int c = t;
-      const bool on = next;
-      const T v = l;
-#define LTLT_SET_GROUP(G0)                                                                                  \
-      if ((c >> 4) == (G0) / 16) {                                                                        \
-        _Pragma("unroll") for (int i = 0; i < 16; ++i) L[(G0) + i] = (on && c == (G0) + i) ? v : L[(G0) + i]; \
-      }
-      LTLT_SET_GROUP(0) LTLT_SET_GROUP(16) LTLT_SET_GROUP(32) LTLT_SET_GROUP(48)
-#undef LTLT_SET_GROUP
-    }
-    if (lane == 0) my_lrowp[t + 1] = T(1);         // Lrow[t] = 1 (unit diagonal)
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    // g for step t+1 (t+1 terms), row-broadcast layout
-    {
-      const int c = lane & 15;
+      T X[18];
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        if (kk * 16 <= t) {
-          const int u = 16 * kk + c;
-          const T a0 = my_alpha[u], a1 = my_alpha[u + 1];
-          const T lm = my_lrowp[u], l1 = my_lrowp[u + 2];
-          const T up = (u <= t - 1) ? a1 * l1 : T(0);
-          const T g = (u >= 1) ? up - a0 * lm : up;
-          gr[kk] = (u <= t) ? g : T(0);
-        }
+      for (int u = 0; u < kBBlk; ++u) X[u] = Lb[u];
+      X[16] = cv;
+      X[17] = T(0);
+      const T* al = my_alpha + k0;                 // al[u] = alpha_{k0+u}
+      const uint64_t tmask = __ballot(ta);         // bit l: row l+1 trailing
+#pragma unroll 1
+      for (int q = 0; q < 4; ++q) {
+        const unsigned qm = (unsigned)(tmask >> (16 * q)) & 0xFFFFu;
+        if (qm == 0) continue;
+        const int addr = (16 * q + (lane & 15)) * 4;
+        T R[18];
+        R[0] = bperm(addr, al[1] * X[1]);
+#pragma unroll
+        for (int u = 1; u < kBBlk - 1; ++u) R[u] = bperm(addr, al[u + 1] * X[u + 1] - al[u] * X[u - 1]);
+        R[15] = bperm(addr, X[16] - al[15] * X[14]);
+        R[16] = bperm(addr, -X[15]);
+        R[17] = T(0);
+        update_group<0>(orig, n, lane, pos, ta, qm, q, R, X);
+        update_group<1>(orig, n, lane, pos, ta, qm, q, R, X);
+        update_group<2>(orig, n, lane, pos, ta, qm, q, R, X);
+        update_group<3>(orig, n, lane, pos, ta, qm, q, R, X);
       }
     }
+    // archive the block's multipliers
+#define LTLT_ARCHIVE(B)                                                   \
+    if (k0 == 16 * B) {                                                   \
+      _Pragma("unroll") for (int u = 0; u < kBBlk; ++u) L[16 * B + u] = Lb[u]; \
+    }
+    LTLT_ARCHIVE(0) LTLT_ARCHIVE(1) LTLT_ARCHIVE(2) LTLT_ARCHIVE(3)
+#pragma unroll
+    for (int u = 0; u < kBBlk; ++u) Lb[u] = T(0);
+    gr = T(0);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    k0 = kn;
   }
+  LTLT_ARCHIVE(0) LTLT_ARCHIVE(1) LTLT_ARCHIVE(2) LTLT_ARCHIVE(3)
+#undef LTLT_ARCHIVE
 
   // ---- outputs: A(k+1,k) = alpha_k; the row at final position r holds the
   //      multipliers of the steps before it became final: A(r, u) = L[u],
