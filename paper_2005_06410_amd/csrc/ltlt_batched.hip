@@ -39,7 +39,7 @@ constexpr int kBBlk = 16;                        // column steps per block
 constexpr int kBPack = kBN * (kBN - 1) / 2;      // packed strict lower triangle
 constexpr int kBAlpha = kBSlots + 2;             // alpha history (even length keeps the next array 16-byte aligned)
 constexpr int kBRow = kBBlk + 2;                 // pivot row's in-block multipliers and its unit
-constexpr int kBWaveLds = kBPack + kBAlpha + kBRow + kBN;   // + ipiv (kBN ints fit in kBN elements)
+constexpr int kBWaveLds = kBPack + kBAlpha + kBRow + 2 * kBN;   // + ipiv and the trailing-row table (kBN ints each)
 constexpr int kBWaves = 4;                       // matrices per workgroup
 
 // Offset of X(i, c), i > c, in the column-packed strict lower triangle.
@@ -82,6 +82,57 @@ LTLT_REFRESH_FNS(float, "v_fmac_f32_dpp")
 #undef LTLT_REFRESH_FNS
 #undef LTLT_REFRESH8
 #undef LTLT_BF
+
+// Wave-wide maximum of an unsigned key, every lane gets it: DPP row shifts and
+// row broadcasts folded into v_max_u32 (a lane without a source is not
+// written and keeps its key), two wait states before each DPP read.
+__device__ __forceinline__ unsigned wave_umax_b(unsigned x) {
+  asm volatile(
+      "s_nop 1\n"
+      "v_max_u32_dpp %0, %0, %0 row_shr:1 row_mask:0xf bank_mask:0xf\n"
+      "s_nop 1\n"
+      "v_max_u32_dpp %0, %0, %0 row_shr:2 row_mask:0xf bank_mask:0xf\n"
+      "s_nop 1\n"
+      "v_max_u32_dpp %0, %0, %0 row_shr:4 row_mask:0xf bank_mask:0xf\n"
+      "s_nop 1\n"
+      "v_max_u32_dpp %0, %0, %0 row_shr:8 row_mask:0xf bank_mask:0xf\n"
+      "s_nop 1\n"
+      "v_max_u32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
+      "s_nop 1\n"
+      "v_max_u32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf\n"
+      "s_nop 1\n"
+      : "+v"(x));
+  return (unsigned)__builtin_amdgcn_readlane((int)x, 63);
+}
+// First maximum of (value, key) over the wave, as wave_first_max: the largest
+// value, among equal values the smallest key (then the lowest lane).
+__device__ __forceinline__ int wave_first_max_b(double v, int key, double& vmax, int& kmin) {
+  const unsigned hk = v >= 0.0 ? (unsigned)__double2hiint(v) + 1u : 0u;
+  const unsigned mh = wave_umax_b(hk);
+  if (mh == 0) { vmax = -1.0; kmin = INT32_MAX; return -1; }
+  const bool tie_hi = hk == mh;
+  unsigned long long hit = __ballot(tie_hi);
+  int src = __ffsll(hit) - 1;
+  unsigned blo = (unsigned)__builtin_amdgcn_readlane(__double2loint(v), src);
+  kmin = __builtin_amdgcn_readlane(key, src);
+  hit &= hit - 1;
+  if (hit) {
+    if (mh == 1u && __ballot(tie_hi && __double2loint(v) != 0) == 0) {   // every tied value is +0
+      kmin = (int)~wave_umax_b(tie_hi ? ~(unsigned)key : 0u);
+      src = __ffsll(__ballot(tie_hi && key == kmin)) - 1;
+    } else {
+      while (hit) {
+        const int l2 = __ffsll(hit) - 1;
+        const unsigned lo2 = (unsigned)__builtin_amdgcn_readlane(__double2loint(v), l2);
+        const int k2 = __builtin_amdgcn_readlane(key, l2);
+        if (lo2 > blo || (lo2 == blo && k2 < kmin)) { blo = lo2; kmin = k2; src = l2; }
+        hit &= hit - 1;
+      }
+    }
+  }
+  vmax = __hiloint2double((int)(mh - 1u), (int)blo);
+  return src;
+}
 
 // Block update of four columns b = 16q + C0..C0+3 (lanes of one 16-lane row):
 // a[j] += sum_u R_u(lane C0+j of each row) * X_u, u = U0..U0+8, where R_u holds
@@ -131,21 +182,24 @@ LTLT_UPD_FNS(float, "v_fmac_f32_dpp")
 #undef LTLT_BU9
 #undef LTLT_BU1
 
-// Columns b = 16q + 4G .. 16q + 4G + 3 of the block update (see upd4):
-// entries S(pos, b+1) of this lane's row for b+1 < pos, both rows trailing.
+// Columns 16q + 4G .. 16q + 4G + 3 of the trailing rows in lane order (see
+// upd4): for the row b of each, S(pos, b) += sum_u Lx(pos,u) Bt(b,u) when
+// b < pos and this lane's row is trailing.  pbv holds, in lane c of each
+// 16-lane row, the original index of column 16q + c (0 past the last).
 template <int G, typename T>
-__device__ __forceinline__ void update_group(T* orig, int n, int lane, int pos, bool ta, unsigned qm, int q,
-                                             const T (&R)[18], const T (&X)[18]) {
-  if (((qm >> (4 * G)) & 0xFu) == 0) return;     // none of the four rows is still trailing
+__device__ __forceinline__ void update_group(T* orig, int n, int pos, bool ta, int pbv, const T (&R)[18],
+                                             const T (&X)[18]) {
+  int pb[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) pb[j] = __builtin_amdgcn_readlane(pbv, 4 * G + j);
+  if (pb[0] == 0) return;                        // past the last trailing row
   T a[4];
   int idx[4];
   bool ok[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const int c = 4 * G + j;
-    const int bl = 16 * q + c;                   // lane of row b+1
-    ok[j] = ta && lane > bl && ((qm >> c) & 1u);
-    idx[j] = ok[j] ? pack_idx(n, pos, bl + 1) : 0;
+    ok[j] = ta && pb[j] != 0 && pos > pb[j];
+    idx[j] = ok[j] ? pack_idx(n, pos, pb[j]) : 0;
     a[j] = orig[idx[j]];
   }
   upd4<G>(a, R, X);
@@ -169,12 +223,12 @@ __global__ void __launch_bounds__(256, 2) batched_kernel(int n, int batch, T* Aa
   T* my_alpha = orig + kBPack;
   T* my_lrow = my_alpha + kBAlpha;                 // my_lrow[u] = Lrow[k0 + u]
   int* my_piv = reinterpret_cast<int*>(my_lrow + kBRow);   // ipiv, written out at the end
+  int* my_tab = reinterpret_cast<int*>(my_lrow + kBRow + kBN);   // lanes of the trailing rows, in lane order
 
   // strict lower triangle into LDS.  Column c holds n-1-c < 64 entries, one
-  // per lane (coalesced); the loads of 16 columns are issued before any of
-  // them is written, so a matrix costs four memory round trips instead of one
-  // per column.
-  constexpr int kBFill = 16;
+  // per lane (coalesced); the loads of all columns are issued before any of
+  // them is written, so a matrix costs one memory round trip.
+  constexpr int kBFill = kBN;
   for (int c0 = 0; c0 + 1 < n; c0 += kBFill) {
     T v[kBFill];
 #pragma unroll
@@ -226,7 +280,7 @@ __global__ void __launch_bounds__(256, 2) batched_kernel(int n, int batch, T* Aa
       }
       double vmax;
       int p;
-      const int wl = wave_first_max(av, active ? lp : INT32_MAX, vmax, p);
+      const int wl = wave_first_max_b(av, active ? lp : INT32_MAX, vmax, p);
       T alph;
       int posw;
       if (wl < 0) {                                // no finite candidate: no exchange
@@ -297,12 +351,17 @@ __global__ void __launch_bounds__(256, 2) batched_kernel(int n, int batch, T* Aa
       X[16] = cv;
       X[17] = T(0);
       const T* al = my_alpha + k0;                 // al[u] = alpha_{k0+u}
+      // the trailing rows' lanes in lane order: my_tab[j] = lane of the j-th
       const uint64_t tmask = __ballot(ta);         // bit l: row l+1 trailing
+      const int m = __popcll(tmask);
+      if (ta) my_tab[__builtin_amdgcn_mbcnt_hi((unsigned)(tmask >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)tmask, 0u))] = lane;
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll 1
-      for (int q = 0; q < 4; ++q) {
-        const unsigned qm = (unsigned)(tmask >> (16 * q)) & 0xFFFFu;
-        if (qm == 0) continue;
-        const int addr = (16 * q + (lane & 15)) * 4;
+      for (int q = 0; 16 * q < m; ++q) {
+        const int j = 16 * q + (lane & 15);        // this lane's column of the group
+        const int src = j < m ? my_tab[j] : 0;
+        const int pbv = j < m ? src + 1 : 0;       // original index of that column's row
+        const int addr = src * 4;
         T R[18];
         R[0] = bperm(addr, al[1] * X[1]);
 #pragma unroll
@@ -310,10 +369,10 @@ __global__ void __launch_bounds__(256, 2) batched_kernel(int n, int batch, T* Aa
         R[15] = bperm(addr, X[16] - al[15] * X[14]);
         R[16] = bperm(addr, -X[15]);
         R[17] = T(0);
-        update_group<0>(orig, n, lane, pos, ta, qm, q, R, X);
-        update_group<1>(orig, n, lane, pos, ta, qm, q, R, X);
-        update_group<2>(orig, n, lane, pos, ta, qm, q, R, X);
-        update_group<3>(orig, n, lane, pos, ta, qm, q, R, X);
+        update_group<0>(orig, n, pos, ta, pbv, R, X);
+        update_group<1>(orig, n, pos, ta, pbv, R, X);
+        update_group<2>(orig, n, pos, ta, pbv, R, X);
+        update_group<3>(orig, n, pos, ta, pbv, R, X);
       }
     }
     // archive the block's multipliers
