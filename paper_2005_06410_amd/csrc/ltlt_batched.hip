@@ -39,7 +39,8 @@ constexpr int kBBlk = 16;                        // column steps per block
 constexpr int kBPack = kBN * (kBN - 1) / 2;      // packed strict lower triangle
 constexpr int kBAlpha = kBSlots + 2;             // alpha history (even length keeps the next array 16-byte aligned)
 constexpr int kBRow = kBBlk + 2;                 // pivot row's in-block multipliers and its unit
-constexpr int kBWaveLds = kBPack + kBAlpha + kBRow + 2 * kBN;   // + ipiv and the trailing-row table (kBN ints each)
+constexpr int kBPiv = kBN + 4;                   // ipiv entries 0..64 (steps past n-2 write up to entry 64)
+constexpr int kBWaveLds = kBPack + kBAlpha + kBRow + kBPiv + kBN;   // + ipiv and the trailing-row table (ints)
 constexpr int kBWaves = 4;                       // matrices per workgroup
 
 // Offset of X(i, c), i > c, in the column-packed strict lower triangle.
@@ -223,7 +224,7 @@ __global__ void __launch_bounds__(256, 2) batched_kernel(int n, int batch, T* Aa
   T* my_alpha = orig + kBPack;
   T* my_lrow = my_alpha + kBAlpha;                 // my_lrow[u] = Lrow[k0 + u]
   int* my_piv = reinterpret_cast<int*>(my_lrow + kBRow);   // ipiv, written out at the end
-  int* my_tab = reinterpret_cast<int*>(my_lrow + kBRow + kBN);   // lanes of the trailing rows, in lane order
+  int* my_tab = reinterpret_cast<int*>(my_lrow + kBRow + kBPiv);   // lanes of the trailing rows, in lane order
 
   // strict lower triangle into LDS.  Column c holds n-1-c < 64 entries, one
   // per lane (coalesced); the loads of all columns are issued before any of
@@ -257,13 +258,15 @@ __global__ void __launch_bounds__(256, 2) batched_kernel(int n, int batch, T* Aa
   T lv = my_row ? orig[pack_idx(n, pos, 0)] : T(0), lsg = T(1);   // column 0: S(pos, 0)
   int npiv = 0;                                    // exchanges made (Pfaffian sign)
 
+  // Every block runs all 16 steps: a step with k + 2 >= n has at most the
+  // row at position n-1 as candidate and no row below it, so it forms alpha_k
+  // (k = n-2) or nothing, exchanges nothing and leaves every multiplier 0;
+  // its alpha and pivot entries past n-2 are never read.
   int k0 = 0;
-  bool done = n < 2;
-  while (!done) {
+  while (k0 + 1 < n) {
 #pragma unroll
-    for (int tt = 0; tt < kBBlk; ++tt) {          // step k = k0 + tt; k = n-2 only forms alpha_{n-2}
+    for (int tt = 0; tt < kBBlk; ++tt) {          // step k = k0 + tt
       const int k = k0 + tt;
-      if (done || k + 1 >= n) { done = true; continue; }
       const bool active = my_row && lp >= k + 1;
       if (tt > 0 || k0 == 0) {                    // a block's first column is the carry of the block before
         T acc[4] = {T(0), T(0), T(0), T(0)};
@@ -292,9 +295,10 @@ __global__ void __launch_bounds__(256, 2) batched_kernel(int n, int batch, T* Aa
         alph = (T)vmax;
         if (__builtin_amdgcn_readlane(cv < T(0) ? 1 : 0, wl)) alph = -alph;
       }
-      if (lane == 0) my_alpha[k] = alph;
-      if (k + 2 == n) { done = true; continue; }   // alpha_{n-2}: last entry of T
-      if (lane == 0) my_piv[k + 1] = p;
+      if (lane == 0) {
+        my_alpha[k] = alph;
+        my_piv[k + 1] = p;                         // k + 1 <= 64 < kBPiv
+      }
       if (p != k + 1) {
         ++npiv;
         if (my_row) {
@@ -315,22 +319,24 @@ __global__ void __launch_bounds__(256, 2) batched_kernel(int n, int batch, T* Aa
 #pragma unroll
         for (int u = 0; u < tt; ++u) my_lrow[u] = Lb[u];
       }
-      // multiplier of step k
-      Lb[tt] = next ? ((alph != T(0)) ? cv / alph : T(0)) : T(0);
       if (lane == 0) my_lrow[tt] = T(1);           // Lrow[k] = 1 (unit diagonal)
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      // multiplier of step k: the division is issued after the LDS stores
+      // above and before the wait below, so its latency overlaps theirs
+      asm volatile("" : "+v"(cv) : : "memory");
+      Lb[tt] = next ? ((alph != T(0)) ? cv / alph : T(0)) : T(0);
+      asm volatile("s_waitcnt lgkmcnt(0)" : : "v"(Lb[tt]) : "memory");
       // g for step k+1: in-block terms u = k0 .. k, row-broadcast layout
       {
         const int u = lane & 15;
-        const T a0 = my_alpha[k0 + u], a1 = my_alpha[k0 + u + 1];
-        const T lm = my_lrow[u > 0 ? u - 1 : 0], l1 = my_lrow[u + 1];
+        T a0 = my_alpha[k0 + u], a1 = my_alpha[k0 + u + 1];
+        T lm = my_lrow[u > 0 ? u - 1 : 0], l1 = my_lrow[u + 1];
+        asm volatile("" : "+v"(a0), "+v"(a1), "+v"(lm), "+v"(l1));   // all four loads in one round trip
         const T up = (u <= tt - 1) ? a1 * l1 : T(0);
         const T g = (u >= 1) ? up - a0 * lm : up;
         gr = (u <= tt) ? g : T(0);
       }
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     }
-    if (done) break;
     const int kn = k0 + kBBlk;                     // first step of the next block
     if (kn + 1 >= n) break;
     // the carry: column kn refreshed with all of this block's steps
