@@ -43,8 +43,10 @@ constexpr int kBPiv = kBN + 4;                   // ipiv entries 0..64 (steps pa
 constexpr int kBWaveLds = kBPack + kBAlpha + kBRow + kBPiv + kBN;   // + ipiv and the trailing-row table (ints)
 constexpr int kBWaves = 4;                       // matrices per workgroup
 
-// Offset of X(i, c), i > c, in the column-packed strict lower triangle.
-__device__ __forceinline__ int pack_idx(int n, int i, int c) { return c * (2 * n - c - 1) / 2 + (i - c - 1); }
+// Offset of X(i, c), i > c, in the column-packed strict lower triangle:
+// col_off(n, c) + i.
+__device__ __forceinline__ int col_off(int n, int c) { return c * (2 * n - c - 1) / 2 - c - 1; }
+__device__ __forceinline__ int pack_idx(int n, int i, int c) { return col_off(n, c) + i; }
 
 // One value from lane addr/4 (ds_bpermute: a cross-lane read, no LDS storage).
 __device__ __forceinline__ double bperm(int addr, double v) {
@@ -117,7 +119,7 @@ __device__ __forceinline__ int wave_first_max_b(double v, int key, double& vmax,
   unsigned blo = (unsigned)__builtin_amdgcn_readlane(__double2loint(v), src);
   kmin = __builtin_amdgcn_readlane(key, src);
   hit &= hit - 1;
-  if (hit) {
+  if (__builtin_expect(hit != 0, 0)) {
     if (mh == 1u && __ballot(tie_hi && __double2loint(v) != 0) == 0) {   // every tied value is +0
       kmin = (int)~wave_umax_b(tie_hi ? ~(unsigned)key : 0u);
       src = __ffsll(__ballot(tie_hi && key == kmin)) - 1;
@@ -200,7 +202,7 @@ __device__ __forceinline__ void update_group(T* orig, int n, int pos, bool ta, i
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     ok[j] = ta && pb[j] != 0 && pos > pb[j];
-    idx[j] = ok[j] ? pack_idx(n, pos, pb[j]) : 0;
+    idx[j] = ok[j] ? col_off(n, pb[j]) + pos : 0;
     a[j] = orig[idx[j]];
   }
   upd4<G>(a, R, X);
@@ -247,6 +249,7 @@ __global__ void __launch_bounds__(256, 2) batched_kernel(int n, int batch, T* Aa
 
   const bool my_row = lane + 1 < n;
   const int pos = lane + 1;                        // original index of this lane's row
+  const int cof = col_off(n, pos);                 // its column's offset in the packed triangle
   int lp = pos;                                    // its current position
   T L[kBSlots], Lb[kBBlk];                         // finished blocks' multipliers; the current block's
 #pragma unroll
@@ -284,42 +287,33 @@ __global__ void __launch_bounds__(256, 2) batched_kernel(int n, int batch, T* Aa
       double vmax;
       int p;
       const int wl = wave_first_max_b(av, active ? lp : INT32_MAX, vmax, p);
-      T alph;
-      int posw;
-      if (wl < 0) {                                // no finite candidate: no exchange
-        p = k + 1;
-        alph = T(NAN);
-        posw = k + 1;
-      } else {
-        posw = __builtin_amdgcn_readlane(pos, wl);
-        alph = (T)vmax;
-        if (__builtin_amdgcn_readlane(cv < T(0) ? 1 : 0, wl)) alph = -alph;
-      }
-      if (lane == 0) {
-        my_alpha[k] = alph;
-        my_piv[k + 1] = p;                         // k + 1 <= 64 < kBPiv
-      }
-      if (p != k + 1) {
-        ++npiv;
-        if (my_row) {
-          if (lp == p) lp = k + 1;
-          else if (lp == k + 1) lp = p;
-        }
-      }
+      // no finite candidate (wl < 0): no exchange, alpha NaN
+      const int wsrc = wl < 0 ? 0 : wl;
+      const int posw = wl < 0 ? k + 1 : __builtin_amdgcn_readlane(pos, wsrc);
+      const int wneg = __builtin_amdgcn_readlane(cv < T(0) ? 1 : 0, wsrc);
+      const T alph = wl < 0 ? T(NAN) : (wneg ? -(T)vmax : (T)vmax);
+      if (wl < 0) p = k + 1;
+      my_alpha[k] = alph;                          // uniform values, stored by every lane
+      my_piv[k + 1] = p;                           // k + 1 <= 64 < kBPiv
+      npiv += p != k + 1 ? 1 : 0;
+      if (my_row) lp = lp == p ? k + 1 : (lp == k + 1 ? p : lp);
       const bool next = my_row && lp >= k + 2;
 
       // stored column of the pivot row for the next step: S(pos, posw)
-      if (next) {
-        const int hi = max(pos, posw), lo = min(pos, posw);
-        lv = orig[pack_idx(n, hi, lo)];
-        lsg = pos > posw ? T(1) : T(-1);
+      {
+        const int idx = pos > posw ? col_off(n, posw) + pos : cof + posw;
+        const T v = orig[next ? idx : 0];
+        if (next) {
+          lv = v;
+          lsg = pos > posw ? T(1) : T(-1);
+        }
       }
       // the pivot row's in-block multipliers (steps k0 .. k-1) into LDS
       if (wl >= 0 && lane == wl) {
 #pragma unroll
         for (int u = 0; u < tt; ++u) my_lrow[u] = Lb[u];
       }
-      if (lane == 0) my_lrow[tt] = T(1);           // Lrow[k] = 1 (unit diagonal)
+      my_lrow[tt] = T(1);                          // Lrow[k] = 1 (unit diagonal), every lane
       // multiplier of step k: the division is issued after the LDS stores
       // above and before the wait below, so its latency overlaps theirs
       asm volatile("" : "+v"(cv) : : "memory");
