@@ -285,7 +285,12 @@ def test_skew_update_operand_layouts(layout):
 
 # --------------------------------------------------------------------------
 @pytest.mark.parametrize("n,batch,dtype", [(64, 8192, np.float64), (64, 300, np.float32), (1, 5, np.float64),
-                                           (2, 5, np.float64), (7, 33, np.float64), (40, 129, np.float64)])
+                                           (2, 5, np.float64), (7, 33, np.float64), (40, 129, np.float64),
+                                           # orders at the 16-step block boundaries of the batched kernel
+                                           (16, 65, np.float64), (17, 65, np.float64), (18, 65, np.float64),
+                                           (32, 65, np.float64), (33, 65, np.float64), (48, 65, np.float64),
+                                           (49, 65, np.float64), (50, 65, np.float64), (63, 65, np.float64),
+                                           (33, 65, np.float32)])
 def test_batched_parity(n, batch, dtype):
     Xs = synth.skew_batch(n, batch, 6 << 32 if n == 64 else 99).astype(dtype)
     ref_p, ref_i, ref_l, ref_s = oracle.ltlt_batched(Xs)
