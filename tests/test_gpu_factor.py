@@ -324,6 +324,44 @@ def test_batched_parity(n, batch, dtype):
     assert np.array_equal(full[:, iu[0], iu[1]], Xs[:, iu[0], iu[1]])
 
 
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+def test_batched_padded_layout(dtype):
+    """lda > n and a matrix stride past lda*n: the factors land in each
+    matrix's strict lower triangle at its leading dimension, and the padding
+    rows, the gaps between matrices, the diagonal and the upper triangle keep
+    their sentinel values."""
+    n, batch, lda = 40, 37, 47
+    stride = lda * n + 13
+    Xs = synth.skew_batch(n, batch, 4242).astype(dtype)
+    ref_p, ref_i, ref_l, ref_s = oracle.ltlt_batched(Xs)
+    sentinel = dtype(-7.25)
+    flat = np.full(stride * batch, sentinel, dtype=dtype)
+    for b in range(batch):
+        M = np.full((n, lda), sentinel, dtype=dtype)     # M[c, r] = A(r, c): column-major with lda
+        M[:, :n] = Xs[b].T
+        flat[b * stride:b * stride + lda * n] = M.ravel()
+    d = torch.from_numpy(flat.copy()).cuda()
+    A = d.as_strided((batch, n, n), (stride, 1, lda))
+    ipiv, logabs, sign = lt().factor_batched(A)
+    torch.cuda.synchronize()
+    out = d.cpu().numpy()
+    gi = ipiv.cpu().numpy()
+    tol = 1e-10 if dtype == np.float64 else 1e-4
+    for b in range(batch):
+        blk = out[b * stride:(b + 1) * stride]
+        M = blk[:lda * n].reshape(n, lda)               # M[c, r] = A(r, c)
+        got = np.tril(M[:, :n].T, -1)
+        if np.array_equal(gi[b], ref_i[b]):
+            assert np.abs(got.astype(np.float64) - ref_p[b]).max() <= tol * max(np.abs(ref_p[b]).max(), 1e-300)
+        else:
+            compare_factors(Xs[b], got, gi[b], dtype)
+        assert np.all(M[:, n:] == sentinel)             # padding rows n .. lda-1
+        assert np.all(blk[lda * n:] == sentinel)        # gap before the next matrix
+        iu = np.triu_indices(n, 0)
+        assert np.array_equal(M[:, :n].T[iu], Xs[b][iu])
+    assert np.array_equal(sign.cpu().numpy(), ref_s)
+
+
 def test_batched_zero_structured_matrices():
     """Zero-structured members of a batch: 4x4 block-diagonal matrices (every
     column step ties on zeros outside one block, and every k = 3 mod 4 column
