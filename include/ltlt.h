@@ -228,7 +228,10 @@ int ltlt_solve(int64_t n, const void* A, int64_t lda, int dtype, const int32_t* 
 
 /*
  * ltlt_factor_batched -- independent factorizations and Pfaffians of `batch`
- * matrices of order n <= LTLT_BATCHED_MAX_N, one workgroup per matrix.
+ * matrices of order n <= LTLT_BATCHED_MAX_N, one wave per matrix (four per
+ * workgroup).  The pivot rule, storage and Pfaffian are those of
+ * ltlt_factor and ltlt_pfaffian; the column updates are applied in blocks of
+ * 16 steps (a different rounding order, same tolerance).
  *   n          (1) order, 0 <= n <= LTLT_BATCHED_MAX_N.
  *   batch      (2) number of matrices, >= 0.
  *   A          (3) device; matrix b is column-major at A + b*strideA
