@@ -86,57 +86,6 @@ LTLT_REFRESH_FNS(float, "v_fmac_f32_dpp")
 #undef LTLT_REFRESH8
 #undef LTLT_BF
 
-// Wave-wide maximum of an unsigned key, every lane gets it: DPP row shifts and
-// row broadcasts folded into v_max_u32 (a lane without a source is not
-// written and keeps its key), two wait states before each DPP read.
-__device__ __forceinline__ unsigned wave_umax_b(unsigned x) {
-  asm volatile(
-      "s_nop 1\n"
-      "v_max_u32_dpp %0, %0, %0 row_shr:1 row_mask:0xf bank_mask:0xf\n"
-      "s_nop 1\n"
-      "v_max_u32_dpp %0, %0, %0 row_shr:2 row_mask:0xf bank_mask:0xf\n"
-      "s_nop 1\n"
-      "v_max_u32_dpp %0, %0, %0 row_shr:4 row_mask:0xf bank_mask:0xf\n"
-      "s_nop 1\n"
-      "v_max_u32_dpp %0, %0, %0 row_shr:8 row_mask:0xf bank_mask:0xf\n"
-      "s_nop 1\n"
-      "v_max_u32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
-      "s_nop 1\n"
-      "v_max_u32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf\n"
-      "s_nop 1\n"
-      : "+v"(x));
-  return (unsigned)__builtin_amdgcn_readlane((int)x, 63);
-}
-// First maximum of (value, key) over the wave, as wave_first_max: the largest
-// value, among equal values the smallest key (then the lowest lane).
-__device__ __forceinline__ int wave_first_max_b(double v, int key, double& vmax, int& kmin) {
-  const unsigned hk = v >= 0.0 ? (unsigned)__double2hiint(v) + 1u : 0u;
-  const unsigned mh = wave_umax_b(hk);
-  if (mh == 0) { vmax = -1.0; kmin = INT32_MAX; return -1; }
-  const bool tie_hi = hk == mh;
-  unsigned long long hit = __ballot(tie_hi);
-  int src = __ffsll(hit) - 1;
-  unsigned blo = (unsigned)__builtin_amdgcn_readlane(__double2loint(v), src);
-  kmin = __builtin_amdgcn_readlane(key, src);
-  hit &= hit - 1;
-  if (__builtin_expect(hit != 0, 0)) {
-    if (mh == 1u && __ballot(tie_hi && __double2loint(v) != 0) == 0) {   // every tied value is +0
-      kmin = (int)~wave_umax_b(tie_hi ? ~(unsigned)key : 0u);
-      src = __ffsll(__ballot(tie_hi && key == kmin)) - 1;
-    } else {
-      while (hit) {
-        const int l2 = __ffsll(hit) - 1;
-        const unsigned lo2 = (unsigned)__builtin_amdgcn_readlane(__double2loint(v), l2);
-        const int k2 = __builtin_amdgcn_readlane(key, l2);
-        if (lo2 > blo || (lo2 == blo && k2 < kmin)) { blo = lo2; kmin = k2; src = l2; }
-        hit &= hit - 1;
-      }
-    }
-  }
-  vmax = __hiloint2double((int)(mh - 1u), (int)blo);
-  return src;
-}
-
 // Block update of four columns b = 16q + C0..C0+3 (lanes of one 16-lane row):
 // a[j] += sum_u R_u(lane C0+j of each row) * X_u, u = U0..U0+8, where R_u holds
 // row 16q + (lane & 15) of Bt and X the lane's own row of Lx.
@@ -286,7 +235,7 @@ __global__ void __launch_bounds__(256, 2) batched_kernel(int n, int batch, T* Aa
       }
       double vmax;
       int p;
-      const int wl = wave_first_max_b(av, active ? lp : INT32_MAX, vmax, p);
+      const int wl = wave_first_max(av, active ? lp : INT32_MAX, vmax, p);
       // no finite candidate (wl < 0): no exchange, alpha NaN
       const int wsrc = wl < 0 ? 0 : wl;
       const int posw = wl < 0 ? k + 1 : __builtin_amdgcn_readlane(pos, wsrc);

@@ -145,19 +145,25 @@ __device__ __forceinline__ void refresh16(float (&acc)[4], float g, const float 
 #undef LTLT_FMAC16
 
 // Wave-wide maximum of an unsigned key (every lane gets it): DPP row shifts
-// and row broadcasts; lanes without a source keep their own key.
-template <int CTRL, int ROW_MASK>
-__device__ __forceinline__ unsigned dpp_umax_step(unsigned x) {
-  const unsigned o = (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, CTRL, ROW_MASK, 0xF, false);
-  return o > x ? o : x;
-}
+// and row broadcasts folded into v_max_u32 (a lane without a source is not
+// written and keeps its key), two wait states before each DPP read; lane 63
+// ends with the maximum.
 __device__ __forceinline__ unsigned wave_umax(unsigned x) {
-  x = dpp_umax_step<0x111, 0xF>(x);   // row_shr:1
-  x = dpp_umax_step<0x112, 0xF>(x);   // row_shr:2
-  x = dpp_umax_step<0x114, 0xF>(x);   // row_shr:4
-  x = dpp_umax_step<0x118, 0xF>(x);   // row_shr:8  -> lane 15 of each row holds the row maximum
-  x = dpp_umax_step<0x142, 0xA>(x);   // row_bcast:15 into rows 1 and 3
-  x = dpp_umax_step<0x143, 0xC>(x);   // row_bcast:31 into rows 2 and 3 -> lane 63 holds the maximum
+  asm volatile(
+      "s_nop 1\n"
+      "v_max_u32_dpp %0, %0, %0 row_shr:1 row_mask:0xf bank_mask:0xf\n"
+      "s_nop 1\n"
+      "v_max_u32_dpp %0, %0, %0 row_shr:2 row_mask:0xf bank_mask:0xf\n"
+      "s_nop 1\n"
+      "v_max_u32_dpp %0, %0, %0 row_shr:4 row_mask:0xf bank_mask:0xf\n"
+      "s_nop 1\n"
+      "v_max_u32_dpp %0, %0, %0 row_shr:8 row_mask:0xf bank_mask:0xf\n"
+      "s_nop 1\n"
+      "v_max_u32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf\n"
+      "s_nop 1\n"
+      "v_max_u32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf\n"
+      "s_nop 1\n"
+      : "+v"(x));
   return (unsigned)__builtin_amdgcn_readlane((int)x, 63);
 }
 // First maximum of (value, key) over the wave: the largest value, and among
@@ -183,7 +189,7 @@ __device__ __forceinline__ int wave_first_max(double v, int key, double& vmax, i
   unsigned blo = (unsigned)__builtin_amdgcn_readlane(__double2loint(v), src);
   kmin = __builtin_amdgcn_readlane(key, src);
   hit &= hit - 1;
-  if (hit) {
+  if (__builtin_expect(hit != 0, 0)) {
     if (mh == 1u && __ballot(tie_hi && __double2loint(v) != 0) == 0) {   // every tied value is +0
       kmin = (int)~wave_umax(tie_hi ? ~(unsigned)key : 0u);
       src = __ffsll(__ballot(tie_hi && key == kmin)) - 1;

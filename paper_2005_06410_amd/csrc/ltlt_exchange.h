@@ -82,11 +82,41 @@ __device__ __forceinline__ void set_slot(T (&L)[KC], int c, bool on, T v) {
 #undef LTLT_SLOT_CASE4
 #undef LTLT_SLOT_CASE
 
+// v + (v of lane ^ 16) or v + (v of lane ^ 32) through the gfx950 lane
+// swaps (no LDS crossbar round trip): with both operands v, permlane16_swap
+// returns in every 16-lane row the values of the even row of its pair and
+// of the odd row (permlane32_swap: of the lower and the upper half), whose
+// sum has the same two terms as v + shfl_xor(v, 16 | 32), bit for bit.
+template <int OFF>
+__device__ __forceinline__ unsigned xor_pair(unsigned x, unsigned& other) {
+  if constexpr (OFF == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    other = r[1];
+    return r[0];
+  } else {
+    const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    other = r[1];
+    return r[0];
+  }
+}
+template <int OFF>
+__device__ __forceinline__ double xor_add(double v) {
+  unsigned lo1, hi1;
+  const unsigned lo0 = xor_pair<OFF>((unsigned)__double2loint(v), lo1);
+  const unsigned hi0 = xor_pair<OFF>((unsigned)__double2hiint(v), hi1);
+  return __hiloint2double((int)hi0, (int)lo0) + __hiloint2double((int)hi1, (int)lo1);
+}
+template <int OFF>
+__device__ __forceinline__ float xor_add(float v) {
+  unsigned o;
+  const unsigned a = xor_pair<OFF>(__float_as_uint(v), o);
+  return __uint_as_float(a) + __uint_as_float(o);
+}
 // Sum of v over the S parts of a row (lanes lane ^ 16, lane ^ 32).
 template <int S, typename T>
 __device__ __forceinline__ T part_sum(T v) {
-  if constexpr (S == 4) v += __shfl_xor(v, 16, kWave);
-  if constexpr (S >= 2) v += __shfl_xor(v, 32, kWave);
+  if constexpr (S == 4) v = xor_add<16>(v);
+  if constexpr (S >= 2) v = xor_add<32>(v);
   return v;
 }
 
