@@ -19,9 +19,13 @@
 //    way, and the block's update S += Lx Tx Lx^T, Lx = [block multipliers,
 //    carry], Tx skew tridiagonal (Tx[u,u+1] = alpha_{k0+u+1}, Tx[15,16] = 1),
 //    is applied to the pairs of rows still to be eliminated: each lane forms
-//    its row of Bt = Lx Tx^T, the rows of 16 lanes at a time are spread over
-//    the wave with ds_bpermute, and lane a adds sum_u Lx(a,u) Bt(b,u) to
-//    S(a,b) for every b < a (17 DPP-broadcast FMAs per entry).
+//    its row of Bt = Lx Tx^T, the rows still to be eliminated are listed in
+//    lane order in a small LDS table, 16 of their Bt rows at a time are
+//    spread over the wave with ds_bpermute, and lane a adds
+//    sum_u Lx(a,u) Bt(b,u) to S(a,b) for every listed b < a (17
+//    DPP-broadcast FMAs per entry).  The 16 steps of a block are unrolled:
+//    slot indices are compile-time constants and a step past n-2 simply
+//    changes nothing that is read later.
 // This is the right-looking skew rank-2k update of the method applied every
 // 16 steps inside the wave, with the left-looking refresh confined to the
 // block, so a step's refresh, staging and g formation stay short.
