@@ -84,3 +84,34 @@ def test_fp32_anchored_acceptance(part):
         else:
             with pytest.raises(AssertionError, match="from fp64"):
                 compare_factors(X, S, ipiv, np.float32)
+
+
+def _split_case():
+    """Graded fp32 input on which the fp32 and fp64 oracles choose different
+    pivots at step 377 (a near-tie that rounding decides)."""
+    X = synth.skew_graded(800, 1).astype(np.float32)
+    P32, i32 = oracle.ltlt(X)
+    P64, i64 = oracle.ltlt(X.astype(np.float64))
+    return X, P32, i32, P64, i64
+
+
+def test_fp32_oracle_split_compares_prefix():
+    X, P32, i32, P64, i64 = _split_case()
+    info = compare_factors(X, P32.copy(), i32, np.float32)
+    assert info["oracle_split"] == 378 and info["first_pivot_mismatch"] == 800
+    # the fp64 oracle's factors, rounded, with its own pivots: a near-tie
+    # split at the same step, accepted, prefix within the bars
+    info = compare_factors(X, P64.astype(np.float32), i64, np.float32)
+    assert info["first_pivot_mismatch"] == 378
+
+
+def test_fp32_oracle_split_planted_mistake_fails():
+    X, P32, i32, P64, i64 = _split_case()
+    bad = P32.copy()
+    bad[600, 100] += 1e-2 * np.abs(P32[:, :377]).max()    # a multiplier of step 100, before the split
+    with pytest.raises(AssertionError):
+        compare_factors(X, bad, i32, np.float32)
+    bad = P32.copy()
+    bad[201, 200] *= 1.01                                    # alpha_200
+    with pytest.raises(AssertionError):
+        compare_factors(X, bad, i32, np.float32)
