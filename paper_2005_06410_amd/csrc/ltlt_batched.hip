@@ -164,8 +164,11 @@ __device__ __forceinline__ void update_group(T* orig, int n, int pos, bool ta, i
     if (ok[j]) orig[idx[j]] = a[j];
 }
 
+// Waves per SIMD: fp64 two (the packed triangle takes 17.8 KB of LDS per
+// matrix, and the registers fill 256 VGPRs); fp32 four, by capping it at 128
+// VGPRs (a few values then live in scratch, which still beats three waves).
 template <typename T>
-__global__ void __launch_bounds__(256, 2) batched_kernel(int n, int batch, T* Aall, int64_t lda, int64_t strideA,
+__global__ void __launch_bounds__(256, sizeof(T) == 4 ? 4 : 2) batched_kernel(int n, int batch, T* Aall, int64_t lda, int64_t strideA,
                                                          int* ipiv_all, int64_t strideIpiv, double* logabs,
                                                          int* sign) {
   extern __shared__ __align__(16) unsigned char smem[];
