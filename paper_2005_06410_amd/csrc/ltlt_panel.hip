@@ -176,15 +176,12 @@ __global__ void __launch_bounds__(kPanelThreads, 1) panel_kernel(PanelArgs a) {
     }
     const bool next = my_row && lp >= k + 2;      // rows still to be eliminated
 
-    // ---- one round of loads: next stored column, pivot row multipliers.
-    //      Every lane issues the same number of multiplier loads (addresses
-    //      clamped to steps < t) so that waiting for them is exact. ----
-    if (next && part == 0) {
-      // S(pos, posw) = +A(pos, posw) below the diagonal, -A(posw, pos) above:
-      // element (max, min) of the stored triangle
-      lv = A[(int64_t)max(pos, posw) + (int64_t)min(pos, posw) * lda];
-      lsg = pos > posw ? T(1) : T(-1);
-    }
+    // ---- one round of loads: pivot row multipliers, then the next stored
+    //      column.  Every lane issues the same loads (multiplier addresses
+    //      clamped to steps < t, the stored column's to A(j+1, j) where it
+    //      is not needed), so the in-order memory counter lets g be formed
+    //      from the multipliers while the stored column, a strided row read
+    //      for rows above the pivot, is still in flight. ----
     constexpr int NLQ = TOT / kWave;              // multiplier loads per lane
     T lr[NLQ];
     {
@@ -193,10 +190,22 @@ __global__ void __launch_bounds__(kPanelThreads, 1) panel_kernel(PanelArgs a) {
 #pragma unroll
       for (int q = 0; q < NLQ; ++q) lr[q] = ld_coh_t(&grow[min(q * kWave + lane, umax)]);
     }
+    // S(pos, posw) = +A(pos, posw) below the diagonal, -A(posw, pos) above:
+    // element (max, min) of the stored triangle
+    const bool ldv = next && part == 0;
+    const int64_t lvi = ldv ? (int64_t)max(pos, posw) + (int64_t)min(pos, posw) * lda : (int64_t)(j + 1) + (int64_t)j * lda;
+    const T lvn = A[lvi];
+    __builtin_amdgcn_sched_barrier(0);             // keep the load ahead of the work below
 
-    // ---- multipliers of step k (registers now, G after the loads are used) ----
+    // ---- multiplier of step k; the pivot row's multipliers into LDS before
+    //      the slot write below (a jump), so their wait counts exactly.
+    //      Entries past step t hold clamped copies that g discards; lane 0
+    //      then writes the unit entry over entry t+1. ----
     T l = T(0);
     if (next) l = (alph != T(0)) ? cv / alph : T(0);
+#pragma unroll
+    for (int q = 0; q < NLQ; ++q) my_lrowp[q * kWave + lane + 1] = lr[q];
+    if (lane == 0) { my_alpha[t] = alph; my_lrowp[t + 1] = T(1); }   // Lrow[t] = 1: unit diagonal
     {
       const int c = t / S;
       const bool on = next && part == t % S;
@@ -210,12 +219,6 @@ __global__ void __launch_bounds__(kPanelThreads, 1) panel_kernel(PanelArgs a) {
     }
 
     // ---- g coefficients for step k+1 (t+1 terms), row broadcast layout ----
-#pragma unroll
-    for (int q = 0; q < NLQ; ++q) {
-      const int u = q * kWave + lane;
-      if (u < t) my_lrowp[u + 1] = lr[q];
-    }
-    if (lane == 0) { my_alpha[t] = alph; my_lrowp[t + 1] = T(1); }   // Lrow[t] = 1: unit diagonal
     wave_lds_sync();
     {
       const int c = lane & 15;
@@ -232,6 +235,13 @@ __global__ void __launch_bounds__(kPanelThreads, 1) panel_kernel(PanelArgs a) {
         gr[kk] = (u <= t) ? g : T(0);
       }
     }
+    // the stored column is taken before the stores below are issued, so its
+    // wait does not include their acknowledgement
+    if (ldv) {
+      lv = lvn;
+      lsg = pos > posw ? T(1) : T(-1);
+    }
+    asm volatile("" : "+v"(lv), "+v"(lsg) : : "memory");
     {
       // recompute the row offset here instead of keeping a 64-bit pointer
       // live across the step loop (the kernel runs at the register limit)
