@@ -197,13 +197,16 @@ __global__ void __launch_bounds__(kPanelThreads, 1) cpanel_kernel(CPanelArgs ca)
     }
     const bool next = my_row && lp >= k + 2;
 
-    // ---- one round of loads: next stored column, pivot row multipliers,
-    //      pivot value ----
-    if (next && part == 0) {
-      const int64_t at = (int64_t)max(pos, posw) + (int64_t)min(pos, posw) * lda;
-      lvr = Ar[at];
-      lvi = Ai[at];
-      lsg = pos > posw ? T(1) : T(-1);
+    // ---- one round of loads: pivot value, pivot row multipliers, then the
+    //      next stored column.  Under the in-order memory counter the
+    //      division waits only for the pivot value and the LDS writes below
+    //      only for the multipliers, while the stored column (a strided row
+    //      read for rows above the pivot; every lane loads, at A(j+1, j)
+    //      where it is not needed) is still in flight. ----
+    T alr = T(NAN), ali = T(NAN);
+    if (!none) {
+      alr = ld_coh_t(&Vr[posw - (j + 1)]);
+      ali = ld_coh_t(&Vi[posw - (j + 1)]);
     }
     constexpr int NLQ = (TOT + kWave - 1) / kWave;   // multiplier loads per lane (addresses clamped)
     T lrr[NLQ], lri[NLQ];
@@ -217,16 +220,28 @@ __global__ void __launch_bounds__(kPanelThreads, 1) cpanel_kernel(CPanelArgs ca)
         lri[q] = ld_coh_t(&Gi[at]);
       }
     }
-    T alr = T(NAN), ali = T(NAN);
-    if (!none) {
-      alr = ld_coh_t(&Vr[posw - (j + 1)]);
-      ali = ld_coh_t(&Vi[posw - (j + 1)]);
-    }
+    const bool ldv = next && part == 0;
+    const int64_t lvat =
+        ldv ? (int64_t)max(pos, posw) + (int64_t)min(pos, posw) * lda : (int64_t)(j + 1) + (int64_t)j * lda;
+    const T lvrn = Ar[lvat], lvin = Ai[lvat];
+    __builtin_amdgcn_sched_barrier(0);             // keep the loads ahead of the work below
 
-    // ---- multipliers of step k ----
+    // ---- multipliers of step k; the pivot row's multipliers into LDS before
+    //      the slot write below (a jump), so their wait counts exactly.
+    //      Entries past step t hold clamped copies that g discards; lane 0
+    //      then writes the unit entry over entry t+1. ----
     T lr = T(0), li = T(0);
     if (next) {
       if (alr != T(0) || ali != T(0)) cdiv(cvr, cvi, alr, ali, lr, li);
+    }
+#pragma unroll
+    for (int q = 0; q < NLQ; ++q) {
+      const int u = q * kWave + lane;
+      if (TOT % kWave == 0 || u < TOT) { my_lr[u + 1] = lrr[q]; my_li[u + 1] = lri[q]; }
+    }
+    if (lane == 0) {
+      my_ar[t] = alr; my_ai[t] = ali;
+      my_lr[t + 1] = T(1); my_li[t + 1] = T(0);   // unit diagonal of L
     }
     {
       const int c = t / S;
@@ -242,15 +257,6 @@ __global__ void __launch_bounds__(kPanelThreads, 1) cpanel_kernel(CPanelArgs ca)
 
     // ---- g coefficients for step k+1, row broadcast layout:
     //      g_u = alpha_{u+1} Lrow[u+1] [u <= t-1] - alpha_u Lrow[u-1] [u >= 1] ----
-#pragma unroll
-    for (int q = 0; q < NLQ; ++q) {
-      const int u = q * kWave + lane;
-      if (u < t) { my_lr[u + 1] = lrr[q]; my_li[u + 1] = lri[q]; }
-    }
-    if (lane == 0) {
-      my_ar[t] = alr; my_ai[t] = ali;
-      my_lr[t + 1] = T(1); my_li[t + 1] = T(0);   // unit diagonal of L
-    }
     wave_lds_sync();
     {
       const int c = lane & 15;
@@ -269,6 +275,14 @@ __global__ void __launch_bounds__(kPanelThreads, 1) cpanel_kernel(CPanelArgs ca)
         }
       }
     }
+    // the stored column is taken before the stores below are issued, so its
+    // wait does not include their acknowledgement
+    if (ldv) {
+      lvr = lvrn;
+      lvi = lvin;
+      lsg = pos > posw ? T(1) : T(-1);
+    }
+    asm volatile("" : "+v"(lvr), "+v"(lvi), "+v"(lsg) : : "memory");
     {
       int ro = pos - (j + 1);
       asm volatile("" : "+v"(ro));
